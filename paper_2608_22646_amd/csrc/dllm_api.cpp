@@ -1,0 +1,707 @@
+// Host runtime and C ABI of the dllm library (see include/dllm.h).
+//
+// The runtime validates arguments, carves the caller's workspace into the
+// step's buffers, evaluates the threshold schedule on the host in float64, and
+// enqueues the kernels of one step on the caller's stream:
+//   embed -> n_layers x [norm, qkv+rope, attention, o-proj+residual, norm,
+//   gate/up+swiglu, down+residual] -> final norm of the block rows -> fused LM
+//   head + vocabulary reduction -> commit.
+// dllm_generate runs the semi-autoregressive block loop (Section 4.3) and
+// reads the 4-byte block-finished flag back once per step.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include <string>
+#include <vector>
+
+#include "../../include/dllm.h"
+#include "kernels.h"
+
+using namespace dllm;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+struct ApiError {
+  int code;
+  std::string msg;
+};
+
+[[noreturn]] void fail(int code, const std::string& msg) { throw ApiError{code, msg}; }
+void require(bool ok, int code, const std::string& msg) {
+  if (!ok) fail(code, msg);
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace
+
+struct ProfEvent {
+  int kind;
+  hipEvent_t start, stop;
+};
+
+struct dllm_model {
+  dllm_model_cfg cfg;
+  std::vector<const void*> w;
+  int32_t* pinned_flag = nullptr;
+  bool prof = false;
+  std::vector<ProfEvent> events;
+  size_t n_events = 0;
+};
+
+namespace {
+
+// ---------------------------------------------------------------- layout
+struct Layout {
+  size_t h, a_attn, q, k, vt, attn, a_mlp, u, hb, cosb, sinb;
+  size_t raw, gate, up, logits;                  // fp32 path
+  size_t part_m, part_s, part_i, ticket;         // bf16 head
+  size_t splitk;                                 // bf16 split-K GEMM partials
+  size_t conf, argmax, all_done;                 // step scratch
+  size_t total;
+};
+
+Layout make_layout(const dllm_model_cfg& c, int B, int L, int rows) {
+  const size_t M = (size_t)B * L, d = c.d_model, F = c.d_ff, hd = c.head_dim;
+  const size_t act = c.dtype == DLLM_F32 ? 4 : 2;
+  const size_t R = (size_t)B * rows;
+  Layout o{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  o.h = take(M * d * 4);
+  o.a_attn = take(M * d * act);
+  o.q = take(M * c.n_heads * hd * act);
+  o.k = take(M * c.n_kv_heads * hd * act);
+  o.vt = take(M * c.n_kv_heads * hd * act);     // fp32, or IEEE half for bf16 models
+  o.attn = take(M * c.n_heads * hd * act);
+  o.a_mlp = take(M * d * act);
+  o.u = take(M * F * act);
+  o.hb = take(R * d * act);
+  o.cosb = take((size_t)L * hd / 2 * 4);
+  o.sinb = take((size_t)L * hd / 2 * 4);
+  if (c.dtype == DLLM_F32) {
+    o.raw = take(M * (c.n_heads + 2 * c.n_kv_heads) * hd * 4);
+    o.gate = take(M * F * 4);
+    o.up = take(M * F * 4);
+    o.logits = take(R * c.vocab * 4);
+  } else {
+    const size_t tiles = head_bf16_tiles(c.vocab);
+    o.part_m = take(tiles * R * 4);
+    o.part_s = take(tiles * R * 4);
+    o.part_i = take(tiles * R * 4);
+    o.ticket = take(4);
+    const int qkv_n = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+    const size_t sk = std::max(std::max(gemm_bf16_splitk_bytes((int)M, qkv_n, c.d_model, EPI_QKV_ROPE),
+                                        gemm_bf16_splitk_bytes((int)M, c.d_model, c.n_heads * c.head_dim, EPI_RESID)),
+                               std::max(gemm_bf16_splitk_bytes((int)M, 2 * c.d_ff, c.d_model, EPI_SWIGLU),
+                                        gemm_bf16_splitk_bytes((int)M, c.d_model, c.d_ff, EPI_RESID)));
+    o.splitk = take(sk);
+  }
+  o.conf = take(R * 4);
+  o.argmax = take(R * 4);
+  o.all_done = take(4);
+  o.total = off;
+  return o;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+void check_model(const dllm_model* m) { require(m != nullptr, DLLM_EINVAL, "model is NULL"); }
+
+void check_ws(const dllm_model* m, int B, int L, int rows, void* ws, size_t bytes, Layout* lay) {
+  require(B >= 1 && B <= 16, DLLM_EUNSUPPORTED, "batch must be in [1, 16]");
+  require(L >= 1, DLLM_ESHAPE, "sequence length must be >= 1");
+  require(rows >= 0 && rows <= L, DLLM_ESHAPE, "rows out of range");
+  if (m->cfg.dtype == DLLM_BF16)
+    require((long)B * rows <= head_bf16_max_rows(), DLLM_EUNSUPPORTED, "B * rows exceeds the LM-head kernel limit");
+  else
+    require(L <= 8000, DLLM_EUNSUPPORTED, "float32 attention keeps all scores in LDS: L <= 8000");
+  require(ws != nullptr, DLLM_EINVAL, "workspace is NULL");
+  require(((uintptr_t)ws & 255) == 0, DLLM_EINVAL, "workspace must be 256-byte aligned");
+  *lay = make_layout(m->cfg, B, L, rows);
+  require(bytes >= lay->total, DLLM_ENOMEM, "workspace too small: need " + std::to_string(lay->total) + " bytes");
+}
+
+// ---------------------------------------------------------------- profiling
+struct ProfScope {
+  dllm_model* m;
+  hipStream_t s;
+  ProfEvent* ev = nullptr;
+  ProfScope(const dllm_model* mc, int kind, hipStream_t st) : m(const_cast<dllm_model*>(mc)), s(st) {
+    if (!m->prof) return;
+    if (m->n_events == m->events.size()) {
+      ProfEvent e{};
+      hip_check(hipEventCreate(&e.start), "hipEventCreate");
+      hip_check(hipEventCreate(&e.stop), "hipEventCreate");
+      m->events.push_back(e);
+    }
+    ev = &m->events[m->n_events++];
+    ev->kind = kind;
+    hip_check(hipEventRecord(ev->start, s), "hipEventRecord");
+  }
+  ~ProfScope() {
+    if (ev) (void)hipEventRecord(ev->stop, s);
+  }
+};
+
+enum { PK_GEMM = 0, PK_ATTN = 1, PK_HEAD = 2, PK_COMMIT = 3, PK_NORM = 4, PK_GATEUP = 5 };
+
+const void* W(const dllm_model* m, int i) { return m->w[i]; }
+const bf16_t* Wb(const dllm_model* m, int i) { return static_cast<const bf16_t*>(m->w[i]); }
+const float* Wf(const dllm_model* m, int i) { return static_cast<const float*>(m->w[i]); }
+
+// ---------------------------------------------------------------- forward pieces
+void run_embed(const dllm_model* m, const int32_t* x, int B, int L, void* ws, const Layout& lay, hipStream_t s) {
+  const auto& c = m->cfg;
+  launch_embed(x, W(m, 0), c.dtype, at<float>(ws, lay.h), B * L, c.d_model, s);
+  launch_rope_table(at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), L, c.head_dim, c.rope_base, s);
+}
+
+void gemm_bf16(const dllm_model* m, GemmArgs g, void* ws, const Layout& lay, hipStream_t s, int kind) {
+  g.splitk_buf = at<float>(ws, lay.splitk);
+  ProfScope p(m, kind, s);
+  launch_gemm_bf16(g, s);
+}
+
+void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay,
+                    hipStream_t s) {
+  const auto& c = m->cfg;
+  const int base = 1 + 9 * layer;
+  const int M = B * L, d = c.d_model, hd = c.head_dim;
+  float* h = at<float>(ws, lay.h);
+  if (part == 0 || part == 2) {
+    {
+      ProfScope p(m, PK_NORM, s);
+      launch_rmsnorm(h, W(m, base + 0), at<void>(ws, lay.a_attn), 1, B, L, L, 0, d, c.rms_eps, s);
+    }
+    GemmArgs g{};
+    g.epi = EPI_QKV_ROPE;
+    g.M = M;
+    g.N = (c.n_heads + 2 * c.n_kv_heads) * hd;
+    g.K = d;
+    g.A = at<bf16_t>(ws, lay.a_attn);
+    g.W0 = Wb(m, base + 1);
+    g.W1 = Wb(m, base + 2);
+    g.W2 = Wb(m, base + 3);
+    g.n0 = c.n_heads * hd;
+    g.n1 = c.n_kv_heads * hd;
+    g.q = at<bf16_t>(ws, lay.q);
+    g.k = at<bf16_t>(ws, lay.k);
+    g.vt = at<f16_t>(ws, lay.vt);
+    g.cosb = at<float>(ws, lay.cosb);
+    g.sinb = at<float>(ws, lay.sinb);
+    g.B = B;
+    g.L = L;
+    g.Hq = c.n_heads;
+    g.Hkv = c.n_kv_heads;
+    gemm_bf16(m, g, ws, lay, s, PK_GEMM);
+    {
+      ProfScope p(m, PK_ATTN, s);
+      launch_attn_bf16(g.q, g.k, g.vt, at<bf16_t>(ws, lay.attn), B, L, c.n_heads, c.n_kv_heads, s);
+    }
+    GemmArgs o{};
+    o.epi = EPI_RESID;
+    o.M = M;
+    o.N = d;
+    o.K = c.n_heads * hd;
+    o.A = at<bf16_t>(ws, lay.attn);
+    o.W0 = Wb(m, base + 4);
+    o.n0 = d;
+    o.resid = h;
+    gemm_bf16(m, o, ws, lay, s, PK_GEMM);
+  }
+  if (part == 1 || part == 2) {
+    {
+      ProfScope p(m, PK_NORM, s);
+      launch_rmsnorm(h, W(m, base + 5), at<void>(ws, lay.a_mlp), 1, B, L, L, 0, d, c.rms_eps, s);
+    }
+    GemmArgs g{};
+    g.epi = EPI_SWIGLU;
+    g.M = M;
+    g.N = 2 * c.d_ff;
+    g.K = d;
+    g.A = at<bf16_t>(ws, lay.a_mlp);
+    g.W0 = Wb(m, base + 6);
+    g.W1 = Wb(m, base + 7);
+    g.n0 = c.d_ff;
+    g.n1 = c.d_ff;
+    g.out = at<bf16_t>(ws, lay.u);
+    gemm_bf16(m, g, ws, lay, s, PK_GATEUP);
+    GemmArgs dn{};
+    dn.epi = EPI_RESID;
+    dn.M = M;
+    dn.N = d;
+    dn.K = c.d_ff;
+    dn.A = at<bf16_t>(ws, lay.u);
+    dn.W0 = Wb(m, base + 8);
+    dn.n0 = d;
+    dn.resid = h;
+    gemm_bf16(m, dn, ws, lay, s, PK_GEMM);
+  }
+}
+
+void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay,
+                   hipStream_t s) {
+  const auto& c = m->cfg;
+  const int base = 1 + 9 * layer;
+  const int M = B * L, d = c.d_model, hd = c.head_dim, F = c.d_ff;
+  const int nq = c.n_heads * hd, nkv = c.n_kv_heads * hd, nraw = nq + 2 * nkv;
+  float* h = at<float>(ws, lay.h);
+  if (part == 0 || part == 2) {
+    float* a = at<float>(ws, lay.a_attn);
+    float* raw = at<float>(ws, lay.raw);
+    {
+      ProfScope p(m, PK_NORM, s);
+      launch_rmsnorm(h, W(m, base + 0), a, 0, B, L, L, 0, d, c.rms_eps, s);
+    }
+    {
+      ProfScope p(m, PK_GEMM, s);
+      launch_gemm_f32(a, Wf(m, base + 1), raw, M, nq, d, nraw, false, s);
+      launch_gemm_f32(a, Wf(m, base + 2), raw + nq, M, nkv, d, nraw, false, s);
+      launch_gemm_f32(a, Wf(m, base + 3), raw + nq + nkv, M, nkv, d, nraw, false, s);
+    }
+    launch_rope_split_f32(raw, at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), at<float>(ws, lay.q),
+                          at<float>(ws, lay.k), at<float>(ws, lay.vt), B, L, c.n_heads, c.n_kv_heads, hd, s);
+    {
+      ProfScope p(m, PK_ATTN, s);
+      launch_attn_f32(at<float>(ws, lay.q), at<float>(ws, lay.k), at<float>(ws, lay.vt), at<float>(ws, lay.attn), B,
+                      L, c.n_heads, c.n_kv_heads, hd, s);
+    }
+    ProfScope p(m, PK_GEMM, s);
+    launch_gemm_f32(at<float>(ws, lay.attn), Wf(m, base + 4), h, M, d, nq, d, true, s);
+  }
+  if (part == 1 || part == 2) {
+    float* a = at<float>(ws, lay.a_mlp);
+    {
+      ProfScope p(m, PK_NORM, s);
+      launch_rmsnorm(h, W(m, base + 5), a, 0, B, L, L, 0, d, c.rms_eps, s);
+    }
+    {
+      ProfScope p(m, PK_GATEUP, s);
+      launch_gemm_f32(a, Wf(m, base + 6), at<float>(ws, lay.gate), M, F, d, F, false, s);
+      launch_gemm_f32(a, Wf(m, base + 7), at<float>(ws, lay.up), M, F, d, F, false, s);
+    }
+    launch_swiglu_f32(at<float>(ws, lay.gate), at<float>(ws, lay.up), at<float>(ws, lay.u), (long)M * F, s);
+    ProfScope p(m, PK_GEMM, s);
+    launch_gemm_f32(at<float>(ws, lay.u), Wf(m, base + 8), h, M, d, F, d, true, s);
+  }
+}
+
+void run_layer(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay, hipStream_t s) {
+  if (m->cfg.dtype == DLLM_BF16)
+    run_layer_bf16(m, layer, part, B, L, ws, lay, s);
+  else
+    run_layer_f32(m, layer, part, B, L, ws, lay, s);
+}
+
+void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf, int32_t* argmax, float* logits,
+              void* ws, const Layout& lay, hipStream_t s) {
+  const auto& c = m->cfg;
+  const int nl = c.n_layers;
+  const int R = B * rows;
+  {
+    ProfScope p(m, PK_NORM, s);
+    launch_rmsnorm(at<float>(ws, lay.h), W(m, 1 + 9 * nl), at<void>(ws, lay.hb), c.dtype, B, rows, L, row0,
+                   c.d_model, c.rms_eps, s);
+  }
+  ProfScope p(m, PK_HEAD, s);
+  if (c.dtype == DLLM_F32) {
+    float* lg = logits ? logits : at<float>(ws, lay.logits);
+    launch_gemm_f32(at<float>(ws, lay.hb), Wf(m, 2 + 9 * nl), lg, R, c.vocab, c.d_model, c.vocab, false, s);
+    launch_vocab_reduce_f32(lg, R, c.vocab, c.mask_id, conf, argmax, s);
+  } else {
+    HeadArgs a{};
+    a.hb = at<bf16_t>(ws, lay.hb);
+    a.W = Wb(m, 2 + 9 * nl);
+    a.R = R;
+    a.V = c.vocab;
+    a.d = c.d_model;
+    a.mask_id = c.mask_id;
+    a.conf = conf;
+    a.argmax = argmax;
+    a.logits = logits;
+    a.part_m = at<float>(ws, lay.part_m);
+    a.part_s = at<float>(ws, lay.part_s);
+    a.part_i = at<int32_t>(ws, lay.part_i);
+    a.ticket = at<int>(ws, lay.ticket);
+    // the kernel's last workgroup resets the ticket; clearing it here as well
+    // makes a fresh (uninitialised) workspace safe
+    hip_check(hipMemsetAsync(a.ticket, 0, sizeof(int), s), "hipMemsetAsync");
+    launch_head_bf16(a, s);
+  }
+}
+
+// ---------------------------------------------------------------- controller
+void check_params(const dllm_cai_params* p) {
+  require(p != nullptr, DLLM_EINVAL, "params is NULL");
+  require(p->block_len >= 1 && p->block_len <= 64, DLLM_EUNSUPPORTED, "block_len must be in [1, 64]");
+  require(p->steps_per_block >= 0, DLLM_EINVAL, "steps_per_block must be >= 0");
+  const double dv[] = {p->theta_s, p->theta_e, p->theta_e_step, p->theta_e_floor, p->warmup, p->clip_lo,
+                       p->clip_hi, p->eta_bar, p->pos_factor[0], p->pos_factor[1], p->pos_factor[2],
+                       p->pos_factor[3]};
+  for (double v : dv) require(std::isfinite(v), DLLM_EINVAL, "non-finite controller constant");
+  const float fv[] = {p->s_easy, p->s_hard, p->theta_fb};
+  for (float v : fv) require(std::isfinite(v), DLLM_EINVAL, "non-finite controller constant");
+  require(p->warmup >= 0.0 && p->warmup < 1.0, DLLM_EINVAL, "warmup must be in [0, 1)");
+  require(p->clip_lo <= p->clip_hi, DLLM_EINVAL, "clip_lo > clip_hi");
+  require(p->patience >= 1, DLLM_EINVAL, "patience must be >= 1");
+  require(p->pos_edge[0] <= p->pos_edge[1] && p->pos_edge[1] <= p->pos_edge[2], DLLM_EINVAL,
+          "pos_edge must be non-decreasing");
+}
+
+int steps_T(const dllm_cai_params* p) { return p->steps_per_block > 0 ? p->steps_per_block : p->block_len; }
+
+// theta_b(t) in float64 (Boxes 3 and 4), b 1-based.
+double block_threshold(const dllm_cai_params* p, int b, int t) {
+  const int T = steps_T(p);
+  const double wT = p->warmup * T;
+  if ((double)t < wT) return p->theta_s;
+  double te = p->theta_e;
+  if (p->flags & DLLM_F_BLOCK_SCHED) te = std::max(p->theta_e - p->theta_e_step * (b - 1), p->theta_e_floor);
+  const double u = ((double)t - wT) / ((double)T - wT);
+  return te + 0.5 * (p->theta_s - te) * (1.0 + cos(M_PI * u));
+}
+
+void fill_commit_args(const dllm_cai_params* p, dllm_state* st, CommitArgs* a, int B, int P, int G, int block, int t,
+                      int mask_id) {
+  require(st && st->x && st->commit_step && st->reason && st->s && st->budget && st->ell && st->done, DLLM_EINVAL,
+          "state has a NULL member");
+  require(B >= 1 && B <= 16, DLLM_EUNSUPPORTED, "batch must be in [1, 16]");
+  require(G >= 1 && G % p->block_len == 0, DLLM_ESHAPE, "G must be a positive multiple of block_len");
+  require(P >= 0, DLLM_ESHAPE, "P must be >= 0");
+  require(block >= 0 && block < G / p->block_len, DLLM_ESHAPE, "block index out of range");
+  const int T = steps_T(p);
+  require(t >= 0 && t < T, DLLM_ESHAPE, "step index out of range");
+  a->x = st->x;
+  a->commit_step = st->commit_step;
+  a->reason = st->reason;
+  a->sv = st->s;
+  a->budget = st->budget;
+  a->ell = st->ell;
+  a->done = st->done;
+  a->B = B;
+  a->L = P + G;
+  a->P = P;
+  a->G = G;
+  a->bl = p->block_len;
+  a->g0 = block * p->block_len;
+  a->t = t;
+  a->T = T;
+  a->mask_id = mask_id;
+  const double tb = block_threshold(p, block + 1, t);
+  for (int band = 0; band < 4; ++band) {
+    double th = tb;
+    if (p->flags & DLLM_F_POS) th = std::min(std::max(tb * p->pos_factor[band], p->clip_lo), p->clip_hi);
+    a->thr[band] = (float)th;
+  }
+  for (int i = 0; i < 3; ++i) a->edge[i] = p->pos_edge[i];
+  a->budget_on = (p->flags & DLLM_F_BUDGET) ? 1 : 0;
+  a->grind_on = (p->flags & DLLM_F_GRIND) ? 1 : 0;
+  a->s_easy = p->s_easy;
+  a->s_hard = p->s_hard;
+  a->p_easy = p->p_easy;
+  a->p_hard = p->p_hard;
+  a->b_easy = p->budget_easy;
+  a->b_mid = p->budget_mid;
+  a->b_hard = p->budget_hard;
+  a->eta_bar = p->eta_bar;
+  a->patience = p->patience;
+  a->theta_fb = p->theta_fb;
+}
+
+void forward_all(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, float* conf,
+                 int32_t* argmax, float* logits, void* ws, const Layout& lay, hipStream_t s) {
+  {
+    ProfScope p(m, PK_NORM, s);
+    run_embed(m, x, B, L, ws, lay, s);
+  }
+  for (int l = 0; l < m->cfg.n_layers; ++l) run_layer(m, l, 2, B, L, ws, lay, s);
+  run_head(m, B, L, row0, rows, conf, argmax, logits, ws, lay, s);
+}
+
+int finish(const ApiError& e) {
+  g_last_error = e.msg;
+  return e.code;
+}
+
+}  // namespace
+
+#define API_BEGIN \
+  g_last_error.clear(); \
+  try {
+#define API_END                                   \
+  }                                               \
+  catch (const ApiError& e) {                     \
+    return finish(e);                             \
+  }                                               \
+  catch (const HipError& e) {                     \
+    g_last_error = e.what();                      \
+    return DLLM_EHIP;                             \
+  }                                               \
+  catch (const std::exception& e) {               \
+    g_last_error = e.what();                      \
+    return DLLM_EINVAL;                           \
+  }                                               \
+  return DLLM_OK;
+
+extern "C" {
+
+const char* dllm_last_error(void) { return g_last_error.c_str(); }
+
+int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int32_t n_weights, dllm_model** out) {
+  API_BEGIN
+  require(cfg && weights && out, DLLM_EINVAL, "NULL argument");
+  const auto& c = *cfg;
+  require(c.n_layers >= 0 && c.d_model > 0 && c.n_heads > 0 && c.n_kv_heads > 0 && c.head_dim > 0 && c.d_ff > 0 &&
+              c.vocab > 1,
+          DLLM_EINVAL, "model dimensions must be positive");
+  require(c.n_heads % c.n_kv_heads == 0, DLLM_EINVAL, "n_heads must be a multiple of n_kv_heads");
+  require(c.mask_id >= 0 && c.mask_id < c.vocab, DLLM_EINVAL, "mask_id out of range");
+  require(std::isfinite(c.rms_eps) && c.rms_eps > 0 && std::isfinite(c.rope_base) && c.rope_base > 0, DLLM_EINVAL,
+          "rms_eps and rope_base must be positive");
+  require(c.dtype == DLLM_F32 || c.dtype == DLLM_BF16, DLLM_EINVAL, "dtype must be DLLM_F32 or DLLM_BF16");
+  if (c.dtype == DLLM_BF16)
+    require(c.head_dim == 128 && c.d_model % 256 == 0 && c.d_ff % 128 == 0 && c.n_heads % 2 == 0 &&
+                c.n_kv_heads % 2 == 0,
+            DLLM_EUNSUPPORTED,
+            "bf16 path needs head_dim 128, d_model % 256 == 0, d_ff % 128 == 0, even head counts");
+  else
+    require((c.head_dim == 64 || c.head_dim == 128), DLLM_EUNSUPPORTED, "fp32 path needs head_dim 64 or 128");
+  require(n_weights == 3 + 9 * c.n_layers, DLLM_EINVAL, "n_weights must be 3 + 9 * n_layers");
+  for (int i = 0; i < n_weights; ++i) require(weights[i] != nullptr, DLLM_EINVAL, "NULL weight pointer");
+  auto* m = new dllm_model();
+  m->cfg = c;
+  m->w.assign(weights, weights + n_weights);
+  hipError_t e = hipHostMalloc((void**)&m->pinned_flag, sizeof(int32_t), hipHostMallocDefault);
+  if (e != hipSuccess) {
+    delete m;
+    hip_check(e, "hipHostMalloc");
+  }
+  *out = m;
+  API_END
+}
+
+int dllm_model_destroy(dllm_model* m) {
+  API_BEGIN
+  if (!m) return DLLM_OK;
+  for (auto& e : m->events) {
+    (void)hipEventDestroy(e.start);
+    (void)hipEventDestroy(e.stop);
+  }
+  if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
+  delete m;
+  API_END
+}
+
+int dllm_workspace_size(const dllm_model* m, int32_t B, int32_t L, int32_t rows, size_t* bytes) {
+  API_BEGIN
+  check_model(m);
+  require(bytes != nullptr, DLLM_EINVAL, "bytes is NULL");
+  require(B >= 1 && L >= 1 && rows >= 0 && rows <= L, DLLM_ESHAPE, "bad sizes");
+  *bytes = make_layout(m->cfg, B, L, rows).total;
+  API_END
+}
+
+int dllm_workspace_layout(const dllm_model* m, int32_t B, int32_t L, int32_t rows, dllm_ws_layout* out) {
+  API_BEGIN
+  check_model(m);
+  require(out != nullptr, DLLM_EINVAL, "out is NULL");
+  require(B >= 1 && L >= 1 && rows >= 0 && rows <= L, DLLM_ESHAPE, "bad sizes");
+  const Layout l = make_layout(m->cfg, B, L, rows);
+  out->total = l.total;
+  out->h = l.h;
+  out->a_attn = l.a_attn;
+  out->q = l.q;
+  out->k = l.k;
+  out->vt = l.vt;
+  out->attn = l.attn;
+  out->a_mlp = l.a_mlp;
+  out->u = l.u;
+  out->hb = l.hb;
+  API_END
+}
+
+int dllm_embed(const dllm_model* m, const int32_t* x, int32_t B, int32_t L, void* ws, size_t ws_bytes,
+               void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(x != nullptr, DLLM_EINVAL, "x is NULL");
+  Layout lay;
+  check_ws(m, B, L, 0, ws, ws_bytes, &lay);
+  run_embed(m, x, B, L, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_layer(const dllm_model* m, int32_t layer, int32_t part, int32_t B, int32_t L, void* ws, size_t ws_bytes,
+               void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(layer >= 0 && layer < m->cfg.n_layers, DLLM_EINVAL, "layer out of range");
+  require(part >= 0 && part <= 2, DLLM_EINVAL, "part must be 0, 1 or 2");
+  Layout lay;
+  check_ws(m, B, L, 0, ws, ws_bytes, &lay);
+  run_layer(m, layer, part, B, L, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_head(const dllm_model* m, int32_t B, int32_t L, int32_t row0, int32_t rows, float* conf, int32_t* argmax,
+              float* logits, void* ws, size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(conf && argmax, DLLM_EINVAL, "conf/argmax is NULL");
+  require(row0 >= 0 && rows >= 1 && row0 + rows <= L, DLLM_ESHAPE, "rows out of range");
+  Layout lay;
+  check_ws(m, B, L, rows, ws, ws_bytes, &lay);
+  run_head(m, B, L, row0, rows, conf, argmax, logits, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_forward(const dllm_model* m, const int32_t* x, int32_t B, int32_t L, int32_t row0, int32_t rows,
+                 float* conf, int32_t* argmax, float* logits, void* ws, size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(x && conf && argmax, DLLM_EINVAL, "NULL argument");
+  require(row0 >= 0 && rows >= 1 && row0 + rows <= L, DLLM_ESHAPE, "rows out of range");
+  Layout lay;
+  check_ws(m, B, L, rows, ws, ws_bytes, &lay);
+  forward_all(m, x, B, L, row0, rows, conf, argmax, logits, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_state_init(int32_t mask_id, const int32_t* prompt, int32_t B, int32_t P, int32_t G, dllm_state* st,
+                    void* stream) {
+  API_BEGIN
+  require(mask_id >= 0, DLLM_EINVAL, "mask_id must be >= 0");
+  require(st && st->x && st->commit_step && st->reason && st->s && st->budget && st->ell && st->done, DLLM_EINVAL,
+          "state has a NULL member");
+  require(B >= 1 && B <= 16 && P >= 0 && G >= 1, DLLM_ESHAPE, "bad sizes");
+  require(P == 0 || prompt != nullptr, DLLM_EINVAL, "prompt is NULL");
+  launch_state_init(prompt, st->x, st->commit_step, st->reason, st->s, st->budget, st->ell, st->done, B, P, G,
+                    mask_id, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_commit(const dllm_cai_params* p, dllm_state* st, const float* conf, const int32_t* argmax, int32_t B,
+                int32_t P, int32_t G, int32_t block, int32_t t, int32_t mask_id, int32_t* all_done, void* stream) {
+  API_BEGIN
+  check_params(p);
+  require(conf && argmax, DLLM_EINVAL, "conf/argmax is NULL");
+  CommitArgs a{};
+  fill_commit_args(p, st, &a, B, P, G, block, t, mask_id);
+  a.conf = conf;
+  a.argmax = argmax;
+  a.all_done = all_done;
+  launch_commit(a, (hipStream_t)stream);
+  API_END
+}
+
+namespace {
+void step_impl(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int B, int P, int G, int block, int t,
+               float* conf_out, int32_t* argmax_out, void* ws, const Layout& lay, hipStream_t s) {
+  CommitArgs a{};
+  fill_commit_args(p, st, &a, B, P, G, block, t, m->cfg.mask_id);
+  const int bl = p->block_len;
+  float* conf = conf_out ? conf_out : at<float>(ws, lay.conf);
+  int32_t* arg = argmax_out ? argmax_out : at<int32_t>(ws, lay.argmax);
+  forward_all(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, ws, lay, s);
+  a.conf = conf;
+  a.argmax = arg;
+  a.all_done = at<int32_t>(ws, lay.all_done);
+  ProfScope pr(m, PK_COMMIT, s);
+  launch_commit(a, s);
+}
+}  // namespace
+
+int dllm_step(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int32_t B, int32_t P, int32_t G,
+              int32_t block, int32_t t, float* conf_out, int32_t* argmax_out, int32_t* all_done_host, void* ws,
+              size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  check_params(p);
+  Layout lay;
+  check_ws(m, B, P + G, p->block_len, ws, ws_bytes, &lay);
+  hipStream_t s = (hipStream_t)stream;
+  step_impl(m, p, st, B, P, G, block, t, conf_out, argmax_out, ws, lay, s);
+  if (all_done_host) {
+    hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
+              "hipMemcpyAsync");
+    hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
+    *all_done_host = *m->pinned_flag;
+  }
+  API_END
+}
+
+int dllm_generate(const dllm_model* m, const dllm_cai_params* p, const int32_t* prompt, int32_t B, int32_t P,
+                  int32_t G, dllm_state* st, int32_t* forwards_host, int32_t* total_forwards, float* conf_trace,
+                  int32_t* argmax_trace, void* ws, size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  check_params(p);
+  require(G >= 1 && G % p->block_len == 0, DLLM_ESHAPE, "G must be a positive multiple of block_len");
+  require(P >= 0 && (P == 0 || prompt), DLLM_EINVAL, "bad prompt");
+  Layout lay;
+  check_ws(m, B, P + G, p->block_len, ws, ws_bytes, &lay);
+  hipStream_t s = (hipStream_t)stream;
+  const int bl = p->block_len, nb = G / bl, T = steps_T(p);
+  launch_state_init(prompt, st->x, st->commit_step, st->reason, st->s, st->budget, st->ell, st->done, B, P, G,
+                    m->cfg.mask_id, s);
+  int total = 0;
+  for (int blk = 0; blk < nb; ++blk) {
+    int n = 0;
+    for (int t = 0; t < T; ++t) {
+      float* ct = conf_trace ? conf_trace + ((size_t)blk * T + t) * B * bl : nullptr;
+      int32_t* at_ = argmax_trace ? argmax_trace + ((size_t)blk * T + t) * B * bl : nullptr;
+      step_impl(m, p, st, B, P, G, blk, t, ct, at_, ws, lay, s);
+      ++n;
+      hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
+                "hipMemcpyAsync");
+      hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
+      if (*m->pinned_flag) break;
+    }
+    if (forwards_host) forwards_host[blk] = n;
+    total += n;
+  }
+  if (total_forwards) *total_forwards = total;
+  API_END
+}
+
+int dllm_prof_enable(dllm_model* m, int32_t enable) {
+  API_BEGIN
+  check_model(m);
+  m->prof = enable != 0;
+  m->n_events = 0;
+  API_END
+}
+
+int dllm_prof_read(dllm_model* m, int32_t kind, double* total_ms, int64_t* launches) {
+  API_BEGIN
+  check_model(m);
+  require(total_ms && launches, DLLM_EINVAL, "NULL argument");
+  double tot = 0;
+  int64_t n = 0;
+  for (size_t i = 0; i < m->n_events; ++i) {
+    const ProfEvent& e = m->events[i];
+    if (e.kind != kind) continue;
+    hip_check(hipEventSynchronize(e.stop), "hipEventSynchronize");
+    float ms = 0;
+    hip_check(hipEventElapsedTime(&ms, e.start, e.stop), "hipEventElapsedTime");
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  API_END
+}
+
+}  // extern "C"

@@ -1,0 +1,200 @@
+// Non-causal multi-head attention with grouped KV heads, bf16 operands on
+// CDNA4 matrix cores, float32 online softmax.
+//
+//   out[b, l, h*128 + j] = sum_k softmax_k(q[b,h,l,:] . k[b,g(h),k,:] / sqrt(128)) v[b,g(h),k,j]
+//
+// Every query attends to every key (no mask); g(h) = h / (Hq / Hkv).
+// Workgroup = 4 wavefronts = 128 queries of one (sequence, head); wave w owns
+// 32 queries.  Keys stream through LDS in tiles of 64 (K [64][128] and
+// V^T [128][64], double buffered).  Per tile a wave computes
+//   S^T (64 keys x 32 queries) = K . Q^T      (16 MFMAs, Q held in registers)
+// so that each lane holds scores of a single query: the row max needs one
+// cross-lane exchange (lane ^ 32) and the rescale factor is per lane.  Then
+//   O^T (128 x 32) += V^T . P^T               (16 MFMAs)
+// in IEEE half: P in [0, 1] rounded to half (11-bit significand, 8x finer than
+// bf16) and V^T holding the bf16 values of v, which half represents exactly in
+// its range.  The key order inside each 16-key MFMA slice is permuted to match
+// where the scores already sit in the S^T registers; V^T is read with the same
+// permutation.
+#include "kernels.h"
+
+namespace dllm {
+
+namespace {
+
+constexpr int HD = 128, KT = 64, QW = 32, NW = 4;
+constexpr int K_BYTES = KT * HD * 2, V_BYTES = HD * KT * 2, STAGE = K_BYTES + V_BYTES;
+
+__device__ __forceinline__ int k_off(int key, int chunk) {  // rows of 256 B, 16 chunks
+  return key * 256 + ((chunk ^ (key & 7)) << 4);
+}
+__device__ __forceinline__ int v_off(int d, int chunk) {  // rows of 128 B, 8 chunks
+  return K_BYTES + d * 128 + ((chunk ^ (d & 7)) << 4);
+}
+
+__global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
+                                                           const f16_t* __restrict__ vt, bf16_t* __restrict__ out,
+                                                           int L, int Hq, int Hkv) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
+  const int q0 = blockIdx.x * (QW * NW) + wave * QW;
+  const int lq = lane & 31, half = lane >> 5;
+  const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
+  const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
+
+  // Q as the B operand: lane holds query q0 + lq, dims 16*ks + 8*half .. +7.
+  bf16x8_t qf[8];
+  {
+    const int qi = q0 + lq;
+    const bf16_t* qrow = q + (((size_t)b * Hq + h) * L + (qi < L ? qi : 0)) * HD;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16 + half * 8);
+      if (qi >= L) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+  }
+
+  // tile loader: 4 x 16 B of K and 4 x 16 B of V^T per thread
+  uint4 rk[4], rv[4];
+  auto gload = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = tid + 256 * i;
+      const int key = e >> 4, ch = e & 15;  // K: 64 rows x 16 chunks
+      const int gk = t0 + key;
+      rk[i] = gk < L ? *reinterpret_cast<const uint4*>(kh + (size_t)gk * HD + ch * 8) : make_uint4(0, 0, 0, 0);
+      const int d = e >> 3, vc = e & 7;     // V^T: 128 rows x 8 chunks
+      const int gv = t0 + vc * 8;
+      if ((L & 7) == 0 && gv + 8 <= L) {
+        rv[i] = *reinterpret_cast<const uint4*>(vh + (size_t)d * L + gv);
+      } else {
+        uint16_t tmp[8];
+        for (int x = 0; x < 8; ++x) tmp[x] = (gv + x < L) ? vh[(size_t)d * L + gv + x] : (uint16_t)0;
+        rv[i] = *reinterpret_cast<uint4*>(tmp);
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+    char* base = lds + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = tid + 256 * i;
+      *reinterpret_cast<uint4*>(base + k_off(e >> 4, e & 15)) = rk[i];
+      *reinterpret_cast<uint4*>(base + v_off(e >> 3, e & 7)) = rv[i];
+    }
+  };
+
+  f32x16_t o[4];
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ds][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float sc = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
+
+  const int ntiles = (L + KT - 1) / KT;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntiles) gload((t + 1) * KT);
+    const char* base = lds + buf * STAGE;
+
+    // S^T = K . Q^T for keys 32*st + (rows), queries = lanes
+    f32x16_t s[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[st][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + lq, ks * 2 + half));
+        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[st], 0, 0, 0);
+      }
+    }
+    // scale into the log2 domain, mask keys past L, tile max
+    const int t0 = t * KT;
+    float mt = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = t0 + st * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const float x = key < L ? s[st][r] * sc : -INFINITY;
+        s[st][r] = x;
+        mt = fmaxf(mt, x);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(s[st][r] - m_new);
+        s[st][r] = p;
+        psum += p;
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[ds][r] *= alpha;
+
+    // O^T += V^T . P^T over four 16-key slices
+#pragma unroll
+    for (int jk = 0; jk < 4; ++jk) {
+      f16x8_t pf;
+      const int st = jk >> 1, r0 = (jk & 1) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s[st][r0 + e];
+      // slots 0-3: keys 16jk + 4*half + [0,4); slots 4-7: keys 16jk + 8 + 4*half + [0,4)
+      const int kA = jk * 16 + 4 * half, kB = kA + 8;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) {
+        const int d = ds * 32 + lq;
+        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kA >> 3) + (kA & 7) * 2);
+        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kB >> 3) + (kB & 7) * 2);
+        const f16x8_t vf = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
+        o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
+      }
+    }
+    if (t + 1 < ntiles) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  const int qi = q0 + lq;
+  if (qi >= L) return;
+  bf16_t* orow = out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      const int d = ds * 32 + 8 * rg + 4 * half;
+      uint2 w;
+      w.x = pack_bf16x2(o[ds][rg * 4 + 0] * inv, o[ds][rg * 4 + 1] * inv);
+      w.y = pack_bf16x2(o[ds][rg * 4 + 2] * inv, o[ds][rg * 4 + 3] * inv);
+      *reinterpret_cast<uint2*>(orow + d) = w;
+    }
+}
+
+}  // namespace
+
+void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int L, int Hq, int Hkv,
+                      hipStream_t s) {
+  if (B * L == 0) return;
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)attn_bf16_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * STAGE);
+  hip_check(attr, "hipFuncSetAttribute(attn_bf16)");
+  hipLaunchKernelGGL(attn_bf16_kernel, dim3(ceil_div(L, QW * NW), Hq, B), dim3(256), 2 * STAGE, s, q, k, vt, out, L,
+                     Hq, Hkv);
+  DLLM_LAUNCH_CHECK("attn_bf16");
+}
+
+}  // namespace dllm

@@ -1,0 +1,90 @@
+// Confidence-aware commit for one denoising step (Algorithm 1's body, Boxes 2-7).
+//
+// One workgroup; wavefront b handles sequence b and lane p handles in-block
+// position p (block length <= 64), so every state entry has a single writer
+// and the per-step count eta is a ballot + popcount.  Order inside the step:
+// threshold / budget commits, eta, low-yield counter, grinding fallback,
+// no-mask check, flush of what is still masked when the block ends.
+#include "kernels.h"
+
+namespace dllm {
+
+__global__ void __launch_bounds__(1024) commit_kernel(CommitArgs a) {
+  const int b = threadIdx.x >> 6;
+  const int p = threadIdx.x & 63;
+  __shared__ int fin[16];
+  int finished = 1;
+  if (b < a.B) {
+    int ell = a.ell[b];
+    int dn = a.done[b];
+    if (a.t == 0) {  // step-zero init of the block
+      ell = 0;
+      dn = 0;
+    }
+    if (!dn) {
+      const bool lane_on = p < a.bl;
+      const int g = a.g0 + p;
+      const size_t sg = (size_t)b * a.G + g;
+      bool masked = false;
+      float c = 0.f;
+      int tok = 0, bud = 0;
+      if (lane_on) {
+        masked = a.commit_step[sg] < 0;
+        c = a.conf[(size_t)b * a.bl + p];
+        tok = a.argmax[(size_t)b * a.bl + p];
+        if (a.t == 0) {  // Box 2 (s_i = c_i^(0)) and Box 5 (budget tiers, top to bottom)
+          if (c > a.s_easy && p < a.p_easy) bud = a.b_easy;
+          else if (c < a.s_hard || p >= a.p_hard) bud = a.b_hard;
+          else bud = a.b_mid;
+          a.sv[sg] = c;
+          a.budget[sg] = bud;
+        } else {
+          bud = a.budget[sg];
+        }
+      }
+      const int band = (p >= a.edge[0]) + (p >= a.edge[1]) + (p >= a.edge[2]);
+      const bool by_thr = masked && (c >= a.thr[band]);                         // Box 6 rule
+      const bool by_bud = masked && !by_thr && a.budget_on && (a.t >= bud);   // Box 5 force
+      const bool newly = by_thr || by_bud;
+      const int eta = __popcll(__ballot(newly));
+      ell = ((double)eta < a.eta_bar) ? ell + 1 : 0;                          // Box 7 counter
+      bool exit = false, forced = false;
+      if (a.grind_on && ell >= a.patience) {                                  // grinding fallback
+        forced = masked && !newly && (c > a.theta_fb);
+        exit = true;
+      }
+      const bool remaining = masked && !newly && !forced;
+      if (__ballot(remaining) == 0ull) exit = true;
+      bool flush = false;
+      if (exit || a.t == a.T - 1) {
+        flush = remaining;
+        exit = true;
+      }
+      const int why = by_thr ? 1 : by_bud ? 2 : forced ? 3 : flush ? 4 : 0;
+      if (why) {
+        a.x[(size_t)b * a.L + a.P + g] = tok;
+        a.commit_step[sg] = a.t;
+        a.reason[sg] = (int8_t)why;
+      }
+      if (p == 0) {
+        a.ell[b] = ell;
+        a.done[b] = exit ? 1 : 0;
+      }
+      finished = exit ? 1 : 0;
+    }
+  }
+  if (p == 0 && b < 16) fin[b] = finished;
+  __syncthreads();
+  if (threadIdx.x == 0 && a.all_done) {
+    int all = 1;
+    for (int i = 0; i < a.B; ++i) all &= fin[i];
+    *a.all_done = all;
+  }
+}
+
+void launch_commit(const CommitArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(commit_kernel, dim3(1), dim3(64 * a.B), 0, s, a);
+  DLLM_LAUNCH_CHECK("commit");
+}
+
+}  // namespace dllm

@@ -1,0 +1,115 @@
+// Embedding gather, RoPE table, RMSNorm and decoding-state initialisation.
+#include "kernels.h"
+
+namespace dllm {
+
+// One 256-thread block per row; every thread converts a strided set of columns.
+template <typename T>
+__global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ x, const T* __restrict__ E,
+                                                    float* __restrict__ h, int d) {
+  const int m = blockIdx.x;
+  const size_t src = (size_t)x[m] * d;
+  float* dst = h + (size_t)m * d;
+  for (int c = threadIdx.x; c < d; c += 256) dst[c] = Act<T>::load(E, src + c);
+}
+
+void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int M, int d, hipStream_t s) {
+  if (M == 0) return;
+  if (dtype == 0)
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, x, (const float*)E, h, d);
+  else
+    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(M), dim3(256), 0, s, x, (const bf16_t*)E, h, d);
+  DLLM_LAUNCH_CHECK("embed");
+}
+
+// angle = pos * base^(-2j/hd) in float64 (positions reach 8k, where a float32
+// angle would already be off by ~1e-3 rad), stored as float32 cos/sin.
+__global__ void rope_table_kernel(float* cosb, float* sinb, int L, int half, double base, int hd) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= L * half) return;
+  const int pos = i / half, j = i % half;
+  const double inv_freq = pow(base, -2.0 * (double)j / (double)hd);
+  double sn, cs;
+  sincos((double)pos * inv_freq, &sn, &cs);
+  cosb[i] = (float)cs;
+  sinb[i] = (float)sn;
+}
+
+void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, hipStream_t s) {
+  const int n = L * (hd / 2);
+  if (n == 0) return;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, cosb, sinb, L, hd / 2, base, hd);
+  DLLM_LAUNCH_CHECK("rope_table");
+}
+
+// RMSNorm of one row per 256-thread block.  The sum of squares is accumulated
+// in float64 in a fixed order (per-thread strided sums, then a fixed tree), so
+// results are run-to-run identical; scaling and the gain are applied in float32.
+template <typename TG, typename TO>
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ h, const TG* __restrict__ g,
+                                                      TO* __restrict__ out, int rows, int L, int row0, int d,
+                                                      float eps) {
+  const int r = blockIdx.x;
+  const int b = r / rows, i = r % rows;
+  const float* src = h + ((size_t)b * L + row0 + i) * d;
+  double ss = 0.0;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    const double v = src[c];
+    ss += v * v;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  __shared__ double part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const double tot = (part[0] + part[1]) + (part[2] + part[3]);
+  const float rstd = (float)(1.0 / sqrt(tot / (double)d + (double)eps));
+  TO* dst = out + (size_t)r * d;
+  for (int c = threadIdx.x; c < d; c += 256) Act<TO>::store(dst, c, src[c] * rstd * Act<TG>::load(g, c));
+}
+
+void launch_rmsnorm(const float* h, const void* g, void* out, int dtype, int B, int rows, int L, int row0, int d,
+                    float eps, hipStream_t s) {
+  if (B * rows == 0) return;
+  if (dtype == 0)
+    hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(B * rows), dim3(256), 0, s, h, (const float*)g,
+                       (float*)out, rows, L, row0, d, eps);
+  else
+    hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t>), dim3(B * rows), dim3(256), 0, s, h, (const bf16_t*)g,
+                       (bf16_t*)out, rows, L, row0, d, eps);
+  DLLM_LAUNCH_CHECK("rmsnorm");
+}
+
+__global__ void state_init_kernel(const int32_t* __restrict__ prompt, int32_t* __restrict__ x,
+                                  int32_t* __restrict__ commit_step, int8_t* __restrict__ reason,
+                                  float* __restrict__ sv, int32_t* __restrict__ budget, int32_t* __restrict__ ell,
+                                  int32_t* __restrict__ done, int B, int P, int G, int mask_id) {
+  const int L = P + G;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < B * L) {
+    const int b = i / L, l = i % L;
+    x[i] = l < P ? prompt[(size_t)b * P + l] : mask_id;
+  }
+  if (i < B * G) {
+    commit_step[i] = -1;
+    reason[i] = 0;
+    sv[i] = 0.f;
+    budget[i] = 0;
+  }
+  if (i < B) {
+    ell[i] = 0;
+    done[i] = 0;
+  }
+}
+
+void launch_state_init(const int32_t* prompt, int32_t* x, int32_t* commit_step, int8_t* reason, float* sv,
+                       int32_t* budget, int32_t* ell, int32_t* done, int B, int P, int G, int mask_id,
+                       hipStream_t s) {
+  const int n = B * (P + G);
+  if (n == 0) return;
+  hipLaunchKernelGGL(state_init_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, prompt, x, commit_step, reason,
+                     sv, budget, ell, done, B, P, G, mask_id);
+  DLLM_LAUNCH_CHECK("state_init");
+}
+
+}  // namespace dllm

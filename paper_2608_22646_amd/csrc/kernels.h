@@ -1,0 +1,88 @@
+// Internal launchers of the dllm HIP kernels (not part of the C ABI).
+#pragma once
+#include "common.h"
+
+namespace dllm {
+
+// ---- k_misc.hip ------------------------------------------------------------
+// h[m, :] = float(E[x[m], :]) for m < M.
+void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int M, int d, hipStream_t s);
+// cos/sin [L, hd/2] of pos * base^(-2j/hd), evaluated in float64, stored float32.
+void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, hipStream_t s);
+// out[b*rows + i, :] = act(RMSNorm(h[b*L + row0 + i, :]) * g) for b < B, i < rows.
+void launch_rmsnorm(const float* h, const void* g, void* out, int dtype, int B, int rows, int L, int row0,
+                    int d, float eps, hipStream_t s);
+// Decoding state initialisation (see dllm_state_init).
+void launch_state_init(const int32_t* prompt, int32_t* x, int32_t* commit_step, int8_t* reason, float* sv,
+                       int32_t* budget, int32_t* ell, int32_t* done, int B, int P, int G, int mask_id,
+                       hipStream_t s);
+
+// ---- fp32 path (k_f32.hip) -------------------------------------------------
+// C[M, N] (+)= A[M, K] W[N, K]^T, all float32 row-major, C row stride ldc.
+void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc, bool accumulate,
+                     hipStream_t s);
+// Split raw projections [B*L, (Hq + 2 Hkv) hd] into q/k (RoPE applied) and v^T.
+void launch_rope_split_f32(const float* raw, const float* cosb, const float* sinb, float* q, float* k,
+                           float* vt, int B, int L, int Hq, int Hkv, int hd, hipStream_t s);
+// out[i] = silu(gate[i]) * up[i]
+void launch_swiglu_f32(const float* gate, const float* up, float* out, long n, hipStream_t s);
+// Non-causal attention, float32: out[b*L + l, h*hd + j].
+void launch_attn_f32(const float* q, const float* k, const float* vt, float* out, int B, int L, int Hq, int Hkv,
+                     int hd, hipStream_t s);
+// Per row of logits [R, V]: conf = 1 / sum exp(l - max), argmax (lowest index), mask_id excluded.
+void launch_vocab_reduce_f32(const float* logits, int R, int V, int mask_id, float* conf, int32_t* argmax,
+                             hipStream_t s);
+
+// ---- bf16 path -------------------------------------------------------------
+enum GemmEpi { EPI_QKV_ROPE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_STORE = 3 };
+
+struct GemmArgs {
+  int epi;
+  int M, N, K;              // N counts output columns of the virtual B (gate and up both counted)
+  const bf16_t* A;          // [M, K]
+  const bf16_t* W0;         // q / gate / plain weight [*, K]
+  const bf16_t* W1;         // k / up
+  const bf16_t* W2;         // v
+  int n0, n1;               // rows of W0 and W1 (QKV: Hq*hd, Hkv*hd)
+  // epilogue targets
+  float* resid;             // EPI_RESID: [M, N] float32, += result
+  bf16_t* out;              // EPI_SWIGLU: [M, N/2]; EPI_STORE: [M, N]
+  bf16_t* q; bf16_t* k; f16_t* vt;   // EPI_QKV_ROPE (v^T holds the bf16 values as IEEE half)
+  const float* cosb; const float* sinb;
+  int B, L, Hq, Hkv;
+  // split-K scratch (float32 partials [split, M, N]) from the workspace
+  float* splitk_buf;
+};
+void launch_gemm_bf16(const GemmArgs& a, hipStream_t s);
+// Bytes of split-K scratch a launch of this shape needs (0 if it does not split).
+size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi);
+
+void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int L, int Hq,
+                      int Hkv, hipStream_t s);
+
+struct HeadArgs {
+  const bf16_t* hb;   // [R, d]
+  const bf16_t* W;    // [V, d]
+  int R, V, d, mask_id;
+  float* conf; int32_t* argmax; float* logits;  // logits optional
+  float* part_m; float* part_s; int32_t* part_i;  // [n_tiles, R]
+  int* ticket;                                    // zero before the first launch; left zero
+};
+void launch_head_bf16(const HeadArgs& a, hipStream_t s);
+int head_bf16_tiles(int V);
+int head_bf16_max_rows();
+
+// ---- controller (k_commit.hip) ---------------------------------------------
+struct CommitArgs {
+  int32_t* x; int32_t* commit_step; int8_t* reason; float* sv; int32_t* budget; int32_t* ell; int32_t* done;
+  const float* conf; const int32_t* argmax; int32_t* all_done;
+  int B, L, P, G, bl, g0, t, T, mask_id;
+  float thr[4];        // theta_i(t) per position band (float32)
+  int edge[3];         // band edges
+  int budget_on, grind_on;
+  float s_easy, s_hard; int p_easy, p_hard, b_easy, b_mid, b_hard;
+  double eta_bar; int patience; float theta_fb;
+};
+void launch_commit(const CommitArgs& a, hipStream_t s);
+
+}  // namespace dllm

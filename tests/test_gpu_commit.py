@@ -1,0 +1,122 @@
+"""Commit kernel (dllm_commit) against the oracle controller, bit-exact.
+
+Predictions are seeded synthetic traces [blocks, T, B, bl]; the GPU runs the
+controller step by step (stopping a block when every sequence has finished,
+as the decode loop does) and must reproduce the oracle's token ids, commit
+steps, reasons, first-step confidences, budgets and forwards per block.
+"""
+import numpy as np
+import pytest
+import torch
+
+from helpers import assert_state_equal, replay, say
+from oracle import controller as oc
+from paper_2608_22646_amd import binding as B
+from paper_2608_22646_amd import synth
+
+pytestmark = pytest.mark.gpu
+MASK = 999
+
+
+def run_gpu_controller(ctl: B.Controller, conf, arg, prompts, G):
+    """Drive dllm_commit over a trace; returns (state, forwards per block)."""
+    nb, T, Bn, bl = conf.shape
+    dev = "cuda"
+    st = B.DecodeState(Bn, prompts.shape[1], G, dev)
+    B.state_init(MASK, prompts.to(dev), G, st)
+    cd = conf.to(dev)
+    ad = arg.to(dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    forwards = []
+    for blk in range(nb):
+        n = 0
+        for t in range(T):
+            B.commit(ctl, st, cd[blk, t].contiguous(), ad[blk, t].contiguous(), blk, t, MASK, flag)
+            n += 1
+            if int(flag.item()):
+                break
+        forwards.append(n)
+    torch.cuda.synchronize()
+    return st, forwards
+
+
+def make_trace(kind, nb, T, Bn, bl, seed):
+    shape = (nb, T, Bn, bl)
+    if kind == "uniform":
+        c = synth.make_uniform(shape, seed) ** 0.5
+    elif kind == "grid":   # values on the comparison boundaries
+        vals = torch.tensor([0.0, 0.2, 0.25, 0.4, 0.5, 0.6, 0.72, 0.81, 0.9, 0.945, 0.98, 1.0])
+        idx = synth.make_ints(shape, seed, 0, len(vals))
+        c = vals[idx.long()]
+    elif kind == "low":
+        c = synth.make_uniform(shape, seed, 0.0, 0.45)
+    elif kind == "nan":
+        c = synth.make_uniform(shape, seed) ** 0.5
+        c[synth.make_uniform(shape, seed + 1) < 0.05] = float("nan")
+    else:
+        raise ValueError(kind)
+    a = synth.make_ints(shape, seed + 7, 0, MASK)
+    return c.to(torch.float32), a
+
+
+CASES = [
+    # (trace kind, B, bl, blocks, gating, extra controller fields)
+    ("uniform", 1, 32, 8, True, {}),
+    ("uniform", 1, 32, 8, False, {}),
+    ("grid", 3, 32, 4, True, {}),
+    ("grid", 3, 32, 4, False, {}),
+    ("low", 2, 32, 6, True, {}),
+    ("low", 2, 32, 3, False, {}),
+    ("uniform", 8, 32, 4, True, {}),
+    ("uniform", 16, 64, 2, True, {}),
+    ("grid", 2, 64, 3, True, {}),
+    ("uniform", 2, 4, 5, True, {}),
+    ("nan", 2, 32, 3, True, {}),
+    ("uniform", 2, 32, 3, True, dict(pos_edges=(8, 16, 24), p_easy=16, p_hard=24)),
+    ("uniform", 2, 32, 3, True, dict(block_sched=False)),
+    ("uniform", 2, 32, 3, True, dict(pos_aware=False)),
+    ("uniform", 2, 32, 3, True, dict(steps_per_block=12)),
+    ("low", 2, 32, 3, True, dict(budgets=False)),
+    ("low", 2, 32, 3, True, dict(grinding=False)),
+    ("uniform", 1, 32, 2, True, dict(theta_s=0.9, theta_e=0.9, block_sched=False, pos_aware=False,
+                                      budgets=False, grinding=False)),  # fixed-threshold 0.9
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_commit_matches_oracle(case):
+    kind, Bn, bl, nb, gating, extra = CASES[case]
+    kw = dict(budgets=gating, grinding=gating)
+    kw.update(extra)
+    ctl = B.Controller(block_len=bl, **kw)
+    G, P = nb * bl, 5
+    say(f"commit case {case}: {kind} B={Bn} bl={bl} nb={nb} gating={gating} {extra}")
+    conf, arg = make_trace(kind, nb, ctl.T, Bn, bl, seed=100 + case)
+    prompts = synth.make_ints((Bn, P), 3 + case, 0, MASK)
+    st, fwd = run_gpu_controller(ctl, conf, arg, prompts, G)
+    ref = replay(conf.numpy(), arg.numpy(), prompts.numpy(), G, MASK, ctl)
+    assert_state_equal(st, fwd, ref)
+
+
+# hand-derived traces (the same ones that pin the oracle) run through the kernel
+HAND = [
+    ("S1", lambda t, i: 0.99, True, 1, [(1, 0)] * 32),
+    ("S2", lambda t, i: 0.001, True, 4, [(4, 3)] * 32),
+    ("S2'", lambda t, i: 0.001, False, 32, [(4, 31)] * 32),
+    ("S3", lambda t, i: 0.6, True, 4, [(3, 3)] * 32),
+    ("S3'", lambda t, i: 0.6, False, 32, [(1, 23)] * 16 + [(4, 31)] * 16),
+    ("S4", lambda t, i: 0.6 if i < 16 else 0.3, True, 4, [(3, 3)] * 16 + [(4, 3)] * 16),
+    ("S5", lambda t, i: 0.99 if t >= i // 2 else 0.6, True, 9, [(1, i // 2) for i in range(18)] + [(2, 8)] * 14),
+]
+
+
+@pytest.mark.parametrize("name,fn,gating,n,want", HAND, ids=[h[0] for h in HAND])
+def test_commit_hand_traces(name, fn, gating, n, want):
+    say(f"commit hand trace {name}")
+    ctl = B.Controller.gating(gating)
+    conf = torch.tensor([[[[fn(t, i) for i in range(32)]] for t in range(32)]], dtype=torch.float32)
+    arg = torch.arange(32, dtype=torch.int32).view(1, 1, 1, 32).expand(1, 32, 1, 32).contiguous() + 7
+    st, fwd = run_gpu_controller(ctl, conf, arg, torch.zeros((1, 4), dtype=torch.int32), 32)
+    assert fwd == [n]
+    got = list(zip(st.reason[0].cpu().tolist(), st.commit_step[0].cpu().tolist()))
+    assert got == want
