@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Throughput of the CAI-dLLM decode on one MI355X.
+
+One bench step = one dllm_generate of the workload: the prompt batch is decoded
+block by block with the confidence-aware controller, every denoising step
+running the full bidirectional forward, the fused LM-head reduction and the
+commit kernel.  Inputs (random-init weights of the model's shape, seeded
+prompts) are resident in HBM before timing starts.
+
+Prints one JSON line: generated tokens/s, the dominant kernel's roofline
+(gate/up GEMM, bf16 MFMA, timed with HIP events on its launch stream inside the
+timed region) and the CPU oracle's throughput on a bounded sample.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llada_b1]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def forward_flops(cfg, B, L):
+    """Algorithmic flops of one forward: the projections and the attention."""
+    M = B * L
+    d, hd, F = cfg.d_model, cfg.head_dim, cfg.d_ff
+    qkv = 2 * M * d * (cfg.n_heads + 2 * cfg.n_kv_heads) * hd
+    o = 2 * M * cfg.n_heads * hd * d
+    gu = 2 * M * d * 2 * F
+    down = 2 * M * F * d
+    attn = 4 * B * cfg.n_heads * L * L * hd
+    return dict(qkv=qkv, o=o, gate_up=gu, down=down, attn=attn, layer_gemm=qkv + o + gu + down,
+                total=cfg.n_layers * (qkv + o + gu + down + attn))
+
+
+def head_bytes(cfg, R):
+    return cfg.vocab * cfg.d_model * 2 + R * cfg.d_model * 2 + R * 8
+
+
+def cpu_baseline(cfg, weights, prompts, wl, forwards_per_gen, budget_s=25.0):
+    """The oracle (numpy, float32 matrix products) on the first denoising step of
+    the workload: embedding, as many layers as fit in ~budget_s, the final norm +
+    LM head + confidence reduction of the first block, and the controller step.
+    The per-layer time is extrapolated to every layer; tokens/s uses the number
+    of forwards the GPU decode ran."""
+    import numpy as np
+    import torch
+    from oracle import controller as oc
+    from oracle import forward as of
+    from oracle import vocab as ov
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+
+    def host(t):
+        return t.to("cpu").to(torch.float32).numpy()
+
+    B, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
+    L = P + G
+    x = np.concatenate([prompts.cpu().numpy().astype(np.int64), np.full((B, G), cfg.vocab - 1)], axis=1)
+    cos, sin = of.rope_tables(L, cfg.head_dim, cfg.rope_base)
+    t0 = time.perf_counter()
+    h = host(weights[0])[x].astype(np.float64)
+    t_embed = time.perf_counter() - t0
+    layer_times = []
+    while len(layer_times) < cfg.n_layers:
+        l = len(layer_times)
+        lw = [host(w) for w in weights[1 + 9 * l: 10 + 9 * l]]
+        t0 = time.perf_counter()
+        h = of.layer(cfg, lw, h, cos, sin, "bf16")
+        layer_times.append(time.perf_counter() - t0)
+        if sum(layer_times) > budget_s:
+            break
+    rows = np.arange(P, P + bl)
+    fn, lm = host(weights[-2]), host(weights[-1])
+    t0 = time.perf_counter()
+    logits, _ = of.lm_head(cfg, h[:, rows, :].reshape(-1, cfg.d_model), fn, lm, "bf16")
+    conf, arg = ov.confidence_argmax(logits.reshape(B, bl, -1), cfg.vocab - 1)
+    st = oc.init_state(prompts.cpu().numpy(), G, cfg.vocab - 1)
+    p = oc.CaiParams(block_len=bl, budgets=wl.gating, grinding=wl.gating)
+    for seq in range(B):
+        oc.step_sequence(st, seq, P, 0, 0, conf[seq].astype(np.float32), arg[seq], 0, p)
+    t_head = time.perf_counter() - t0
+    per_layer = sum(layer_times) / len(layer_times)
+    s_per_forward = t_embed + per_layer * cfg.n_layers + t_head
+    tok_s = B * G / (s_per_forward * forwards_per_gen)
+    return {
+        "value": tok_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "sample": (f"first denoising step of the workload: embedding, {len(layer_times)} of {cfg.n_layers} "
+                   f"layers timed ({per_layer:.2f} s/layer, extrapolated to all layers), final norm + LM head + "
+                   f"confidence reduction + controller step ({t_head:.2f} s); {s_per_forward:.1f} s per forward "
+                   f"x {forwards_per_gen} forwards per decode (extrapolated)"),
+        "steps_per_s": 1.0 / s_per_forward,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="llada_b1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=25.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_22646_amd import binding as Bd
+    from paper_2608_22646_amd import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    cfg = wl.model
+    B, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
+    L = P + G
+    dev = "cuda"
+    log(f"workload {wl.name}: {cfg.name} B={B} P={P} G={G} block={bl} gating={wl.gating}")
+    t0 = time.perf_counter()
+    weights = synth.make_weights(cfg, dev)
+    torch.cuda.synchronize()
+    log(f"weights ready ({cfg.param_count() / 1e9:.2f} B params, {time.perf_counter() - t0:.1f} s)")
+    model = Bd.Model(cfg, weights)
+    prompts = synth.make_prompts(wl, dev)
+    ctl = Bd.Controller.gating(wl.gating, block_len=bl)
+    ws = model.workspace(B, L, bl)
+    st = Bd.DecodeState(B, P, G, dev)
+
+    model.prof_enable([Bd.PROF_GATEUP])
+    for i in range(args.warmup):
+        res = model.generate(ctl, prompts, G, ws=ws, st=st)
+        log(f"warmup {i}: forwards {res.total_forwards} {res.forwards}")
+    torch.cuda.synchronize()
+
+    model.prof_enable([Bd.PROF_GATEUP])          # clears the warm-up records
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    total_fwd = 0
+    for _ in range(args.steps):
+        res = model.generate(ctl, prompts, G, ws=ws, st=st)
+        total_fwd += res.total_forwards
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    gu_ms, gu_n = model.prof_read(Bd.PROF_GATEUP)
+    model.prof_enable([])
+
+    flops = forward_flops(cfg, B, L)
+    gu_avg_s = gu_ms / gu_n / 1e3
+    gu_tflops = flops["gate_up"] / gu_avg_s / 1e12
+    fwd_per_gen = total_fwd / args.steps
+    tokens = B * G * args.steps
+    value = tokens / dt
+    log(f"timed {args.steps} decodes in {dt:.3f} s: {value:.1f} tokens/s, {total_fwd / dt:.1f} forwards/s, "
+        f"gate/up GEMM {gu_avg_s * 1e6:.1f} us avg over {gu_n} launches = {gu_tflops:.0f} TFLOP/s")
+
+    # breakdown pass (outside the timed region): every kernel class, one decode
+    kinds = {"gemm_qkv_o_down": Bd.PROF_GEMM, "gemm_gate_up": Bd.PROF_GATEUP, "attention": Bd.PROF_ATTN,
+             "lm_head_reduce": Bd.PROF_HEAD, "commit": Bd.PROF_COMMIT, "norm_embed": Bd.PROF_NORM}
+    model.prof_enable(list(kinds.values()))
+    res = model.generate(ctl, prompts, G, ws=ws, st=st)
+    torch.cuda.synchronize()
+    nf = res.total_forwards
+    breakdown = {}
+    for name, k in kinds.items():
+        ms, n = model.prof_read(k)
+        breakdown[name] = {"ms_per_forward": ms / nf, "launches_per_forward": n / nf}
+    model.prof_enable([])
+    gemm_s = (breakdown["gemm_qkv_o_down"]["ms_per_forward"] + breakdown["gemm_gate_up"]["ms_per_forward"]) / 1e3
+    attn_s = breakdown["attention"]["ms_per_forward"] / 1e3
+    gemm_flops = cfg.n_layers * flops["layer_gemm"]
+    attn_flops = cfg.n_layers * flops["attn"]
+    head_s = breakdown["lm_head_reduce"]["ms_per_forward"] / 1e3
+    hbytes = head_bytes(cfg, B * bl)
+    breakdown["gemm_qkv_o_down"]["mfma_frac"] = None
+    extra = {
+        "forwards_per_decode": fwd_per_gen,
+        "denoising_steps_per_s": total_fwd / dt,
+        "forward_gemm_mfma_frac": gemm_flops / gemm_s / 1e12 / BF16_PEAK_TFLOPS,
+        "forward_attention_mfma_frac": attn_flops / attn_s / 1e12 / BF16_PEAK_TFLOPS,
+        "forward_mfma_frac_wall": flops["total"] * total_fwd / dt / 1e12 / BF16_PEAK_TFLOPS,
+        "lm_head_hbm_frac": hbytes / head_s / 1e9 / HBM_PEAK_GBS,
+        "kernel_ms_per_forward": {k: round(v["ms_per_forward"], 4) for k, v in breakdown.items()},
+    }
+    log(json.dumps(extra))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        cpu = cpu_baseline(cfg, weights, prompts, wl, fwd_per_gen, args.cpu_budget)
+        log(f"cpu baseline: {cpu['value']:.4f} tokens/s on {cpu['cores']} threads")
+
+    out = {
+        "metric": "generated tokens/s (LLaDA-8B shape, gen 256) + forward MFMA util vs peak",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dt / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded random-init weights of the model shape, uniform random prompts)",
+        "config": {"workload": f"{wl.name}: {cfg.name} random-init, batch {B}, prompt {P}, gen {G}, "
+                               f"block {bl}, gating {'on' if wl.gating else 'off'}",
+                   "batch": B, "prompt_len": P, "gen_len": G, "block_len": bl,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "gate/up GEMM + SwiGLU (gemm_bf16_kernel, EPI_SWIGLU)",
+                     "achieved": gu_tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": gu_tflops / BF16_PEAK_TFLOPS, "traffic": None,
+                     "flops_per_launch": flops["gate_up"], "avg_launch_us": gu_avg_s * 1e6,
+                     "launches": gu_n},
+        "cpu_baseline": cpu,
+    }
+    out.update(extra)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -243,11 +243,14 @@ int dllm_generate(const dllm_model* model, const dllm_cai_params* params, const 
                   float* conf_trace, int32_t* argmax_trace, void* workspace, size_t workspace_bytes,
                   void* stream);
 
-/* Per-kernel timing with HIP events on the launch stream.  enable != 0 starts
- * recording (and clears totals); dllm_prof_read returns the summed duration in
- * milliseconds and the launch count of kernel class `kind` (0 = GEMM,
- * 1 = attention, 2 = LM head, 3 = commit, 4 = norm/elementwise, 5 = gate/up
- * GEMM only) recorded since enabling, after waiting for the recorded work. */
+/* Per-kernel timing with HIP events recorded on the launch stream around each
+ * launch of the selected kernel classes.  kind: 0 = q/k/v, output and down
+ * GEMMs, 1 = attention, 2 = LM head + reduction, 3 = commit, 4 = norms and
+ * embedding, 5 = gate/up GEMM.  dllm_prof_enable(model, mask) starts recording
+ * the kinds whose bit (1 << kind) is set and clears earlier records (mask 0
+ * stops); dllm_prof_read waits for the recorded work and returns the summed
+ * duration in milliseconds and the launch count of one kind.  Events are host
+ * objects kept by the model handle (no device memory). */
 int dllm_prof_enable(dllm_model* model, int32_t enable);
 int dllm_prof_read(dllm_model* model, int32_t kind, double* total_ms, int64_t* launches);
 

@@ -301,8 +301,12 @@ class Model:
         return GenResult(st, list(fwd), tot.value, ct, at)
 
     # profiling --------------------------------------------------------------
-    def prof_enable(self, on=True):
-        check(lib().dllm_prof_enable(self.h, 1 if on else 0))
+    def prof_enable(self, kinds=()):
+        """Record per-launch HIP-event timings for the given kernel kinds (PROF_*)."""
+        mask = 0
+        for k in kinds:
+            mask |= 1 << k
+        check(lib().dllm_prof_enable(self.h, mask))
 
     def prof_read(self, kind):
         ms = ctypes.c_double()

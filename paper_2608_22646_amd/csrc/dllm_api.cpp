@@ -48,7 +48,7 @@ struct dllm_model {
   dllm_model_cfg cfg;
   std::vector<const void*> w;
   int32_t* pinned_flag = nullptr;
-  bool prof = false;
+  uint32_t prof_mask = 0;  // bit k: record launches of kind k
   std::vector<ProfEvent> events;
   size_t n_events = 0;
 };
@@ -139,7 +139,7 @@ struct ProfScope {
   hipStream_t s;
   ProfEvent* ev = nullptr;
   ProfScope(const dllm_model* mc, int kind, hipStream_t st) : m(const_cast<dllm_model*>(mc)), s(st) {
-    if (!m->prof) return;
+    if (!(m->prof_mask & (1u << kind))) return;
     if (m->n_events == m->events.size()) {
       ProfEvent e{};
       hip_check(hipEventCreate(&e.start), "hipEventCreate");
@@ -679,7 +679,8 @@ int dllm_generate(const dllm_model* m, const dllm_cai_params* p, const int32_t* 
 int dllm_prof_enable(dllm_model* m, int32_t enable) {
   API_BEGIN
   check_model(m);
-  m->prof = enable != 0;
+  require(enable >= 0 && enable < 64, DLLM_EINVAL, "enable must be a bit mask of kinds 0..5");
+  m->prof_mask = (uint32_t)enable;
   m->n_events = 0;
   API_END
 }

@@ -37,14 +37,15 @@ constexpr int NT = 256;
 // Source of virtual weight row n for the tile's loads.  QKV regions are whole
 // 256-row tiles (Hq and Hkv even), so a tile reads a single tensor; SwiGLU
 // tiles interleave gate and up every 32 rows.
+template <int EPI>
 __device__ __forceinline__ const bf16_t* vrow_ptr(const GemmArgs& g, int n) {
-  if (g.epi == EPI_QKV_ROPE) {
+  if (EPI == EPI_QKV_ROPE) {
     if (n < g.n0) return g.W0 + (size_t)n * g.K;
     n -= g.n0;
     if (n < g.n1) return g.W1 + (size_t)n * g.K;
     return g.W2 + (size_t)(n - g.n1) * g.K;
   }
-  if (g.epi == EPI_SWIGLU) {
+  if (EPI == EPI_SWIGLU) {
     const int chunk = n >> 5;
     const int f = ((chunk >> 1) << 5) + (n & 31);
     return ((chunk & 1) ? g.W1 : g.W0) + (size_t)f * g.K;
@@ -62,7 +63,7 @@ struct Tile {
   static constexpr int LDS_STAGE = (BM + BN) * 128;
 };
 
-template <int BM, int BN>
+template <int BM, int BN, int EPI>
 __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
   using TL = Tile<BM, BN>;
   extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -89,8 +90,8 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
   const size_t rstride = (size_t)32 * g.K;
   const bf16_t* asrc = g.A + (size_t)min(m0 + lrow0, g.M - 1) * g.K + kbeg + lch * 8;
   const int a_rows_left = g.M - m0 - lrow0;  // load i is valid iff 32 i < a_rows_left
-  const bf16_t* bsrc0 = vrow_ptr(g, n0 + lrow0) + kbeg + lch * 8;
-  const bf16_t* bsrc1 = g.epi == EPI_SWIGLU ? vrow_ptr(g, n0 + 32 + lrow0) + kbeg + lch * 8 : bsrc0;
+  const bf16_t* bsrc0 = vrow_ptr<EPI>(g, n0 + lrow0) + kbeg + lch * 8;
+  const bf16_t* bsrc1 = EPI == EPI_SWIGLU ? vrow_ptr<EPI>(g, n0 + 32 + lrow0) + kbeg + lch * 8 : bsrc0;
   const int st_base = swz(lrow0, lch);  // LDS offset of load i: st_base + i * 32 * 128 (row & 7 unchanged)
 
   f32x16_t acc[TL::TI][TL::TJ];
@@ -109,8 +110,8 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
                                      : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < TL::LB; ++i) {
-      const bf16_t* src = g.epi == EPI_SWIGLU ? ((i & 1) ? bsrc1 + (i >> 1) * rstride : bsrc0 + (i >> 1) * rstride)
-                                              : bsrc0 + i * rstride;
+      const bf16_t* src = EPI == EPI_SWIGLU ? ((i & 1) ? bsrc1 + (i >> 1) * rstride : bsrc0 + (i >> 1) * rstride)
+                                            : bsrc0 + i * rstride;
       rb[i] = *reinterpret_cast<const uint4*>(src + kt * BK);
     }
   };
@@ -175,7 +176,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
     return;
   }
 
-  if (g.epi == EPI_RESID || g.epi == EPI_STORE) {
+  if (EPI == EPI_RESID || EPI == EPI_STORE) {
 #pragma unroll
     for (int i = 0; i < TL::TI; ++i)
 #pragma unroll
@@ -185,7 +186,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
         for (int r = 0; r < 16; ++r) {
           const int m = row_of(i, r);
           if (m >= g.M) continue;
-          if (g.epi == EPI_RESID)
+          if (EPI == EPI_RESID)
             g.resid[(size_t)m * g.N + n] += acc[i][j][r];
           else
             g.out[(size_t)m * g.N + n] = f2bf(acc[i][j][r]);
@@ -194,7 +195,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
     return;
   }
 
-  if (g.epi == EPI_SWIGLU) {
+  if (EPI == EPI_SWIGLU) {
     const int F = g.N / 2;
 #pragma unroll
     for (int i = 0; i < TL::TI; ++i)
@@ -214,7 +215,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
   }
 
   // EPI_QKV_ROPE: this wave's 128 columns are exactly one head (hd = 128).
-  {
+  if (EPI == EPI_QKV_ROPE) {
     constexpr int HD = 128, HALF = 64;
     const int ncol0 = n0 + wn * TL::WN;  // multiple of 128
     const int nq = g.Hq * HD, nk_ = g.Hkv * HD;
@@ -291,14 +292,22 @@ Plan plan(int M, int N, int K, int epi) {
   return p;
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int EPI>
 void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * (g.N / BN);
   const size_t lds = 2 * (size_t)Tile<BM, BN>::LDS_STAGE;
-  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<BM, BN>,
+  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<BM, BN, EPI>,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hip_check(attr, "hipFuncSetAttribute(gemm_bf16)");
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN>), dim3(tiles, 1, split), dim3(NT), lds, s, g);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI>), dim3(tiles, 1, split), dim3(NT), lds, s, g);
+}
+
+template <int EPI>
+void launch_epi(const GemmArgs& g, int bm, int split, hipStream_t s) {
+  if (bm == 256)
+    launch_tile<256, 256, EPI>(g, split, s);
+  else
+    launch_tile<128, 256, EPI>(g, split, s);
 }
 
 }  // namespace
@@ -314,10 +323,12 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
   if (a.epi == EPI_QKV_ROPE && (a.n0 % 256 != 0 || a.n1 % 256 != 0))
     throw HipError("gemm_bf16: q and k/v regions must be multiples of 256 rows");
   const Plan p = plan(a.M, a.N, a.K, a.epi);
-  if (p.bm == 256)
-    launch_tile<256, 256>(a, p.split, s);
-  else
-    launch_tile<128, 256>(a, p.split, s);
+  switch (a.epi) {
+    case EPI_QKV_ROPE: launch_epi<EPI_QKV_ROPE>(a, p.bm, p.split, s); break;
+    case EPI_SWIGLU: launch_epi<EPI_SWIGLU>(a, p.bm, p.split, s); break;
+    case EPI_RESID: launch_epi<EPI_RESID>(a, p.bm, p.split, s); break;
+    default: throw HipError("gemm_bf16: unknown epilogue");
+  }
   DLLM_LAUNCH_CHECK("gemm_bf16");
   if (p.split > 1) {
     const long MN = (long)a.M * a.N;
