@@ -12,12 +12,13 @@
 //            the epilogue writes silu(gate) * up as bf16 [M, F].
 //   RESID  : plain W; the epilogue adds the result to the float32 residual.
 //
-// Tiling: BM x BN x 64 per 256-thread workgroup, 2 x 2 wavefronts, each wave owns a
-// (BM/2) x (BN/2) block of 32x32 MFMA tiles (v_mfma_f32_32x32x16_bf16).  Tiles of A
-// and Bv go global -> registers -> LDS (double buffered, one barrier per k-step).
-// LDS rows are 128 bytes (64 bf16); the 16-byte chunk c of row r is stored at slot
-// c ^ (r & 7), so the eight rows read by eight consecutive lanes hit eight
-// different bank groups.
+// Tiling: 128 x 256 x 64 per 256-thread workgroup, 2 x 2 wavefronts, each wave owns
+// a 64 x 128 block of 32x32 MFMA tiles (v_mfma_f32_32x32x16_bf16).  Tiles of A and
+// Bv stream from memory straight into a 3-stage LDS ring (buffer_load_dwordx4 ...
+// lds, no staging registers): two k-tiles are in flight while the third is
+// consumed, with one barrier per k-step.  LDS rows are 128 bytes (64 bf16); the
+// 16-byte chunk c of row r is stored at slot c ^ (r & 7), so the eight rows read
+// by eight consecutive lanes hit eight different bank groups.
 //
 // MFMA register layouts (64 lanes, lane = l):
 //   A operand : row l%32, k = 8*(l/32) .. +7       B operand : col l%32, same k
@@ -59,13 +60,39 @@ template <int BM, int BN>
 struct Tile {
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int TI = WM / 32, TJ = WN / 32;         // MFMA tiles per wave
-  static constexpr int LA = BM * 8 / NT, LB = BN * 8 / NT; // 16-byte loads per thread per stage
+  static constexpr int IA = BM / 32, IB = BN / 32;          // LDS-DMA instructions per wave per stage
   static constexpr int LDS_STAGE = (BM + BN) * 128;
+  static constexpr int STAGES = 3;
 };
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Wait until at most N of this wave's vector-memory operations are in flight
+// (gfx9 s_waitcnt encoding: vmcnt split over bits 3:0 and 15:14, expcnt and
+// lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the memory-model fence of __syncthreads (which
+// would wait for every in-flight LDS-DMA load); the asm clobbers keep the
+// compiler from moving memory operations across it.  Callers wait for their
+// own DMA loads with wait_vmcnt first.
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 template <int BM, int BN, int EPI>
 __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
+  // The buffer-resource builtins exist only for the device target; the host
+  // pass needs just the kernel's signature for its launch stub.
+#if defined(__HIP_DEVICE_COMPILE__)
   using TL = Tile<BM, BN>;
+  constexpr int S = TL::STAGES;
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -83,16 +110,43 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
   const int kbeg = blockIdx.z * ksplit;
   const int nk = ksplit / BK;
 
-  // Load e = tid + 256 i covers tile row tid/8 + 32 i, 16-byte chunk tid % 8.
-  // Row r of A advances by 32 rows per i; virtual rows of Bv advance by 32 rows
-  // per i in the same tensor, except SwiGLU tiles where odd i come from Wup.
-  const int lrow0 = tid >> 3, lch = tid & 7;
-  const size_t rstride = (size_t)32 * g.K;
-  const bf16_t* asrc = g.A + (size_t)min(m0 + lrow0, g.M - 1) * g.K + kbeg + lch * 8;
-  const int a_rows_left = g.M - m0 - lrow0;  // load i is valid iff 32 i < a_rows_left
-  const bf16_t* bsrc0 = vrow_ptr<EPI>(g, n0 + lrow0) + kbeg + lch * 8;
-  const bf16_t* bsrc1 = EPI == EPI_SWIGLU ? vrow_ptr<EPI>(g, n0 + 32 + lrow0) + kbeg + lch * 8 : bsrc0;
-  const int st_base = swz(lrow0, lch);  // LDS offset of load i: st_base + i * 32 * 128 (row & 7 unchanged)
+  // LDS-DMA loads: instruction i of wave w fills tile rows 32 i + 8 w .. +7
+  // (1 KiB of LDS).  Lane l writes row + l/8, slot l%8, which holds the row's
+  // logical 16-byte chunk (l%8) ^ (l/8) (the XOR swizzle, since row % 8 == l/8).
+  // Row offsets are fixed across k; the k advance goes in the scalar offset.
+  // A rows past M are clamped to M-1 (their results are never stored).
+  const int lr = lane >> 3, lc = (lane & 7) ^ (lane >> 3);
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, 0x7fffffff, 0x00020000);
+  uint32_t voa[TL::IA];
+#pragma unroll
+  for (int i = 0; i < TL::IA; ++i) {
+    const int row = min(m0 + 32 * i + 8 * wave + lr, g.M - 1);
+    voa[i] = (uint32_t)(((size_t)row * g.K + kbeg + lc * 8) * 2);
+  }
+  // Bv rows: one tensor per tile for QKV / RESID; SwiGLU alternates gate/up per 32 rows.
+  const bf16_t* wb0 = vrow_ptr<EPI>(g, n0);
+  const bf16_t* wb1 = EPI == EPI_SWIGLU ? vrow_ptr<EPI>(g, n0 + 32) : wb0;
+  const __amdgpu_buffer_rsrc_t rb0 = __builtin_amdgcn_make_buffer_rsrc((void*)wb0, 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb1 = __builtin_amdgcn_make_buffer_rsrc((void*)wb1, 0, 0x7fffffff, 0x00020000);
+  uint32_t vob[TL::IB];
+#pragma unroll
+  for (int i = 0; i < TL::IB; ++i) {
+    const int rrow = EPI == EPI_SWIGLU ? 32 * (i >> 1) + 8 * wave + lr : 32 * i + 8 * wave + lr;
+    vob[i] = (uint32_t)(((size_t)rrow * g.K + kbeg + lc * 8) * 2);
+  }
+  auto issue = [&](int kt) {
+    char* base = lds + (kt % S) * TL::LDS_STAGE;
+    const int soff = kt * BK * 2;
+#pragma unroll
+    for (int i = 0; i < TL::IA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + (32 * i + 8 * wave) * 128), 16, voa[i], soff,
+                                               0, 0);
+#pragma unroll
+    for (int i = 0; i < TL::IB; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds((EPI == EPI_SWIGLU && (i & 1)) ? rb1 : rb0,
+                                               (lds_ptr_t)(base + BM * 128 + (32 * i + 8 * wave) * 128), 16,
+                                               vob[i], soff, 0, 0);
+  };
 
   f32x16_t acc[TL::TI][TL::TJ];
 #pragma unroll
@@ -102,36 +156,21 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  uint4 ra[TL::LA], rb[TL::LB];
-  auto gload = [&](int kt) {
+  constexpr int PER_STAGE = TL::IA + TL::IB;  // DMA instructions per wave per stage
 #pragma unroll
-    for (int i = 0; i < TL::LA; ++i)
-      ra[i] = (32 * i < a_rows_left) ? *reinterpret_cast<const uint4*>(asrc + i * rstride + kt * BK)
-                                     : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < TL::LB; ++i) {
-      const bf16_t* src = EPI == EPI_SWIGLU ? ((i & 1) ? bsrc1 + (i >> 1) * rstride : bsrc0 + (i >> 1) * rstride)
-                                            : bsrc0 + i * rstride;
-      rb[i] = *reinterpret_cast<const uint4*>(src + kt * BK);
-    }
-  };
-  auto sstore = [&](int buf) {
-    char* base = lds + buf * TL::LDS_STAGE;
-#pragma unroll
-    for (int i = 0; i < TL::LA; ++i) *reinterpret_cast<uint4*>(base + st_base + i * 32 * 128) = ra[i];
-#pragma unroll
-    for (int i = 0; i < TL::LB; ++i) *reinterpret_cast<uint4*>(base + BM * 128 + st_base + i * 32 * 128) = rb[i];
-  };
-
-  gload(0);
-  sstore(0);
-  __syncthreads();
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) issue(s);
 
   const int lrow = lane & 31, lhalf = lane >> 5;
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    const char* base = lds + buf * TL::LDS_STAGE;
+    // tile kt has landed once only the later tiles' loads are outstanding
+    if (kt + 1 < nk)
+      wait_vmcnt<PER_STAGE * (S - 2)>();
+    else
+      wait_vmcnt<0>();
+    barrier_nofence();  // tile kt visible to all waves; stage (kt - 1) % S free
+    if (kt + S - 1 < nk) issue(kt + S - 1);
+    const char* base = lds + (kt % S) * TL::LDS_STAGE;
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int ch = ks * 2 + lhalf;
@@ -152,8 +191,6 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
         for (int j = 0; j < TL::TJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) sstore(buf ^ 1);
-    __syncthreads();
   }
 
   // ------------------------------------------------------------ epilogues
@@ -261,6 +298,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
         }
     }
   }
+#endif
 }
 
 // resid[m, n] += sum_z part[z, m, n], z in order.
@@ -282,7 +320,7 @@ struct Plan {
 };
 
 Plan plan(int M, int N, int K, int epi) {
-  Plan p{M >= 2048 ? 256 : 128, 256, 1};
+  Plan p{128, 256, 1};
   const long tiles = (long)((M + p.bm - 1) / p.bm) * (N / p.bn);
   if (epi == EPI_RESID) {
     while (p.split < 8 && tiles * p.split * 2 <= 256 + 64 && (K / BK) % (p.split * 2) == 0 &&
@@ -295,7 +333,7 @@ Plan plan(int M, int N, int K, int epi) {
 template <int BM, int BN, int EPI>
 void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * (g.N / BN);
-  const size_t lds = 2 * (size_t)Tile<BM, BN>::LDS_STAGE;
+  const size_t lds = (size_t)Tile<BM, BN>::STAGES * Tile<BM, BN>::LDS_STAGE;
   static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<BM, BN, EPI>,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hip_check(attr, "hipFuncSetAttribute(gemm_bf16)");
@@ -304,10 +342,8 @@ void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
 
 template <int EPI>
 void launch_epi(const GemmArgs& g, int bm, int split, hipStream_t s) {
-  if (bm == 256)
-    launch_tile<256, 256, EPI>(g, split, s);
-  else
-    launch_tile<128, 256, EPI>(g, split, s);
+  (void)bm;
+  launch_tile<128, 256, EPI>(g, split, s);
 }
 
 }  // namespace

@@ -124,3 +124,16 @@ def test_null_model_is_rejected():
     n = ctypes.c_size_t()
     assert lib.dllm_workspace_size(None, 1, 8, 8, ctypes.byref(n)) == -1
     assert lib.dllm_model_destroy(None) == 0
+
+
+def test_library_has_no_undefined_internal_symbols():
+    """Every kernel the launchers reference is defined (a kernel whose host stub
+    the compiler dropped shows up as an undefined dllm:: symbol)."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-C", "--undefined-only", B.LIB_PATH], capture_output=True, text=True, check=True)
+    bad = [l for l in out.stdout.splitlines() if "dllm::" in l]
+    assert not bad, bad
