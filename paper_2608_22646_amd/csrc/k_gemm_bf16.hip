@@ -33,37 +33,41 @@ namespace dllm {
 namespace {
 
 constexpr int BK = 64;
-constexpr int NT = 256;
 
-// Source of virtual weight row n for the tile's loads.  QKV regions are whole
-// 256-row tiles (Hq and Hkv even), so a tile reads a single tensor; SwiGLU
-// tiles interleave gate and up every 32 rows.
+// Virtual weight row n -> (tensor index, row inside that tensor).  QKV regions
+// are whole 256-row tiles (Hq and Hkv even), so a tile reads a single tensor;
+// SwiGLU rows interleave gate and up every 32 rows.
 template <int EPI>
-__device__ __forceinline__ const bf16_t* vrow_ptr(const GemmArgs& g, int n) {
+__device__ __forceinline__ int2 vrow(const GemmArgs& g, int n) {
   if (EPI == EPI_QKV_ROPE) {
-    if (n < g.n0) return g.W0 + (size_t)n * g.K;
-    n -= g.n0;
-    if (n < g.n1) return g.W1 + (size_t)n * g.K;
-    return g.W2 + (size_t)(n - g.n1) * g.K;
+    if (n < g.n0) return make_int2(0, n);
+    if (n < g.n0 + g.n1) return make_int2(1, n - g.n0);
+    return make_int2(2, n - g.n0 - g.n1);
   }
   if (EPI == EPI_SWIGLU) {
     const int chunk = n >> 5;
-    const int f = ((chunk >> 1) << 5) + (n & 31);
-    return ((chunk & 1) ? g.W1 : g.W0) + (size_t)f * g.K;
+    return make_int2(chunk & 1, ((chunk >> 1) << 5) + (n & 31));
   }
-  return g.W0 + (size_t)n * g.K;
+  return make_int2(0, n);
 }
 
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ (row & 7)) << 4); }
 
-template <int BM, int BN>
+template <int BM_, int BN_, int WAVES_M, int WAVES_N, int STAGES_>
 struct Tile {
-  static constexpr int WM = BM / 2, WN = BN / 2;
-  static constexpr int TI = WM / 32, TJ = WN / 32;         // MFMA tiles per wave
-  static constexpr int IA = BM / 32, IB = BN / 32;          // LDS-DMA instructions per wave per stage
+  static constexpr int BM = BM_, BN = BN_, S = STAGES_;
+  static constexpr int NW = WAVES_M * WAVES_N, NTH = 64 * NW;
+  static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  static constexpr int TI = WM / 32, TJ = WN / 32;          // MFMA tiles per wave
+  static constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;   // LDS-DMA instructions per wave per stage
   static constexpr int LDS_STAGE = (BM + BN) * 128;
-  static constexpr int STAGES = 3;
+  static_assert(WN == 128, "the QKV and SwiGLU epilogues need 128-column wave tiles");
+  static_assert(IA * NW * 8 == BM && IB * NW * 8 == BN, "tile rows must split evenly over the DMA loads");
 };
+// 128 x 256, 4 waves of 64 x 128, three stages (small M: more tiles to spread over 256 CUs)
+using TileS = Tile<128, 256, 2, 2, 3>;
+// 256 x 256, 8 waves of 64 x 128 (two per SIMD), two stages (large M: fewer bytes per flop)
+using TileL = Tile<256, 256, 4, 2, 2>;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -86,31 +90,35 @@ __device__ __forceinline__ void barrier_nofence() {
   asm volatile("" ::: "memory");
 }
 
-template <int BM, int BN, int EPI>
-__global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
+template <class TL, int EPI>
+__global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
   // The buffer-resource builtins exist only for the device target; the host
   // pass needs just the kernel's signature for its launch stub.
 #if defined(__HIP_DEVICE_COMPILE__)
-  using TL = Tile<BM, BN>;
-  constexpr int S = TL::STAGES;
+  constexpr int BM = TL::BM, BN = TL::BN, S = TL::S, NW = TL::NW;
   extern __shared__ __attribute__((aligned(16))) char lds[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  // wave index made provably uniform so per-wave buffer descriptors stay scalar
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / (BN / TL::WN), wn = wave % (BN / TL::WN);
 
-  // XCD-aware tile order: workgroup i runs on XCD i % 8; give each XCD a
-  // contiguous run of tiles (all M-tiles of consecutive N-tiles) so the weight
-  // tile is fetched from HBM once per XCD and A stays in that XCD's L2.
+  // XCD-aware, grouped tile order.  Workgroup i runs on XCD i % 8, so each XCD
+  // takes a contiguous run of the tile order; the order walks groups of up to
+  // GM M-tiles across all N-tiles, so the ~32 tiles an XCD runs at once share
+  // a few A tiles and a few weight tiles in that XCD's L2.
+  constexpr int GM = 8;
   const int mt = (g.M + BM - 1) / BM, ntl = g.N / BN;
   const int tiles = mt * ntl;
   int lin = blockIdx.x;
   if ((tiles & 7) == 0) lin = (blockIdx.x & 7) * (tiles >> 3) + (blockIdx.x >> 3);
-  const int m0 = (lin % mt) * BM, n0 = (lin / mt) * BN;
+  const int grp = lin / (GM * ntl), first_m = grp * GM, gsize = min(mt - first_m, GM);
+  const int in_grp = lin - grp * GM * ntl;
+  const int m0 = (first_m + in_grp % gsize) * BM, n0 = (in_grp / gsize) * BN;
 
   const int ksplit = g.K / gridDim.z;
   const int kbeg = blockIdx.z * ksplit;
   const int nk = ksplit / BK;
 
-  // LDS-DMA loads: instruction i of wave w fills tile rows 32 i + 8 w .. +7
+  // LDS-DMA loads: instruction i of wave w fills tile rows 8 (NW i + w) .. +7
   // (1 KiB of LDS).  Lane l writes row + l/8, slot l%8, which holds the row's
   // logical 16-byte chunk (l%8) ^ (l/8) (the XOR swizzle, since row % 8 == l/8).
   // Row offsets are fixed across k; the k advance goes in the scalar offset.
@@ -120,31 +128,30 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
   uint32_t voa[TL::IA];
 #pragma unroll
   for (int i = 0; i < TL::IA; ++i) {
-    const int row = min(m0 + 32 * i + 8 * wave + lr, g.M - 1);
+    const int row = min(m0 + 8 * (NW * i + wave) + lr, g.M - 1);
     voa[i] = (uint32_t)(((size_t)row * g.K + kbeg + lc * 8) * 2);
   }
-  // Bv rows: one tensor per tile for QKV / RESID; SwiGLU alternates gate/up per 32 rows.
-  const bf16_t* wb0 = vrow_ptr<EPI>(g, n0);
-  const bf16_t* wb1 = EPI == EPI_SWIGLU ? vrow_ptr<EPI>(g, n0 + 32) : wb0;
-  const __amdgpu_buffer_rsrc_t rb0 = __builtin_amdgcn_make_buffer_rsrc((void*)wb0, 0, 0x7fffffff, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rb1 = __builtin_amdgcn_make_buffer_rsrc((void*)wb1, 0, 0x7fffffff, 0x00020000);
+  // Bv rows: each 8-row DMA group lies in one tensor (the tile's q/k/v tensor,
+  // or gate / up by 32-row parity for SwiGLU).
+  const bf16_t* wsrc[3] = {g.W0, g.W1, g.W2};
+  __amdgpu_buffer_rsrc_t rbs[TL::IB];
   uint32_t vob[TL::IB];
 #pragma unroll
   for (int i = 0; i < TL::IB; ++i) {
-    const int rrow = EPI == EPI_SWIGLU ? 32 * (i >> 1) + 8 * wave + lr : 32 * i + 8 * wave + lr;
-    vob[i] = (uint32_t)(((size_t)rrow * g.K + kbeg + lc * 8) * 2);
+    const int2 first = vrow<EPI>(g, n0 + 8 * (NW * i + wave));  // wave-uniform
+    rbs[i] = __builtin_amdgcn_make_buffer_rsrc((void*)wsrc[first.x], 0, 0x7fffffff, 0x00020000);
+    vob[i] = (uint32_t)(((size_t)(first.y + lr) * g.K + kbeg + lc * 8) * 2);
   }
   auto issue = [&](int kt) {
     char* base = lds + (kt % S) * TL::LDS_STAGE;
     const int soff = kt * BK * 2;
 #pragma unroll
     for (int i = 0; i < TL::IA; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + (32 * i + 8 * wave) * 128), 16, voa[i], soff,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + 8 * (NW * i + wave) * 128), 16, voa[i], soff,
                                                0, 0);
 #pragma unroll
     for (int i = 0; i < TL::IB; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds((EPI == EPI_SWIGLU && (i & 1)) ? rb1 : rb0,
-                                               (lds_ptr_t)(base + BM * 128 + (32 * i + 8 * wave) * 128), 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rbs[i], (lds_ptr_t)(base + BM * 128 + 8 * (NW * i + wave) * 128), 16,
                                                vob[i], soff, 0, 0);
   };
 
@@ -171,25 +178,43 @@ __global__ void __launch_bounds__(NT, 1) gemm_bf16_kernel(GemmArgs g) {
     barrier_nofence();  // tile kt visible to all waves; stage (kt - 1) % S free
     if (kt + S - 1 < nk) issue(kt + S - 1);
     const char* base = lds + (kt % S) * TL::LDS_STAGE;
+    // Software pipeline over the four 16-wide k-slices: slices 0 and 1 are read
+    // first, then each MFMA of slice ks is followed by one LDS read of slice
+    // ks + 2 (three fragment register sets), so LDS latency hides under the
+    // MFMAs.  The sched_group_barrier sequence pins that order.
+    constexpr int NS = BK / 16, NF = TL::TI + TL::TJ, NM = TL::TI * TL::TJ;
+    static_assert(NM >= NF, "pipeline needs at least as many MFMAs as fragment reads per slice");
+    bf16x8_t af[3][TL::TI], bfr[3][TL::TJ];
+    auto frag = [&](int ks) {
+      const int ch = ks * 2 + lhalf, set = ks % 3;
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = ks * 2 + lhalf;
-      bf16x8_t af[TL::TI], bfr[TL::TJ];
+      for (int i = 0; i < TL::TI; ++i)
+        af[set][i] = *reinterpret_cast<const bf16x8_t*>(base + swz(wm * TL::WM + i * 32 + lrow, ch));
 #pragma unroll
-      for (int i = 0; i < TL::TI; ++i) {
-        const int row = wm * TL::WM + i * 32 + lrow;
-        af[i] = *reinterpret_cast<const bf16x8_t*>(base + swz(row, ch));
-      }
+      for (int j = 0; j < TL::TJ; ++j)
+        bfr[set][j] = *reinterpret_cast<const bf16x8_t*>(base + BM * 128 + swz(wn * TL::WN + j * 32 + lrow, ch));
+    };
+    frag(0);
+    frag(1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NF, 0);
 #pragma unroll
-      for (int j = 0; j < TL::TJ; ++j) {
-        const int row = wn * TL::WN + j * 32 + lrow;
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(base + BM * 128 + swz(row, ch));
-      }
+    for (int ks = 0; ks < NS; ++ks) {
+      if (ks + 2 < NS) frag(ks + 2);
 #pragma unroll
       for (int i = 0; i < TL::TI; ++i)
 #pragma unroll
         for (int j = 0; j < TL::TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks % 3][i], bfr[ks % 3][j], acc[i][j], 0, 0, 0);
+      if (ks + 2 < NS) {
+#pragma unroll
+        for (int x = 0; x < NF; ++x) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA of slice ks
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read of slice ks + 2
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NM - NF, 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+      }
     }
   }
 
@@ -319,31 +344,49 @@ struct Plan {
   int bm, bn, split;
 };
 
+// Pick the tile (128 x 256 on 4 waves or 256 x 256 on 8 waves) and, for the
+// residual GEMMs, a K split, by the number of rounds of workgroups over the
+// 256 compute units weighted by each tile's measured per-CU throughput
+// (the larger tile moves fewer bytes per flop: ~1.3x faster per flop).
 Plan plan(int M, int N, int K, int epi) {
-  Plan p{128, 256, 1};
-  const long tiles = (long)((M + p.bm - 1) / p.bm) * (N / p.bn);
-  if (epi == EPI_RESID) {
-    while (p.split < 8 && tiles * p.split * 2 <= 256 + 64 && (K / BK) % (p.split * 2) == 0 &&
-           (K / BK) / (p.split * 2) >= 4)
-      p.split *= 2;
+  const double rel_speed[2] = {1.0, 1.3};
+  const int bms[2] = {128, 256};
+  Plan best{128, 256, 1};
+  double best_cost = 1e30;
+  for (int c = 0; c < 2; ++c) {
+    const long tiles = (long)((M + bms[c] - 1) / bms[c]) * (N / 256);
+    int split = 1;
+    if (epi == EPI_RESID) {
+      while (split < 8 && tiles * split * 2 <= 256 + 64 && (K / BK) % (split * 2) == 0 && (K / BK) / (split * 2) >= 4)
+        split *= 2;
+    }
+    const long wgs = tiles * split;
+    const double rounds = (double)((wgs + 255) / 256);
+    const double cost = rounds * (double)bms[c] / split / rel_speed[c];
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best = Plan{bms[c], 256, split};
+    }
   }
-  return p;
+  return best;
 }
 
-template <int BM, int BN, int EPI>
+template <class TL, int EPI>
 void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
-  const int tiles = ((g.M + BM - 1) / BM) * (g.N / BN);
-  const size_t lds = (size_t)Tile<BM, BN>::STAGES * Tile<BM, BN>::LDS_STAGE;
-  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<BM, BN, EPI>,
+  const int tiles = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
+  const size_t lds = (size_t)TL::S * TL::LDS_STAGE;
+  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<TL, EPI>,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hip_check(attr, "hipFuncSetAttribute(gemm_bf16)");
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI>), dim3(tiles, 1, split), dim3(NT), lds, s, g);
+  hipLaunchKernelGGL((gemm_bf16_kernel<TL, EPI>), dim3(tiles, 1, split), dim3(TL::NTH), lds, s, g);
 }
 
 template <int EPI>
 void launch_epi(const GemmArgs& g, int bm, int split, hipStream_t s) {
-  (void)bm;
-  launch_tile<128, 256, EPI>(g, split, s);
+  if (bm == 256)
+    launch_tile<TileL, EPI>(g, split, s);
+  else
+    launch_tile<TileS, EPI>(g, split, s);
 }
 
 }  // namespace
