@@ -1,0 +1,114 @@
+"""Full-size workloads (LLaDA-8B and Dream-7B shapes) at the launch configuration
+the decode uses.
+
+For each workload:
+  * the first denoising step's forward runs layer by layer; at the first and
+    last layer every stage is checked against the oracle applied to the GPU's
+    own stage inputs on sampled rows (all key positions feed the attention
+    check), and the fused LM head is checked on sampled block rows;
+  * a complete decode (dllm_generate) is replayed through the oracle
+    controller on the GPU's recorded predictions: token ids, commit steps,
+    reasons, budgets, first-step confidences and forwards per block must be
+    bit-identical, and the decode invariants must hold.
+Weights are seeded random draws made on the GPU (one 8B-parameter model at a
+time); only the layers the oracle needs are copied to the host.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_stages import check_head, check_layer
+from helpers import assert_state_equal, replay, say, to_np
+from paper_2608_22646_amd import binding as B
+from paper_2608_22646_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+WORKLOADS = ["llada_b1", "llada_b8", "dream_b1", "dream_long"]
+
+
+@pytest.fixture(scope="module")
+def models():
+    cache = {}
+
+    def get(cfg):
+        if cfg.name not in cache:
+            cache.clear()
+            torch.cuda.empty_cache()
+            say(f"generating weights for {cfg.name}")
+            w = synth.make_weights(cfg, "cuda")
+            cache[cfg.name] = (w, B.Model(cfg, w))
+        return cache[cfg.name]
+
+    yield get
+    cache.clear()
+
+
+def host_weights(cfg, w, layers):
+    out = [None] * len(w)
+    for l in layers:
+        for i in range(1 + 9 * l, 10 + 9 * l):
+            out[i] = to_np(w[i])
+    out[-2] = to_np(w[-2])
+    out[-1] = to_np(w[-1])
+    return out
+
+
+def check_invariants(st, forwards, P, G, bl, T, mask_id, ctl):
+    cs = st.commit_step.cpu().numpy()
+    rs = st.reason.cpu().numpy()
+    assert (cs >= 0).all() and (cs <= T - 1).all(), "a token was left masked or committed past T"
+    assert (rs >= 1).all()
+    assert (st.x[:, P:] != mask_id).all().item(), "mask id left in the output"
+    if ctl.budgets:
+        assert (cs <= st.budget.cpu().numpy()).all(), "a token exceeded its step budget"
+    for b in range(cs.shape[0]):
+        for blk in range(G // bl):
+            assert cs[b, blk * bl:(blk + 1) * bl].max() + 1 <= forwards[blk]
+
+
+@pytest.mark.parametrize("name", WORKLOADS)
+def test_full_size_stages_and_head(models, name):
+    wl = synth.WORKLOADS[name]
+    cfg = wl.model
+    w, model = models(cfg)
+    Bn, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
+    L = P + G
+    sample_layers = [0, cfg.n_layers - 1]
+    wnp = host_weights(cfg, w, sample_layers)
+    prompts = synth.make_prompts(wl)
+    x = torch.cat([prompts, torch.full((Bn, G), cfg.mask_id, dtype=torch.int32)], 1).cuda()
+    ws = model.workspace(Bn, L, bl)
+    model.embed(x, ws)
+    rng = np.random.default_rng(17)
+    rows = np.sort(rng.choice(Bn * L, 64, replace=False))
+    keys = np.sort(rng.choice(L, 64, replace=False))
+    for l in range(cfg.n_layers):
+        if l in sample_layers:
+            say(f"{name}: stages of layer {l}")
+            st = check_layer(model, cfg, wnp, ws, Bn, L, l, rows=rows, key_rows=keys)
+            say("  " + ", ".join(f"{k}={v:.2e}" for k, v in st.items()))
+        else:
+            model.layer(l, 2, Bn, L, ws)
+    say(f"{name}: head")
+    head_rows = np.sort(rng.choice(Bn * bl, min(16, Bn * bl), replace=False))
+    hs = check_head(model, cfg, wnp, ws, Bn, L, P, bl, sample=head_rows)
+    say(f"  head {hs}")
+
+
+@pytest.mark.parametrize("name,gating", [(n, None) for n in WORKLOADS] + [("dream_b1", True)])
+def test_full_size_decode_replay(models, name, gating):
+    wl = synth.WORKLOADS[name]
+    cfg = wl.model
+    _, model = models(cfg)
+    gating = wl.gating if gating is None else gating
+    ctl = B.Controller.gating(gating, block_len=wl.block_len)
+    prompts = synth.make_prompts(wl)
+    say(f"{name}: decode, gating {'on' if gating else 'off'}")
+    res = model.generate(ctl, prompts.cuda(), wl.gen_len, trace=True)
+    torch.cuda.synchronize()
+    ref = replay(res.conf_trace.cpu().numpy(), res.argmax_trace.cpu().numpy(), prompts.numpy(), wl.gen_len,
+                 cfg.mask_id, ctl)
+    assert_state_equal(res.state, res.forwards, ref)
+    check_invariants(res.state, res.forwards, wl.prompt_len, wl.gen_len, wl.block_len, ctl.T, cfg.mask_id, ctl)
+    say(f"  forwards per block {res.forwards} (total {res.total_forwards})")
