@@ -27,6 +27,41 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+TRAFFIC_SUMMARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                               "gemm_gateup_llada_b1_traffic.txt")
+GEMM_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_22646_amd", "csrc",
+                           "k_gemm_bf16.hip")
+
+
+def measured_traffic():
+    """HBM bytes per gate/up GEMM launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading
+    for a plain copy of known size), or None when the summary is missing or was
+    taken on a different version of the GEMM source."""
+    import hashlib
+    try:
+        fields = dict(l.split("=", 1) for l in open(TRAFFIC_SUMMARY).read().split("\n") if "=" in l)
+        src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+        if fields.get("gemm_source_sha256", "").strip() != src:
+            return None
+        return float(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    """A plain 1 GiB device-to-device copy, five times: the counter reading of a
+    kernel whose HBM traffic is known (1 GiB read + 1 GiB written per launch)."""
+    import torch
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 5 x {n} bytes")
+
+
 def forward_flops(cfg, B, L):
     """Algorithmic flops of one forward: the projections and the attention."""
     M = B * L
@@ -111,11 +146,16 @@ def main():
     ap.add_argument("--workload", default="llada_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=25.0)
+    ap.add_argument("--copy-calib", action="store_true", help="run only the copy used to calibrate HBM counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calib:
+        copy_calibration()
+        return
 
     import torch
     from paper_2608_22646_amd import binding as Bd
@@ -219,7 +259,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "gate/up GEMM + SwiGLU (gemm_bf16_kernel, EPI_SWIGLU)",
                      "achieved": gu_tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": gu_tflops / BF16_PEAK_TFLOPS, "traffic": None,
+                     "frac": gu_tflops / BF16_PEAK_TFLOPS, "traffic": measured_traffic(),
                      "flops_per_launch": flops["gate_up"], "avg_launch_us": gu_avg_s * 1e6,
                      "launches": gu_n},
         "cpu_baseline": cpu,
