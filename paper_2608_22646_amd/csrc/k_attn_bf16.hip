@@ -184,11 +184,222 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Streaming variant for sequences whose length is a multiple of 8: NW
+// wavefronts x 32 queries per workgroup (NW = 8: two waves per SIMD, so one
+// wave's softmax overlaps the other's MFMAs, and each K/V tile serves 256
+// queries).  K and V^T tiles are copied straight into a 3-stage LDS ring with
+// buffer_load_dwordx4 ... lds.  Keys past L are masked; their K rows read as
+// zero through the buffer bound, and their V^T columns hold either the next
+// d-row's (finite) values or, past the end of the head, zeros.  The 1/sqrt(hd) * log2(e) scale is folded into the
+// exp2 argument, and the running maximum is only raised when a tile's maximum
+// exceeds it by more than 8 (log2 units): unnormalised probabilities then stay
+// below 2^8 (exact to half's relative precision) and the O / l rescale is
+// skipped for most tiles.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_a() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ __forceinline__ void barrier_nofence_a() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int NW>
+__global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* __restrict__ q,
+                                                                 const bf16_t* __restrict__ k,
+                                                                 const f16_t* __restrict__ vt,
+                                                                 bf16_t* __restrict__ out, int L, int Hq, int Hkv) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int S = 3, PER_STAGE = 32 / NW;  // 16 K + 16 V^T DMA instructions per tile
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
+  const int q0 = blockIdx.x * (QW * NW) + wave * QW;
+  const int lq = lane & 31, half = lane >> 5;
+  const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
+  const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
+
+  bf16x8_t qf[8];
+  {
+    const int qi = q0 + lq;
+    const bf16_t* qrow = q + (((size_t)b * Hq + h) * L + (qi < L ? qi : 0)) * HD;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16 + half * 8);
+      if (qi >= L) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+  }
+
+  // DMA: K instruction i fills keys 4i..4i+3 (rows of 256 B, lane l -> key
+  // 4i + l/16, slot l%16 holding chunk (l%16) ^ (key & 7)); V^T instruction i
+  // fills d rows 8i..8i+7 (rows of 128 B, lane l -> d = 8i + l/8, slot l%8
+  // holding chunk (l%8) ^ (d & 7)).  Wave w issues instructions w, w + NW, ...
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, 0, L * HD * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, 0, HD * L * 2, 0x00020000);
+  constexpr int PK = 16 / NW;
+  uint32_t vok[PK], vov[PK];
+#pragma unroll
+  for (int j = 0; j < PK; ++j) {
+    const int i = wave + NW * j;
+    const int key = 4 * i + (lane >> 4), kc = (lane & 15) ^ (key & 7);
+    vok[j] = (uint32_t)((key * HD + kc * 8) * 2);
+    const int d = 8 * i + (lane >> 3), vc = (lane & 7) ^ (d & 7);
+    vov[j] = (uint32_t)(((size_t)d * L + vc * 8) * 2);
+  }
+  auto issue = [&](int t) {
+    char* base = lds + (t % S) * STAGE;
+    const int t0 = t * KT;
+#pragma unroll
+    for (int j = 0; j < PK; ++j) {
+      const int i = wave + NW * j;
+      // the tile offset goes in the per-lane offset, which the buffer bound
+      // checks: reads past the end of this head's K or V^T return zeros
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(base + i * 1024), 16, vok[j] + t0 * HD * 2, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(base + K_BYTES + i * 1024), 16, vov[j] + t0 * 2, 0, 0,
+                                               0);
+    }
+  };
+
+  f32x16_t o[4];
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ds][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float sc = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
+
+  const int ntiles = (L + KT - 1) / KT;
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s)
+    if (s < ntiles) issue(s);
+  for (int t = 0; t < ntiles; ++t) {
+    if (t + 1 < ntiles)
+      wait_vmcnt_a<PER_STAGE * (S - 2)>();
+    else
+      wait_vmcnt_a<0>();
+    barrier_nofence_a();
+    if (t + S - 1 < ntiles) issue(t + S - 1);
+    const char* base = lds + (t % S) * STAGE;
+
+    f32x16_t s2[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s2[st][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + lq, ks * 2 + half));
+        s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s2[st], 0, 0, 0);
+      }
+    }
+    const int t0 = t * KT;
+    float mt = -INFINITY;
+    if (t0 + KT <= L) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s2[st][r]);
+    } else {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = t0 + st * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (key >= L) s2[st][r] = -INFINITY;
+          mt = fmaxf(mt, s2[st][r]);
+        }
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sc;
+    // raise the running maximum only when it grows by more than 2^8
+    if (__ballot(mt > m_run + 8.0f) != 0ull) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[ds][r] *= alpha;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(fmaf(s2[st][r], sc, -m_run));
+        s2[st][r] = p;
+        psum += p;
+      }
+    l_run += psum;
+
+#pragma unroll
+    for (int jk = 0; jk < 4; ++jk) {
+      f16x8_t pf;
+      const int st = jk >> 1, r0 = (jk & 1) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[st][r0 + e];
+      const int kA = jk * 16 + 4 * half, kB = kA + 8;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) {
+        const int d = ds * 32 + lq;
+        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kA >> 3) + (kA & 7) * 2);
+        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kB >> 3) + (kB & 7) * 2);
+        const f16x8_t vf = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
+        o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
+      }
+    }
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  const int qi = q0 + lq;
+  if (qi >= L) return;
+  bf16_t* orow = out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      const int d = ds * 32 + 8 * rg + 4 * half;
+      uint2 w;
+      w.x = pack_bf16x2(o[ds][rg * 4 + 0] * inv, o[ds][rg * 4 + 1] * inv);
+      w.y = pack_bf16x2(o[ds][rg * 4 + 2] * inv, o[ds][rg * 4 + 3] * inv);
+      *reinterpret_cast<uint2*>(orow + d) = w;
+    }
+#endif
+}
+
 }  // namespace
 
 void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int L, int Hq, int Hkv,
                       hipStream_t s) {
   if (B * L == 0) return;
+  if (L % 8 == 0) {
+    // streaming kernel: 8 waves (256 queries) per workgroup when that still gives
+    // two or more workgroups per CU over the launch, else 4 waves
+    const bool wide = (long)((L + 255) / 256) * Hq * B >= 512;
+    const size_t lds = 3 * (size_t)STAGE;
+    if (wide) {
+      static const hipError_t a8 =
+          hipFuncSetAttribute((const void*)attn_stream_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      hip_check(a8, "hipFuncSetAttribute(attn_stream<8>)");
+      hipLaunchKernelGGL(attn_stream_kernel<8>, dim3(ceil_div(L, QW * 8), Hq, B), dim3(512), lds, s, q, k, vt, out, L,
+                         Hq, Hkv);
+    } else {
+      static const hipError_t a4 =
+          hipFuncSetAttribute((const void*)attn_stream_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      hip_check(a4, "hipFuncSetAttribute(attn_stream<4>)");
+      hipLaunchKernelGGL(attn_stream_kernel<4>, dim3(ceil_div(L, QW * 4), Hq, B), dim3(256), lds, s, q, k, vt, out, L,
+                         Hq, Hkv);
+    }
+    DLLM_LAUNCH_CHECK("attn_stream");
+    return;
+  }
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)attn_bf16_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * STAGE);
   hip_check(attr, "hipFuncSetAttribute(attn_bf16)");
