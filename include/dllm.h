@@ -131,13 +131,21 @@ typedef struct dllm_model dllm_model;
 
 /*
  * Create a model handle from caller-owned device weights (borrowed for the
- * handle's lifetime, never copied).  `weights` is a host array of n_weights =
+ * handle's lifetime).  `weights` is a host array of n_weights =
  * 3 + 9*n_layers device pointers in this order, each row-major, of cfg.dtype
  * (norm gains included):
  *   embed [V, d]; per layer: attn_norm [d], wq [Hq*hd, d], wk [Hkv*hd, d],
  *   wv [Hkv*hd, d], wo [d, Hq*hd], mlp_norm [d], w_gate [F, d], w_up [F, d],
  *   w_down [d, F]; then final_norm [d], lm_head [V, d].
- * Errors: DLLM_EINVAL (null pointer, bad count), DLLM_EUNSUPPORTED (shape).
+ * For DLLM_BF16 the handle also owns a copy of lm_head (ceil(V/256)*256*d
+ * bf16 values in a tiled layout that the LM-head kernel streams contiguously),
+ * made here and freed by dllm_model_destroy: later writes to the caller's
+ * lm_head are not seen.  The copy is taken after a device synchronisation, so
+ * the weights may still be being written on any stream when this is called.
+ * All other weights are read in place on every call.
+ * Errors: DLLM_EINVAL (null pointer, bad count), DLLM_EUNSUPPORTED (shape, or
+ * a bf16 LM head above 2 GiB), DLLM_EHIP (a device call failed, allocation
+ * included).
  */
 int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int32_t n_weights,
                       dllm_model** out);

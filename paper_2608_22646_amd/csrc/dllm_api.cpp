@@ -47,6 +47,7 @@ struct ProfEvent {
 struct dllm_model {
   dllm_model_cfg cfg;
   std::vector<const void*> w;
+  bf16_t* head_tiled = nullptr;  // bf16: owned tiled copy of the LM head
   int32_t* pinned_flag = nullptr;
   uint32_t prof_mask = 0;  // bit k: record launches of kind k
   std::vector<ProfEvent> events;
@@ -323,7 +324,7 @@ void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf
   } else {
     HeadArgs a{};
     a.hb = at<bf16_t>(ws, lay.hb);
-    a.W = Wb(m, 2 + 9 * nl);
+    a.W = m->head_tiled;
     a.R = R;
     a.V = c.vocab;
     a.d = c.d_model;
@@ -480,13 +481,27 @@ int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int
     require((c.head_dim == 64 || c.head_dim == 128), DLLM_EUNSUPPORTED, "fp32 path needs head_dim 64 or 128");
   require(n_weights == 3 + 9 * c.n_layers, DLLM_EINVAL, "n_weights must be 3 + 9 * n_layers");
   for (int i = 0; i < n_weights; ++i) require(weights[i] != nullptr, DLLM_EINVAL, "NULL weight pointer");
+  if (c.dtype == DLLM_BF16)
+    require(head_bf16_packed_bytes(c.vocab, c.d_model) <= 0x7fffffffu, DLLM_EUNSUPPORTED,
+            "bf16 LM head larger than 2 GiB");
   auto* m = new dllm_model();
   m->cfg = c;
   m->w.assign(weights, weights + n_weights);
-  hipError_t e = hipHostMalloc((void**)&m->pinned_flag, sizeof(int32_t), hipHostMallocDefault);
-  if (e != hipSuccess) {
+  try {
+    hip_check(hipHostMalloc((void**)&m->pinned_flag, sizeof(int32_t), hipHostMallocDefault), "hipHostMalloc");
+    if (c.dtype == DLLM_BF16) {
+      // weights may still be in flight on any stream: wait, copy, wait
+      hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
+      hip_check(hipMalloc((void**)&m->head_tiled, head_bf16_packed_bytes(c.vocab, c.d_model)), "hipMalloc");
+      launch_pack_head_bf16(static_cast<const bf16_t*>(m->w[2 + 9 * c.n_layers]), m->head_tiled, c.vocab,
+                            c.d_model, nullptr);
+      hip_check(hipStreamSynchronize(nullptr), "hipStreamSynchronize");
+    }
+  } catch (...) {
+    if (m->head_tiled) (void)hipFree(m->head_tiled);
+    if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
     delete m;
-    hip_check(e, "hipHostMalloc");
+    throw;
   }
   *out = m;
   API_END
@@ -500,6 +515,7 @@ int dllm_model_destroy(dllm_model* m) {
     (void)hipEventDestroy(e.stop);
   }
   if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
+  if (m->head_tiled) (void)hipFree(m->head_tiled);
   delete m;
   API_END
 }

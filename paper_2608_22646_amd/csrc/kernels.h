@@ -60,12 +60,18 @@ size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi);
 void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int L, int Hq,
                       int Hkv, hipStream_t s);
 
+// The bf16 LM head is read from a tiled copy: vocabulary tiles of HEAD_TILE rows,
+// each stored as d/64 consecutive [HEAD_TILE, 64] blocks, rows past V zero.
+constexpr int HEAD_TILE = 256;
+size_t head_bf16_packed_bytes(int V, int d);
+void launch_pack_head_bf16(const bf16_t* W, bf16_t* Wt, int V, int d, hipStream_t s);
+
 struct HeadArgs {
   const bf16_t* hb;   // [R, d]
-  const bf16_t* W;    // [V, d]
+  const bf16_t* W;    // tiled copy of the [V, d] LM head (launch_pack_head_bf16)
   int R, V, d, mask_id;
   float* conf; int32_t* argmax; float* logits;  // logits optional
-  float* part_m; float* part_s; int32_t* part_i;  // [n_tiles, R]
+  float* part_m; float* part_s; int32_t* part_i;  // [head_bf16_tiles(V), R]: one slot per workgroup
   int* ticket;                                    // zero before the first launch; left zero
 };
 void launch_head_bf16(const HeadArgs& a, hipStream_t s);
