@@ -25,11 +25,15 @@ namespace {
 constexpr int HD = 128, KT = 64, QW = 32, NW = 4;
 constexpr int K_BYTES = KT * HD * 2, V_BYTES = HD * KT * 2, STAGE = K_BYTES + V_BYTES;
 
+// XOR swizzles sized for the 64 banks (256 bytes) that one 16-lane pass of
+// ds_read_b128 covers: sixteen consecutive K rows (256 B each) put a given
+// chunk in sixteen different slots; sixteen consecutive V^T rows (128 B, two
+// per bank line) put it in eight slots of each line parity.
 __device__ __forceinline__ int k_off(int key, int chunk) {  // rows of 256 B, 16 chunks
-  return key * 256 + ((chunk ^ (key & 7)) << 4);
+  return key * 256 + ((chunk ^ (key & 15)) << 4);
 }
 __device__ __forceinline__ int v_off(int d, int chunk) {  // rows of 128 B, 8 chunks
-  return K_BYTES + d * 128 + ((chunk ^ (d & 7)) << 4);
+  return K_BYTES + d * 128 + ((chunk ^ ((d >> 1) & 7)) << 4);
 }
 
 __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
@@ -237,9 +241,9 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
   }
 
   // DMA: K instruction i fills keys 4i..4i+3 (rows of 256 B, lane l -> key
-  // 4i + l/16, slot l%16 holding chunk (l%16) ^ (key & 7)); V^T instruction i
+  // 4i + l/16, slot l%16 holding chunk (l%16) ^ (key & 15)); V^T instruction i
   // fills d rows 8i..8i+7 (rows of 128 B, lane l -> d = 8i + l/8, slot l%8
-  // holding chunk (l%8) ^ (d & 7)).  Wave w issues instructions w, w + NW, ...
+  // holding chunk (l%8) ^ ((d >> 1) & 7)).  Wave w issues instructions w, w + NW, ...
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, 0, L * HD * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, 0, HD * L * 2, 0x00020000);
   constexpr int PK = 16 / NW;
@@ -247,9 +251,9 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
 #pragma unroll
   for (int j = 0; j < PK; ++j) {
     const int i = wave + NW * j;
-    const int key = 4 * i + (lane >> 4), kc = (lane & 15) ^ (key & 7);
+    const int key = 4 * i + (lane >> 4), kc = (lane & 15) ^ (key & 15);
     vok[j] = (uint32_t)((key * HD + kc * 8) * 2);
-    const int d = 8 * i + (lane >> 3), vc = (lane & 7) ^ (d & 7);
+    const int d = 8 * i + (lane >> 3), vc = (lane & 7) ^ ((d >> 1) & 7);
     vov[j] = (uint32_t)(((size_t)d * L + vc * 8) * 2);
   }
   auto issue = [&](int t) {

@@ -17,8 +17,8 @@
 // Bv stream from memory straight into a 3-stage LDS ring (buffer_load_dwordx4 ...
 // lds, no staging registers): two k-tiles are in flight while the third is
 // consumed, with one barrier per k-step.  LDS rows are 128 bytes (64 bf16); the
-// 16-byte chunk c of row r is stored at slot c ^ (r & 7), so the eight rows read
-// by eight consecutive lanes hit eight different bank groups.
+// 16-byte chunk c of row r is stored at slot c ^ ((r >> 1) & 7), so the sixteen
+// rows read by sixteen consecutive lanes cover all 64 LDS banks.
 //
 // MFMA register layouts (64 lanes, lane = l):
 //   A operand : row l%32, k = 8*(l/32) .. +7       B operand : col l%32, same k
@@ -51,7 +51,10 @@ __device__ __forceinline__ int2 vrow(const GemmArgs& g, int n) {
   return make_int2(0, n);
 }
 
-__device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ (row & 7)) << 4); }
+// 16-byte chunk c of 128-byte LDS row r lives in slot c ^ ((r >> 1) & 7): the
+// 16 consecutive rows that one 16-lane pass of ds_read_b128 touches then cover
+// all 64 banks (two rows per 256-byte bank line, eight slots each).
+__device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4); }
 
 template <int BM_, int BN_, int WAVES_M, int WAVES_N, int STAGES_>
 struct Tile {
@@ -63,6 +66,7 @@ struct Tile {
   static constexpr int LDS_STAGE = (BM + BN) * 128;
   static_assert(WN == 128, "the QKV and SwiGLU epilogues need 128-column wave tiles");
   static_assert(IA * NW * 8 == BM && IB * NW * 8 == BN, "tile rows must split evenly over the DMA loads");
+  static_assert(NW % 2 == 0, "the DMA swizzle assumes an even wave count");
 };
 // 128 x 256, 4 waves of 64 x 128, three stages (small M: more tiles to spread over 256 CUs)
 using TileS = Tile<128, 256, 2, 2, 3>;
@@ -80,6 +84,13 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// The same with lgkmcnt(0): this wave's LDS reads (and writes) have completed.
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
 // Workgroup barrier without the memory-model fence of __syncthreads (which
 // would wait for every in-flight LDS-DMA load); the asm clobbers keep the
 // compiler from moving memory operations across it.  Callers wait for their
@@ -90,40 +101,35 @@ __device__ __forceinline__ void barrier_nofence() {
   asm volatile("" ::: "memory");
 }
 
-template <class TL, int EPI>
-__global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
-  // The buffer-resource builtins exist only for the device target; the host
-  // pass needs just the kernel's signature for its launch stub.
-#if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int BM = TL::BM, BN = TL::BN, S = TL::S, NW = TL::NW;
-  extern __shared__ __attribute__((aligned(16))) char lds[];
-  // wave index made provably uniform so per-wave buffer descriptors stay scalar
-  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / (BN / TL::WN), wn = wave % (BN / TL::WN);
-
-  // XCD-aware, grouped tile order.  Workgroup i runs on XCD i % 8, so each XCD
-  // takes a contiguous run of the tile order; the order walks groups of up to
-  // GM M-tiles across all N-tiles, so the ~32 tiles an XCD runs at once share
-  // a few A tiles and a few weight tiles in that XCD's L2.
+// XCD-aware, grouped tile order: linear position lin -> tile origin (m0, n0).
+// The order walks groups of up to GM M-tiles across all N-tiles, so tiles that
+// run together share a few A tiles and a few weight tiles in L2.
+template <class TL>
+__device__ __forceinline__ int2 tile_origin(const GemmArgs& g, int lin) {
   constexpr int GM = 8;
-  const int mt = (g.M + BM - 1) / BM, ntl = g.N / BN;
-  const int tiles = mt * ntl;
-  int lin = blockIdx.x;
-  if ((tiles & 7) == 0) lin = (blockIdx.x & 7) * (tiles >> 3) + (blockIdx.x >> 3);
+  const int mt = (g.M + TL::BM - 1) / TL::BM, ntl = g.N / TL::BN;
   const int grp = lin / (GM * ntl), first_m = grp * GM, gsize = min(mt - first_m, GM);
   const int in_grp = lin - grp * GM * ntl;
-  const int m0 = (first_m + in_grp % gsize) * BM, n0 = (in_grp / gsize) * BN;
+  return make_int2((first_m + in_grp % gsize) * TL::BM, (in_grp / gsize) * TL::BN);
+}
 
-  const int ksplit = g.K / gridDim.z;
-  const int kbeg = blockIdx.z * ksplit;
-  const int nk = ksplit / BK;
+// acc += A[m0 : m0+BM, k] * Bv[n0 : n0+BN, k]^T over the k-steps kt0 .. kt0+nk-1
+// (64 wide), streamed through the S-stage LDS ring.  Starts with a barrier, so
+// the ring may still be in use by a previous call; leaves no load in flight.
+template <class TL, int EPI>
+__device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave, int lane, int m0, int n0, int kt0,
+                                         int nk, f32x16_t (&acc)[TL::TI][TL::TJ]) {
+  constexpr int BM = TL::BM, BN = TL::BN, S = TL::S, NW = TL::NW;
+  const int wm = wave / (BN / TL::WN), wn = wave % (BN / TL::WN);
+  const int kbeg = kt0 * BK;
 
   // LDS-DMA loads: instruction i of wave w fills tile rows 8 (NW i + w) .. +7
   // (1 KiB of LDS).  Lane l writes row + l/8, slot l%8, which holds the row's
-  // logical 16-byte chunk (l%8) ^ (l/8) (the XOR swizzle, since row % 8 == l/8).
+  // logical 16-byte chunk (l%8) ^ ((row >> 1) & 7); with NW even, row >> 1
+  // = 4 (w & 1) + (l/8) / 2 modulo 8, the same for every i.
   // Row offsets are fixed across k; the k advance goes in the scalar offset.
   // A rows past M are clamped to M-1 (their results are never stored).
-  const int lr = lane >> 3, lc = (lane & 7) ^ (lane >> 3);
+  const int lr = lane >> 3, lc = (lane & 7) ^ (((wave & 1) << 2) | (lr >> 1));
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, 0x7fffffff, 0x00020000);
   uint32_t voa[TL::IA];
 #pragma unroll
@@ -155,61 +161,71 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
                                                vob[i], soff, 0, 0);
   };
 
-  f32x16_t acc[TL::TI][TL::TJ];
+  constexpr int PER_STAGE = TL::IA + TL::IB;  // DMA instructions per wave per stage
+  constexpr int NS = BK / 16, NF = TL::TI + TL::TJ, NM = TL::TI * TL::TJ;
+  static_assert(NM >= NF && NS % 2 == 0, "pipeline needs at least as many MFMAs as fragment reads per slice");
+  const int lrow = lane & 31, lhalf = lane >> 5;
+
+  // Fragments of the four 16-wide k-slices of a tile go through two register
+  // sets: slice ks + 1 is read while the MFMAs of slice ks run.  The barrier
+  // that publishes tile kt + 1 sits before the last slice of tile kt, so the
+  // first fragments of tile kt + 1 are read under that slice's MFMAs and the
+  // k-step boundary costs no exposed LDS latency; the slot tile kt occupied is
+  // refilled (tile kt + S) right after that barrier.
+  bf16x8_t af[2][TL::TI], bfr[2][TL::TJ];
+  auto frag = [&](const char* base, int ks) {
+    const int ch = ks * 2 + lhalf, set = ks & 1;
 #pragma unroll
-  for (int i = 0; i < TL::TI; ++i)
+    for (int i = 0; i < TL::TI; ++i)
+      af[set][i] = *reinterpret_cast<const bf16x8_t*>(base + swz(wm * TL::WM + i * 32 + lrow, ch));
 #pragma unroll
     for (int j = 0; j < TL::TJ; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      bfr[set][j] = *reinterpret_cast<const bf16x8_t*>(base + BM * 128 + swz(wn * TL::WN + j * 32 + lrow, ch));
+  };
 
-  constexpr int PER_STAGE = TL::IA + TL::IB;  // DMA instructions per wave per stage
+  wait_vm_lds<0>();
+  barrier_nofence();  // every wave is done with the ring's previous contents
 #pragma unroll
-  for (int s = 0; s < S - 1; ++s)
+  for (int s = 0; s < S; ++s)
     if (s < nk) issue(s);
+  // this wave's loads of tile 0 are done once only the later tiles' are outstanding
+  if (nk >= S)
+    wait_vm_lds<PER_STAGE * (S - 1)>();
+  else
+    wait_vm_lds<0>();
+  barrier_nofence();
+  frag(lds, 0);
 
-  const int lrow = lane & 31, lhalf = lane >> 5;
   for (int kt = 0; kt < nk; ++kt) {
-    // tile kt has landed once only the later tiles' loads are outstanding
-    if (kt + 1 < nk)
-      wait_vmcnt<PER_STAGE * (S - 2)>();
-    else
-      wait_vmcnt<0>();
-    barrier_nofence();  // tile kt visible to all waves; stage (kt - 1) % S free
-    if (kt + S - 1 < nk) issue(kt + S - 1);
     const char* base = lds + (kt % S) * TL::LDS_STAGE;
-    // Software pipeline over the four 16-wide k-slices: slices 0 and 1 are read
-    // first, then each MFMA of slice ks is followed by one LDS read of slice
-    // ks + 2 (three fragment register sets), so LDS latency hides under the
-    // MFMAs.  The sched_group_barrier sequence pins that order.
-    constexpr int NS = BK / 16, NF = TL::TI + TL::TJ, NM = TL::TI * TL::TJ;
-    static_assert(NM >= NF, "pipeline needs at least as many MFMAs as fragment reads per slice");
-    bf16x8_t af[3][TL::TI], bfr[3][TL::TJ];
-    auto frag = [&](int ks) {
-      const int ch = ks * 2 + lhalf, set = ks % 3;
-#pragma unroll
-      for (int i = 0; i < TL::TI; ++i)
-        af[set][i] = *reinterpret_cast<const bf16x8_t*>(base + swz(wm * TL::WM + i * 32 + lrow, ch));
-#pragma unroll
-      for (int j = 0; j < TL::TJ; ++j)
-        bfr[set][j] = *reinterpret_cast<const bf16x8_t*>(base + BM * 128 + swz(wn * TL::WN + j * 32 + lrow, ch));
-    };
-    frag(0);
-    frag(1);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NF, 0);
 #pragma unroll
     for (int ks = 0; ks < NS; ++ks) {
-      if (ks + 2 < NS) frag(ks + 2);
+      bool next = false;
+      if (ks + 1 < NS) {
+        frag(base, ks + 1);
+        next = true;
+      } else if (kt + 1 < nk) {
+        // tile kt + 1 has landed once only tiles kt + 2 .. kt + S - 1 are
+        // outstanding; every LDS read of tile kt has completed (lgkmcnt 0)
+        if (kt + S - 1 < nk)
+          wait_vm_lds<PER_STAGE * (S - 2)>();
+        else
+          wait_vm_lds<0>();
+        barrier_nofence();  // tile kt + 1 visible to all waves; slot kt % S free
+        if (kt + S < nk) issue(kt + S);
+        frag(lds + ((kt + 1) % S) * TL::LDS_STAGE, 0);
+        next = true;
+      }
 #pragma unroll
       for (int i = 0; i < TL::TI; ++i)
 #pragma unroll
         for (int j = 0; j < TL::TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks % 3][i], bfr[ks % 3][j], acc[i][j], 0, 0, 0);
-      if (ks + 2 < NS) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks & 1][i], bfr[ks & 1][j], acc[i][j], 0, 0, 0);
+      if (next) {
 #pragma unroll
         for (int x = 0; x < NF; ++x) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA of slice ks
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read of slice ks + 2
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one fragment read of the next slice
         }
         __builtin_amdgcn_sched_group_barrier(0x008, NM - NF, 0);
       } else {
@@ -217,112 +233,164 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
       }
     }
   }
+}
 
-  // ------------------------------------------------------------ epilogues
-  const int col_in = lane & 31;
-  auto row_of = [&](int i, int r) { return m0 + wm * TL::WM + i * 32 + 8 * (r >> 2) + 4 * lhalf + (r & 3); };
-
-  if (gridDim.z > 1) {  // split-K partial tile
-    float* part = g.splitk_buf + (size_t)blockIdx.z * g.M * g.N;
-#pragma unroll
-    for (int i = 0; i < TL::TI; ++i)
-#pragma unroll
-      for (int j = 0; j < TL::TJ; ++j) {
-        const int n = n0 + wn * TL::WN + j * 32 + col_in;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = row_of(i, r);
-          if (m < g.M) part[(size_t)m * g.N + n] = acc[i][j][r];
-        }
-      }
-    return;
-  }
+// Epilogue of one unit of a tile: the accumulator rows 8c .. 8c+7 ... that a
+// lane holds for row block i, i.e. v[j][e] = acc[i][j][4c + e] for the TJ = 4
+// column blocks j of the wave (rows 8c + 4 (lane/32) + e, columns j*32 + lane%32
+// of the wave's 32-row x 128-column block i).
+template <class TL, int EPI>
+__device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, int m0, int n0, int i, int c,
+                                         const float (&v)[TL::TJ][4]) {
+  static_assert(TL::TJ == 4, "epilogues need 128-column wave tiles");
+  const int wm = wave / (TL::BN / TL::WN), wn = wave % (TL::BN / TL::WN);
+  const int lhalf = lane >> 5, col_in = lane & 31;
+  const int mrow = m0 + wm * TL::WM + i * 32 + 8 * c + 4 * lhalf;  // + e
+  const int ncol0 = n0 + wn * TL::WN;                               // + j*32 + col_in
 
   if (EPI == EPI_RESID || EPI == EPI_STORE) {
 #pragma unroll
-    for (int i = 0; i < TL::TI; ++i)
+    for (int e = 0; e < 4; ++e) {
+      const int m = mrow + e;
+      if (m >= g.M) continue;
 #pragma unroll
-      for (int j = 0; j < TL::TJ; ++j) {
-        const int n = n0 + wn * TL::WN + j * 32 + col_in;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = row_of(i, r);
-          if (m >= g.M) continue;
-          if (EPI == EPI_RESID)
-            g.resid[(size_t)m * g.N + n] += acc[i][j][r];
-          else
-            g.out[(size_t)m * g.N + n] = f2bf(acc[i][j][r]);
-        }
+      for (int j = 0; j < 4; ++j) {
+        const int n = ncol0 + j * 32 + col_in;
+        if (EPI == EPI_RESID)
+          g.resid[(size_t)m * g.N + n] += v[j][e];
+        else
+          g.out[(size_t)m * g.N + n] = f2bf(v[j][e]);
       }
+    }
     return;
   }
 
-  if (EPI == EPI_SWIGLU) {
+  if (EPI == EPI_SWIGLU) {  // column blocks alternate gate, up: (0, 1) and (2, 3) pair
     const int F = g.N / 2;
 #pragma unroll
-    for (int i = 0; i < TL::TI; ++i)
+    for (int e = 0; e < 4; ++e) {
+      const int m = mrow + e;
+      if (m >= g.M) continue;
 #pragma unroll
-      for (int j = 0; j < TL::TJ; j += 2) {
-        const int chunk = (n0 + wn * TL::WN + j * 32) >> 5;  // even: gate, odd (j+1): up
+      for (int j = 0; j < 4; j += 2) {
+        const int chunk = (ncol0 + j * 32) >> 5;  // even: gate
         const int f = ((chunk >> 1) << 5) + col_in;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = row_of(i, r);
-          if (m >= g.M) continue;
-          const float gt = acc[i][j][r], up = acc[i][j + 1][r];
-          g.out[(size_t)m * F + f] = f2bf(gt / (1.0f + expf(-gt)) * up);
-        }
+        const float gt = v[j][e], up = v[j + 1][e];
+        g.out[(size_t)m * F + f] = f2bf(gt / (1.0f + expf(-gt)) * up);
       }
+    }
     return;
   }
 
   // EPI_QKV_ROPE: this wave's 128 columns are exactly one head (hd = 128).
   if (EPI == EPI_QKV_ROPE) {
     constexpr int HD = 128, HALF = 64;
-    const int ncol0 = n0 + wn * TL::WN;  // multiple of 128
     const int nq = g.Hq * HD, nk_ = g.Hkv * HD;
-    static_assert(TL::TJ == 4, "QKV epilogue needs 128-column wave tiles");
     if (ncol0 < nq + nk_) {
       const bool isq = ncol0 < nq;
       const int head = isq ? ncol0 / HD : (ncol0 - nq) / HD;
       const int H = isq ? g.Hq : g.Hkv;
       bf16_t* dst = isq ? g.q : g.k;
 #pragma unroll
-      for (int i = 0; i < TL::TI; ++i)
+      for (int e = 0; e < 4; ++e) {
+        const int m = mrow + e;
+        if (m >= g.M) continue;
+        const int b = m / g.L, pos = m - b * g.L;
+        bf16_t* o = dst + (((size_t)b * H + head) * g.L + pos) * HD;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          const int jj = j * 32 + col_in;  // < 64: pairs with jj + 64 (register tile j + 2)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int m = row_of(i, r);
-            if (m >= g.M) continue;
-            const int b = m / g.L, pos = m - b * g.L;
-            const float c = g.cosb[(size_t)pos * HALF + jj], sn = g.sinb[(size_t)pos * HALF + jj];
-            const float x1 = acc[i][j][r], x2 = acc[i][j + 2][r];
-            bf16_t* o = dst + (((size_t)b * H + head) * g.L + pos) * HD;
-            o[jj] = f2bf(x1 * c - x2 * sn);
-            o[jj + HALF] = f2bf(x2 * c + x1 * sn);
-          }
+          const int jj = j * 32 + col_in;  // < 64: pairs with jj + 64 (column block j + 2)
+          const float cs = g.cosb[(size_t)pos * HALF + jj], sn = g.sinb[(size_t)pos * HALF + jj];
+          const float x1 = v[j][e], x2 = v[j + 2][e];
+          o[jj] = f2bf(x1 * cs - x2 * sn);
+          o[jj + HALF] = f2bf(x2 * cs + x1 * sn);
         }
+      }
     } else {
       const int head = (ncol0 - nq - nk_) / HD;
 #pragma unroll
-      for (int i = 0; i < TL::TI; ++i)
+      for (int e = 0; e < 4; ++e) {
+        const int m = mrow + e;
+        if (m >= g.M) continue;
+        const int b = m / g.L, pos = m - b * g.L;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int cj = j * 32 + col_in;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int m = row_of(i, r);
-            if (m >= g.M) continue;
-            const int b = m / g.L, pos = m - b * g.L;
-            // v is a bf16 value; it is stored as IEEE half (exact in half's range)
-            // for the half-precision P.V product of the attention kernel
-            g.vt[(((size_t)b * g.Hkv + head) * HD + cj) * g.L + pos] = f2h(bf2f(f2bf(acc[i][j][r])));
-          }
+          // v is a bf16 value; it is stored as IEEE half (exact in half's range)
+          // for the half-precision P.V product of the attention kernel
+          g.vt[(((size_t)b * g.Hkv + head) * HD + cj) * g.L + pos] = f2h(bf2f(f2bf(v[j][e])));
         }
+      }
     }
   }
+}
+
+// Writes the finished tile at (m0, n0) from the accumulators.
+template <class TL, int EPI>
+__device__ __forceinline__ void epilogue(const GemmArgs& g, int wave, int lane, int m0, int n0,
+                                         const f32x16_t (&acc)[TL::TI][TL::TJ]) {
+#pragma unroll
+  for (int i = 0; i < TL::TI; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      float v[TL::TJ][4];
+#pragma unroll
+      for (int j = 0; j < TL::TJ; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[j][e] = acc[i][j][4 * c + e];
+      epi_unit<TL, EPI>(g, wave, lane, m0, n0, i, c, v);
+    }
+}
+
+template <class TL>
+__device__ __forceinline__ void zero_acc(f32x16_t (&acc)[TL::TI][TL::TJ]) {
+#pragma unroll
+  for (int i = 0; i < TL::TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::TJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+}
+
+// One workgroup per output tile (grid.x), optionally split over K (grid.z:
+// float32 partial tiles, summed by splitk_resid_kernel).
+template <class TL, int EPI>
+__global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
+  // The buffer-resource builtins exist only for the device target; the host
+  // pass needs just the kernel's signature for its launch stub.
+#if defined(__HIP_DEVICE_COMPILE__)
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  // wave index made provably uniform so per-wave buffer descriptors stay scalar
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tiles = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
+  // workgroup i runs on XCD i % 8: give each XCD a contiguous run of the order
+  int lin = blockIdx.x;
+  if ((tiles & 7) == 0) lin = (blockIdx.x & 7) * (tiles >> 3) + (blockIdx.x >> 3);
+  const int2 o = tile_origin<TL>(g, lin);
+  const int nk = g.K / gridDim.z / BK;
+
+  f32x16_t acc[TL::TI][TL::TJ];
+  zero_acc<TL>(acc);
+  mma_tile<TL, EPI>(g, lds, wave, lane, o.x, o.y, blockIdx.z * nk, nk, acc);
+
+  if (gridDim.z > 1) {  // split-K partial tile
+    const int wm = wave / (TL::BN / TL::WN), wn = wave % (TL::BN / TL::WN);
+    const int lhalf = lane >> 5, col_in = lane & 31;
+    float* part = g.splitk_buf + (size_t)blockIdx.z * g.M * g.N;
+#pragma unroll
+    for (int i = 0; i < TL::TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TL::TJ; ++j) {
+        const int n = o.y + wn * TL::WN + j * 32 + col_in;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = o.x + wm * TL::WM + i * 32 + 8 * (r >> 2) + 4 * lhalf + (r & 3);
+          if (m < g.M) part[(size_t)m * g.N + n] = acc[i][j][r];
+        }
+      }
+    return;
+  }
+  epilogue<TL, EPI>(g, wave, lane, o.x, o.y, acc);
 #endif
 }
 
@@ -382,11 +450,11 @@ void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
 }
 
 template <int EPI>
-void launch_epi(const GemmArgs& g, int bm, int split, hipStream_t s) {
-  if (bm == 256)
-    launch_tile<TileL, EPI>(g, split, s);
+void launch_epi(const GemmArgs& g, const Plan& p, hipStream_t s) {
+  if (p.bm == 256)
+    launch_tile<TileL, EPI>(g, p.split, s);
   else
-    launch_tile<TileS, EPI>(g, split, s);
+    launch_tile<TileS, EPI>(g, p.split, s);
 }
 
 }  // namespace
@@ -403,9 +471,9 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
     throw HipError("gemm_bf16: q and k/v regions must be multiples of 256 rows");
   const Plan p = plan(a.M, a.N, a.K, a.epi);
   switch (a.epi) {
-    case EPI_QKV_ROPE: launch_epi<EPI_QKV_ROPE>(a, p.bm, p.split, s); break;
-    case EPI_SWIGLU: launch_epi<EPI_SWIGLU>(a, p.bm, p.split, s); break;
-    case EPI_RESID: launch_epi<EPI_RESID>(a, p.bm, p.split, s); break;
+    case EPI_QKV_ROPE: launch_epi<EPI_QKV_ROPE>(a, p, s); break;
+    case EPI_SWIGLU: launch_epi<EPI_SWIGLU>(a, p, s); break;
+    case EPI_RESID: launch_epi<EPI_RESID>(a, p, s); break;
     default: throw HipError("gemm_bf16: unknown epilogue");
   }
   DLLM_LAUNCH_CHECK("gemm_bf16");

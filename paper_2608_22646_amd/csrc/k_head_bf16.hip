@@ -73,7 +73,10 @@ __device__ __forceinline__ void barrier_nofence_h() {
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
-__device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ (row & 7)) << 4); }
+// 16-byte chunk c of 128-byte LDS row r lives in slot c ^ ((r >> 1) & 7): the
+// 16 consecutive rows that one 16-lane pass of ds_read_b128 touches then cover
+// all 64 banks (two rows per 256-byte bank line, eight slots each).
+__device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4); }
 
 template <int RG, int VT, int NW, int S>
 __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
@@ -98,8 +101,9 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
   const int units = my_tiles * nk;
 
   // DMA sources: instruction i of wave w fills rows 8 (NW i + w) .. +7 of the
-  // slice; lane l loads row + l/8, logical chunk (l%8) ^ (l/8) into slot l%8.
-  const int dr = lane >> 3, dc = (lane & 7) ^ (lane >> 3);
+  // slice; lane l loads row + l/8, logical chunk (l%8) ^ ((row >> 1) & 7) into
+  // slot l%8 (NW even: row >> 1 = 4 (w & 1) + (l/8) / 2 modulo 8 for every i).
+  const int dr = lane >> 3, dc = (lane & 7) ^ (((wave & 1) << 2) | (dr >> 1));
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc((void*)a.hb, 0, 0x7fffffff, 0x00020000);
   uint32_t voh[IH_HI];
@@ -276,16 +280,6 @@ __global__ void pack_head_kernel(const bf16_t* __restrict__ W, bf16_t* __restric
   }
 }
 
-int num_cus() {
-  static const int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-    return n;
-  }();
-  return cus;
-}
 
 // one launch shape: RG groups of 32 head rows, vocabulary tiles of VT rows on
 // NW waves, an S-stage ring
@@ -299,7 +293,7 @@ struct HeadCfg {
   static int ntiles(int V) { return (V + HEAD_TILE - 1) / HEAD_TILE * (HEAD_TILE / VT); }
   static int grid(int V) {
     const int per_cu = 2 * lds_all <= 160 * 1024 ? 2 : 1;
-    return std::min(std::min(ntiles(V), num_cus() * per_cu), MAX_WG);
+    return std::min(std::min(ntiles(V), device_cu_count() * per_cu), MAX_WG);
   }
   static void launch(const HeadArgs& a, hipStream_t s) {
     static const hipError_t attr = hipFuncSetAttribute((const void*)head_bf16_kernel<RG, VT, NW, S>,

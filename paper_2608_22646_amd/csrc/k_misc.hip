@@ -3,6 +3,17 @@
 
 namespace dllm {
 
+int device_cu_count() {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    return n;
+  }();
+  return cus;
+}
+
 // One 256-thread block per row; every thread converts a strided set of columns.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ x, const T* __restrict__ E,
@@ -68,15 +79,91 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
   for (int c = threadIdx.x; c < d; c += 256) Act<TO>::store(dst, c, src[c] * rstd * Act<TG>::load(g, c));
 }
 
+// Vector form of the same computation for d % 4 == 0 and d <= 1024 NV: the
+// row is read once, as float4, into registers (NV per thread) and written from
+// there.  The float64 sum of squares runs over a different fixed order; its
+// float32 result is the same in all but astronomically rare ties.
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+  static __device__ __forceinline__ float4 load(const float* p, int c4) { return reinterpret_cast<const float4*>(p)[c4]; }
+  static __device__ __forceinline__ void store(float* p, int c4, float4 v) { reinterpret_cast<float4*>(p)[c4] = v; }
+};
+template <> struct Vec4<bf16_t> {
+  static __device__ __forceinline__ float4 load(const bf16_t* p, int c4) {
+    const uint2 u = reinterpret_cast<const uint2*>(p)[c4];
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+  }
+  static __device__ __forceinline__ void store(bf16_t* p, int c4, float4 v) {
+    uint2 u;
+    u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+    u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+    reinterpret_cast<uint2*>(p)[c4] = u;
+  }
+};
+
+template <typename TG, typename TO, int NV>
+__global__ void __launch_bounds__(256) rmsnorm_vec_kernel(const float* __restrict__ h, const TG* __restrict__ g,
+                                                          TO* __restrict__ out, int rows, int L, int row0, int d,
+                                                          float eps) {
+  const int r = blockIdx.x;
+  const int b = r / rows, i = r % rows;
+  const float* src = h + ((size_t)b * L + row0 + i) * d;
+  const int d4 = d / 4;
+  float4 v[NV];
+  double ss = 0.0;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int c = threadIdx.x + 256 * j;
+    if (c < d4) {
+      v[j] = Vec4<float>::load(src, c);
+      ss += (double)v[j].x * v[j].x + (double)v[j].y * v[j].y + (double)v[j].z * v[j].z + (double)v[j].w * v[j].w;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  __shared__ double part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const double tot = (part[0] + part[1]) + (part[2] + part[3]);
+  const float rstd = (float)(1.0 / sqrt(tot / (double)d + (double)eps));
+  TO* dst = out + (size_t)r * d;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int c = threadIdx.x + 256 * j;
+    if (c < d4) {
+      const float4 gg = Vec4<TG>::load(g, c);
+      Vec4<TO>::store(dst, c,
+                      make_float4(v[j].x * rstd * gg.x, v[j].y * rstd * gg.y, v[j].z * rstd * gg.z, v[j].w * rstd * gg.w));
+    }
+  }
+}
+
+template <typename TG, typename TO>
+void launch_rmsnorm_t(const float* h, const TG* g, TO* out, int B, int rows, int L, int row0, int d, float eps,
+                      hipStream_t s) {
+  const dim3 grid(B * rows), blk(256);
+  const bool aligned = ((uintptr_t)h | (uintptr_t)g | (uintptr_t)out) % 16 == 0;
+  if (d % 4 == 0 && aligned && d <= 1024 * 8) {
+    const int nv = ceil_div(d, 1024);
+    if (nv <= 2)
+      hipLaunchKernelGGL((rmsnorm_vec_kernel<TG, TO, 2>), grid, blk, 0, s, h, g, out, rows, L, row0, d, eps);
+    else if (nv <= 4)
+      hipLaunchKernelGGL((rmsnorm_vec_kernel<TG, TO, 4>), grid, blk, 0, s, h, g, out, rows, L, row0, d, eps);
+    else
+      hipLaunchKernelGGL((rmsnorm_vec_kernel<TG, TO, 8>), grid, blk, 0, s, h, g, out, rows, L, row0, d, eps);
+  } else {
+    hipLaunchKernelGGL((rmsnorm_kernel<TG, TO>), grid, blk, 0, s, h, g, out, rows, L, row0, d, eps);
+  }
+}
+
 void launch_rmsnorm(const float* h, const void* g, void* out, int dtype, int B, int rows, int L, int row0, int d,
                     float eps, hipStream_t s) {
   if (B * rows == 0) return;
   if (dtype == 0)
-    hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(B * rows), dim3(256), 0, s, h, (const float*)g,
-                       (float*)out, rows, L, row0, d, eps);
+    launch_rmsnorm_t(h, (const float*)g, (float*)out, B, rows, L, row0, d, eps, s);
   else
-    hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t>), dim3(B * rows), dim3(256), 0, s, h, (const bf16_t*)g,
-                       (bf16_t*)out, rows, L, row0, d, eps);
+    launch_rmsnorm_t(h, (const bf16_t*)g, (bf16_t*)out, B, rows, L, row0, d, eps, s);
   DLLM_LAUNCH_CHECK("rmsnorm");
 }
 

@@ -53,6 +53,7 @@ struct GemmArgs {
   // split-K scratch (float32 partials [split, M, N]) from the workspace
   float* splitk_buf;
 };
+int device_cu_count();  // compute units of the current device (256 if it cannot be queried)
 void launch_gemm_bf16(const GemmArgs& a, hipStream_t s);
 // Bytes of split-K scratch a launch of this shape needs (0 if it does not split).
 size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi);
