@@ -138,6 +138,48 @@ def cpu_baseline(cfg, weights, prompts, wl, forwards_per_gen, budget_s=25.0):
     }
 
 
+ABLATION_PRESETS = ["fixed_schedule", "cai", "cai_gate_off", "apd", "apd_block", "apd_block_budget",
+                    "fixed_threshold_0.9", "fixed_threshold_0.7", "apd_0.9_to_0.5"]
+
+
+def ablation(args):
+    """Forwards per decode and tokens/s of the workload under each controller
+    preset, after one warm-up decode each; step reduction is relative to the
+    fixed-schedule baseline (one token per step), as in Section 6's table."""
+    import torch
+    from paper_2608_22646_amd import binding as Bd
+    from paper_2608_22646_amd import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    cfg = wl.model
+    B, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
+    model = Bd.Model(cfg, synth.make_weights(cfg, "cuda"))
+    prompts = synth.make_prompts(wl, "cuda")
+    ws = model.workspace(B, P + G, bl)
+    st = Bd.DecodeState(B, P, G, "cuda")
+    rows = []
+    for name in ABLATION_PRESETS:
+        ctl = Bd.Controller.preset(name, block_len=bl)
+        model.generate(ctl, prompts, G, ws=ws, st=st)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        res = model.generate(ctl, prompts, G, ws=ws, st=st)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        rows.append({"preset": name, "forwards_per_decode": res.total_forwards, "forwards_per_block": res.forwards,
+                     "tokens_per_s": B * G / dt, "ms_per_decode": dt * 1e3})
+        log(f"{name}: {res.total_forwards} forwards {res.forwards}, {B * G / dt:.1f} tokens/s")
+    base = rows[0]["forwards_per_decode"]
+    for r in rows:
+        r["step_reduction_vs_fixed"] = 1.0 - r["forwards_per_decode"] / base
+        r["speedup_vs_fixed"] = r["tokens_per_s"] / rows[0]["tokens_per_s"]
+    print(json.dumps({"metric": "controller ablation: forwards per decode, tokens/s", "n_gpus": 1,
+                      "data": "synthetic (seeded random-init weights of the model shape, uniform random prompts)",
+                      "config": {"workload": f"{wl.name}: {cfg.name} random-init, batch {B}, prompt {P}, gen {G}, "
+                                             f"block {bl}"},
+                      "variants": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,6 +189,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=25.0)
     ap.add_argument("--copy-calib", action="store_true", help="run only the copy used to calibrate HBM counters")
+    ap.add_argument("--ablation", action="store_true",
+                    help="decode the workload under each controller preset (component ablation, fixed-threshold "
+                         "decoding, fixed-schedule baseline) and print one JSON line of forwards and tokens/s")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -155,6 +200,9 @@ def main():
 
     if args.copy_calib:
         copy_calibration()
+        return
+    if args.ablation:
+        ablation(args)
         return
 
     import torch

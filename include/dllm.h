@@ -67,7 +67,14 @@ enum {
   DLLM_F_BLOCK_SCHED = 1u, /* Box 4: theta_e^(b) decreases with the block index        */
   DLLM_F_POS = 2u,         /* Box 6: position factor and clip; off: theta_i = theta_b(t) */
   DLLM_F_BUDGET = 4u,      /* Box 5: per-token step budgets B_i                           */
-  DLLM_F_GRIND = 8u        /* Box 7: grinding detector and its fallback commit            */
+  DLLM_F_GRIND = 8u,       /* Box 7: grinding detector and its fallback commit            */
+  /* Fixed-schedule baseline (the "Fixed" column of Section 6's step-reduction
+   * table) instead of the confidence-aware rule: at local step t each sequence
+   * commits its floor(bl/T) masked tokens of highest confidence (one more in
+   * the first bl % T steps; equal confidence: lower position first; NaN ranks
+   * lowest), reason DLLM_R_FIXED.  s, budget and ell are left untouched; the
+   * other switches and the threshold constants are ignored. */
+  DLLM_F_FIXED = 16u
 };
 
 /*
@@ -110,7 +117,14 @@ typedef struct dllm_cai_params {
 } dllm_cai_params;
 
 /* Reason codes stored per committed token. */
-enum { DLLM_R_MASKED = 0, DLLM_R_THRESH = 1, DLLM_R_BUDGET = 2, DLLM_R_GRIND = 3, DLLM_R_FLUSH = 4 };
+enum {
+  DLLM_R_MASKED = 0,
+  DLLM_R_THRESH = 1,
+  DLLM_R_BUDGET = 2,
+  DLLM_R_GRIND = 3,
+  DLLM_R_FLUSH = 4,
+  DLLM_R_FIXED = 5
+};
 
 /*
  * Decoding state: all device pointers, caller-owned, updated in place.

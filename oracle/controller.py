@@ -27,9 +27,15 @@ where the paper is silent or inconsistent:
   R14 A batch advances in lockstep: each sequence keeps its own s, B, ell and
       done flag; a finished sequence is frozen; the block ends when every
       sequence has finished.
+  R19 The fixed-schedule baseline (the "Fixed" column of the step-reduction
+      table, Section 6: as many denoising steps as generated tokens) commits,
+      at local step t, the k_t masked tokens of highest confidence (lowest
+      position first on equal confidence), k_t = floor(bl/T) plus one in the
+      first bl mod T steps; with T = block_len that is one token per step.
+      A NaN confidence ranks below every number.  It keeps no s, B or ell.
 
 Reason codes per committed token: 1 threshold, 2 budget, 3 grinding
-fallback, 4 flush.
+fallback, 4 flush, 5 fixed schedule.
 
 Test infrastructure only; see the package docstring.
 """
@@ -38,7 +44,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-THRESH, BUDGET, GRIND_FB, FLUSH = 1, 2, 3, 4
+THRESH, BUDGET, GRIND_FB, FLUSH, FIXED = 1, 2, 3, 4, 5
 
 
 @dataclass
@@ -69,10 +75,17 @@ class CaiParams:
     pos_aware: bool = True            # Box 6 on (else theta_i = theta_b(t), no clip)
     budgets: bool = True              # Box 5 on   } confidence gating (Section 4.6)
     grinding: bool = True             # Box 7 on   }
+    fixed: bool = False               # fixed-schedule baseline instead (R19)
 
     @property
     def T(self):
         return self.steps_per_block or self.block_len
+
+
+def fixed_commits(t, p: CaiParams):
+    """k_t, the tokens the fixed schedule commits at local step t (R19)."""
+    base, extra = divmod(p.block_len, p.T)
+    return base + (1 if t < extra else 0)
 
 
 def block_end_threshold(b, p: CaiParams):
@@ -157,16 +170,29 @@ def step_sequence(st: DecodeState, seq, P, blk, t, conf, arg, ell, p: CaiParams)
     conf = np.asarray(conf, dtype=np.float32)
     masked = [st.commit_step[seq, g0 + i] < 0 for i in range(bl)]
 
-    if t == 0:                                            # step-zero init (Boxes 2, 5)
-        for i in range(bl):
-            st.s[seq, g0 + i] = conf[i]
-            st.budget[seq, g0 + i] = token_budget(conf[i], i, p)
-
     def commit(i, why):
         st.x[seq, P + g0 + i] = int(arg[i])
         st.commit_step[seq, g0 + i] = t
         st.reason[seq, g0 + i] = why
         masked[i] = False
+
+    if p.fixed:                                           # fixed-schedule baseline (R19)
+        key = lambda i: (-(float(conf[i]) if conf[i] == conf[i] else -math.inf), i)   # NaN ranks lowest
+        order = sorted((i for i in range(bl) if masked[i]), key=key)
+        for i in order[:fixed_commits(t, p)]:
+            commit(i, FIXED)
+        exited = not any(masked)
+        if not exited and t == p.T - 1:                   # flush (R1), unreachable when sum k_t = bl
+            for i in range(bl):
+                if masked[i]:
+                    commit(i, FLUSH)
+            exited = True
+        return ell, exited
+
+    if t == 0:                                            # step-zero init (Boxes 2, 5)
+        for i in range(bl):
+            st.s[seq, g0 + i] = conf[i]
+            st.budget[seq, g0 + i] = token_budget(conf[i], i, p)
 
     eta = 0                                               # threshold / budget commits
     for i in range(bl):

@@ -18,8 +18,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdllm.so")
 
 DLLM_F32, DLLM_BF16 = 0, 1
-F_BLOCK_SCHED, F_POS, F_BUDGET, F_GRIND = 1, 2, 4, 8
-R_MASKED, R_THRESH, R_BUDGET, R_GRIND, R_FLUSH = 0, 1, 2, 3, 4
+F_BLOCK_SCHED, F_POS, F_BUDGET, F_GRIND, F_FIXED = 1, 2, 4, 8, 16
+R_MASKED, R_THRESH, R_BUDGET, R_GRIND, R_FLUSH, R_FIXED = 0, 1, 2, 3, 4, 5
 PROF_GEMM, PROF_ATTN, PROF_HEAD, PROF_COMMIT, PROF_NORM, PROF_GATEUP = range(6)
 
 _c = ctypes
@@ -140,10 +140,33 @@ class Controller:
     pos_aware: bool = True
     budgets: bool = True
     grinding: bool = True
+    fixed: bool = False   # fixed-schedule baseline instead of the confidence rule
 
     @classmethod
     def gating(cls, on: bool, **kw):
         return cls(budgets=on, grinding=on, **kw)
+
+    @classmethod
+    def preset(cls, name: str, **kw):
+        """Named controller settings: the method with gating on / off (Section 4.6),
+        the component ablation of Section 6 (+APD, +Block, +Budget = the
+        per-token controls of Boxes 5-7), fixed-threshold decoding and the
+        fixed-schedule baseline.  Keyword arguments override fields."""
+        apd_only = dict(block_sched=False, pos_aware=False, budgets=False, grinding=False)
+        table = {
+            "cai": {},
+            "cai_gate_off": dict(budgets=False, grinding=False),
+            "apd": apd_only,
+            "apd_block": dict(pos_aware=False, budgets=False, grinding=False),
+            "apd_block_budget": {},
+            "fixed_threshold_0.9": dict(apd_only, theta_s=0.9, theta_e=0.9),
+            "fixed_threshold_0.7": dict(apd_only, theta_s=0.7, theta_e=0.7),
+            "apd_0.9_to_0.5": dict(apd_only, theta_s=0.9, theta_e=0.5),
+            "fixed_schedule": dict(fixed=True),
+        }
+        if name not in table:
+            raise KeyError(f"unknown controller preset {name!r}; known: {sorted(table)}")
+        return cls(**dict(table[name], **kw))
 
     def to_c(self) -> CaiParams:
         p = CaiParams()
@@ -154,7 +177,8 @@ class Controller:
         p.pos_edge[:] = list(self.pos_edges)
         p.pos_factor[:] = list(self.pos_factors)
         p.flags = ((F_BLOCK_SCHED if self.block_sched else 0) | (F_POS if self.pos_aware else 0)
-                   | (F_BUDGET if self.budgets else 0) | (F_GRIND if self.grinding else 0))
+                   | (F_BUDGET if self.budgets else 0) | (F_GRIND if self.grinding else 0)
+                   | (F_FIXED if self.fixed else 0))
         return p
 
     @property

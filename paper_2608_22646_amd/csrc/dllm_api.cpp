@@ -346,6 +346,8 @@ void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf
 // ---------------------------------------------------------------- controller
 void check_params(const dllm_cai_params* p) {
   require(p != nullptr, DLLM_EINVAL, "params is NULL");
+  require((p->flags & ~(uint32_t)(DLLM_F_BLOCK_SCHED | DLLM_F_POS | DLLM_F_BUDGET | DLLM_F_GRIND | DLLM_F_FIXED)) == 0,
+          DLLM_EINVAL, "unknown flag bits");
   require(p->block_len >= 1 && p->block_len <= 64, DLLM_EUNSUPPORTED, "block_len must be in [1, 64]");
   require(p->steps_per_block >= 0, DLLM_EINVAL, "steps_per_block must be >= 0");
   const double dv[] = {p->theta_s, p->theta_e, p->theta_e_step, p->theta_e_floor, p->warmup, p->clip_lo,
@@ -419,6 +421,8 @@ void fill_commit_args(const dllm_cai_params* p, dllm_state* st, CommitArgs* a, i
   a->eta_bar = p->eta_bar;
   a->patience = p->patience;
   a->theta_fb = p->theta_fb;
+  // fixed schedule: floor(bl / T) per step, one more in the first bl % T steps
+  a->fixed_k = (p->flags & DLLM_F_FIXED) ? p->block_len / T + (t < p->block_len % T ? 1 : 0) : 0;
 }
 
 void forward_all(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, float* conf,

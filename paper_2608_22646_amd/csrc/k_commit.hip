@@ -5,6 +5,11 @@
 // and the per-step count eta is a ballot + popcount.  Order inside the step:
 // threshold / budget commits, eta, low-yield counter, grinding fallback,
 // no-mask check, flush of what is still masked when the block ends.
+//
+// Fixed-schedule baseline (fixed_k > 0 this step): the wave commits its
+// fixed_k masked positions of highest confidence (lowest position first on
+// equal confidence; a NaN confidence ranks lowest), found by fixed_k butterfly
+// reductions; no s, B or ell is kept.
 #include "kernels.h"
 
 namespace dllm {
@@ -32,35 +37,66 @@ __global__ void __launch_bounds__(1024) commit_kernel(CommitArgs a) {
         masked = a.commit_step[sg] < 0;
         c = a.conf[(size_t)b * a.bl + p];
         tok = a.argmax[(size_t)b * a.bl + p];
-        if (a.t == 0) {  // Box 2 (s_i = c_i^(0)) and Box 5 (budget tiers, top to bottom)
-          if (c > a.s_easy && p < a.p_easy) bud = a.b_easy;
-          else if (c < a.s_hard || p >= a.p_hard) bud = a.b_hard;
-          else bud = a.b_mid;
-          a.sv[sg] = c;
-          a.budget[sg] = bud;
-        } else {
-          bud = a.budget[sg];
+      }
+      int why = 0;
+      bool exit = false;
+      if (a.fixed_k > 0) {
+        const float ce = c == c ? c : -INFINITY;
+        bool sel = false;
+        for (int it = 0; it < a.fixed_k; ++it) {
+          int e = masked && !sel ? 1 : 0, bp = e ? p : 64;
+          float bc = e ? ce : -INFINITY;
+#pragma unroll
+          for (int off = 32; off > 0; off >>= 1) {
+            const int oe = __shfl_xor(e, off, 64), op = __shfl_xor(bp, off, 64);
+            const float oc = __shfl_xor(bc, off, 64);
+            if (oe > e || (oe == e && (oc > bc || (oc == bc && op < bp)))) {
+              e = oe;
+              bc = oc;
+              bp = op;
+            }
+          }
+          if (e == 0) break;  // nothing eligible is left (the same on every lane)
+          if (p == bp) sel = true;
         }
+        const bool remaining = masked && !sel;
+        exit = __ballot(remaining) == 0ull;
+        const bool flush = (exit || a.t == a.T - 1) && remaining;
+        if (a.t == a.T - 1) exit = true;
+        why = sel ? 5 : flush ? 4 : 0;
+        ell = 0;
+      } else {
+        if (lane_on) {
+          if (a.t == 0) {  // Box 2 (s_i = c_i^(0)) and Box 5 (budget tiers, top to bottom)
+            if (c > a.s_easy && p < a.p_easy) bud = a.b_easy;
+            else if (c < a.s_hard || p >= a.p_hard) bud = a.b_hard;
+            else bud = a.b_mid;
+            a.sv[sg] = c;
+            a.budget[sg] = bud;
+          } else {
+            bud = a.budget[sg];
+          }
+        }
+        const int band = (p >= a.edge[0]) + (p >= a.edge[1]) + (p >= a.edge[2]);
+        const bool by_thr = masked && (c >= a.thr[band]);                         // Box 6 rule
+        const bool by_bud = masked && !by_thr && a.budget_on && (a.t >= bud);   // Box 5 force
+        const bool newly = by_thr || by_bud;
+        const int eta = __popcll(__ballot(newly));
+        ell = ((double)eta < a.eta_bar) ? ell + 1 : 0;                          // Box 7 counter
+        bool forced = false;
+        if (a.grind_on && ell >= a.patience) {                                  // grinding fallback
+          forced = masked && !newly && (c > a.theta_fb);
+          exit = true;
+        }
+        const bool remaining = masked && !newly && !forced;
+        if (__ballot(remaining) == 0ull) exit = true;
+        bool flush = false;
+        if (exit || a.t == a.T - 1) {
+          flush = remaining;
+          exit = true;
+        }
+        why = by_thr ? 1 : by_bud ? 2 : forced ? 3 : flush ? 4 : 0;
       }
-      const int band = (p >= a.edge[0]) + (p >= a.edge[1]) + (p >= a.edge[2]);
-      const bool by_thr = masked && (c >= a.thr[band]);                         // Box 6 rule
-      const bool by_bud = masked && !by_thr && a.budget_on && (a.t >= bud);   // Box 5 force
-      const bool newly = by_thr || by_bud;
-      const int eta = __popcll(__ballot(newly));
-      ell = ((double)eta < a.eta_bar) ? ell + 1 : 0;                          // Box 7 counter
-      bool exit = false, forced = false;
-      if (a.grind_on && ell >= a.patience) {                                  // grinding fallback
-        forced = masked && !newly && (c > a.theta_fb);
-        exit = true;
-      }
-      const bool remaining = masked && !newly && !forced;
-      if (__ballot(remaining) == 0ull) exit = true;
-      bool flush = false;
-      if (exit || a.t == a.T - 1) {
-        flush = remaining;
-        exit = true;
-      }
-      const int why = by_thr ? 1 : by_bud ? 2 : forced ? 3 : flush ? 4 : 0;
       if (why) {
         a.x[(size_t)b * a.L + a.P + g] = tok;
         a.commit_step[sg] = a.t;

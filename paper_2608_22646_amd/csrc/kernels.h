@@ -89,6 +89,7 @@ struct CommitArgs {
   int budget_on, grind_on;
   float s_easy, s_hard; int p_easy, p_hard, b_easy, b_mid, b_hard;
   double eta_bar; int patience; float theta_fb;
+  int fixed_k;         // > 0: fixed-schedule baseline, commit this many tokens this step
 };
 void launch_commit(const CommitArgs& a, hipStream_t s);
 

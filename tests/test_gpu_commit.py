@@ -80,7 +80,16 @@ CASES = [
     ("low", 2, 32, 3, True, dict(grinding=False)),
     ("uniform", 1, 32, 2, True, dict(theta_s=0.9, theta_e=0.9, block_sched=False, pos_aware=False,
                                       budgets=False, grinding=False)),  # fixed-threshold 0.9
+    # fixed-schedule baseline: one token per step, or several (T < block_len)
+    ("uniform", 2, 32, 3, True, dict(fixed=True)),
+    ("grid", 3, 32, 2, True, dict(fixed=True)),            # equal confidences: lower position first
+    ("nan", 2, 32, 2, True, dict(fixed=True)),             # NaN ranks lowest
+    ("uniform", 2, 32, 2, True, dict(fixed=True, steps_per_block=12)),
+    ("grid", 2, 64, 2, True, dict(fixed=True, steps_per_block=64)),
+    ("uniform", 2, 4, 3, True, dict(fixed=True, steps_per_block=3)),
 ]
+PRESETS = ["cai", "cai_gate_off", "apd", "apd_block", "apd_block_budget", "fixed_threshold_0.9",
+           "fixed_threshold_0.7", "apd_0.9_to_0.5", "fixed_schedule"]
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
@@ -96,6 +105,32 @@ def test_commit_matches_oracle(case):
     st, fwd = run_gpu_controller(ctl, conf, arg, prompts, G)
     ref = replay(conf.numpy(), arg.numpy(), prompts.numpy(), G, MASK, ctl)
     assert_state_equal(st, fwd, ref)
+
+
+@pytest.mark.parametrize("name", PRESETS)
+def test_commit_presets_match_oracle(name):
+    ctl = B.Controller.preset(name)
+    Bn, nb, P = 2, 3, 5
+    G = nb * ctl.block_len
+    say(f"commit preset {name}")
+    conf, arg = make_trace("uniform", nb, ctl.T, Bn, ctl.block_len, seed=300 + PRESETS.index(name))
+    prompts = synth.make_ints((Bn, P), 31, 0, MASK)
+    st, fwd = run_gpu_controller(ctl, conf, arg, prompts, G)
+    ref = replay(conf.numpy(), arg.numpy(), prompts.numpy(), G, MASK, ctl)
+    assert_state_equal(st, fwd, ref)
+
+
+def test_commit_fixed_schedule_hand_trace():
+    # S9 (the oracle's hand trace) through the kernel: block of 4, one token per
+    # step, chosen positions 1, 0, 3, 2; each takes the argmax of its step
+    ctl = B.Controller(block_len=4, fixed=True)
+    confs = torch.tensor([[[.1, .5, .3, .5]], [[.9, .9, .2, .1]], [[.3, .2, .1, .4]], [[0., 0., 0., 0.]]])[None]
+    args = torch.tensor([[[10 + t, 20 + t, 30 + t, 40 + t]] for t in range(4)], dtype=torch.int32)[None]
+    st, fwd = run_gpu_controller(ctl, confs.float(), args, torch.zeros((1, 2), dtype=torch.int32), 4)
+    assert fwd == [4]
+    assert st.commit_step.cpu().tolist() == [[1, 0, 3, 2]]
+    assert st.reason.cpu().tolist() == [[B.R_FIXED] * 4]
+    assert st.x.cpu().tolist() == [[0, 0, 11, 20, 33, 42]]
 
 
 # hand-derived traces (the same ones that pin the oracle) run through the kernel

@@ -60,7 +60,7 @@ def check_invariants(st, forwards, P, G, bl, T, mask_id, ctl):
     assert (cs >= 0).all() and (cs <= T - 1).all(), "a token was left masked or committed past T"
     assert (rs >= 1).all()
     assert (st.x[:, P:] != mask_id).all().item(), "mask id left in the output"
-    if ctl.budgets:
+    if ctl.budgets and not ctl.fixed:
         assert (cs <= st.budget.cpu().numpy()).all(), "a token exceeded its step budget"
     for b in range(cs.shape[0]):
         for blk in range(G // bl):
@@ -96,15 +96,16 @@ def test_full_size_stages_and_head(models, name):
     say(f"  head {hs}")
 
 
-@pytest.mark.parametrize("name,gating", [(n, None) for n in WORKLOADS] + [("dream_b1", True)])
-def test_full_size_decode_replay(models, name, gating):
+@pytest.mark.parametrize("name,preset", [(n, None) for n in WORKLOADS] + [("dream_b1", "cai"),
+                                                                          ("llada_b1", "fixed_schedule")])
+def test_full_size_decode_replay(models, name, preset):
     wl = synth.WORKLOADS[name]
     cfg = wl.model
     _, model = models(cfg)
-    gating = wl.gating if gating is None else gating
-    ctl = B.Controller.gating(gating, block_len=wl.block_len)
+    preset = preset or ("cai" if wl.gating else "cai_gate_off")
+    ctl = B.Controller.preset(preset, block_len=wl.block_len)
     prompts = synth.make_prompts(wl)
-    say(f"{name}: decode, gating {'on' if gating else 'off'}")
+    say(f"{name}: decode, controller {preset}")
     res = model.generate(ctl, prompts.cuda(), wl.gen_len, trace=True)
     torch.cuda.synchronize()
     ref = replay(res.conf_trace.cpu().numpy(), res.argmax_trace.cpu().numpy(), prompts.numpy(), wl.gen_len,
@@ -112,3 +113,5 @@ def test_full_size_decode_replay(models, name, gating):
     assert_state_equal(res.state, res.forwards, ref)
     check_invariants(res.state, res.forwards, wl.prompt_len, wl.gen_len, wl.block_len, ctl.T, cfg.mask_id, ctl)
     say(f"  forwards per block {res.forwards} (total {res.total_forwards})")
+    if ctl.fixed:
+        assert res.forwards == [ctl.T] * (wl.gen_len // wl.block_len)

@@ -1,7 +1,8 @@
 """Tiny fp32 LLaDA-style model end to end (dllm_generate) against the float64 oracle.
 
 Workload: 2 layers, d 256, 4 heads x 64, FFN 704, vocab 2048 (mask 2047),
-prompt 32, 64 generated tokens in 2 blocks of 32, batch 1, gating on.
+prompt 32, 64 generated tokens in 2 blocks of 32, batch 1, under the method
+with gating on and off, the fixed-schedule baseline and three ablation presets.
   * every step's logits and confidences, teacher-forced on the token array the
     GPU saw, agree with the oracle within 1e-5; argmax agrees except at a
     logit near-tie (reported);
@@ -41,13 +42,16 @@ def _run(model, ctl, prompts, G):
     return res
 
 
-@pytest.mark.parametrize("gating", [True, False])
-def test_tiny_generate_matches_oracle(tiny, gating):
+CONTROLLERS = ["cai", "cai_gate_off", "fixed_schedule", "apd", "apd_block", "fixed_threshold_0.9"]
+
+
+@pytest.mark.parametrize("name", CONTROLLERS)
+def test_tiny_generate_matches_oracle(tiny, name):
     cfg, model, wnp = tiny
-    ctl = B.Controller.gating(gating)
+    ctl = B.Controller.preset(name)
     prompts = synth.make_prompts(WL)
     P, G, bl = WL.prompt_len, WL.gen_len, ctl.block_len
-    say(f"tiny generate gating={gating}")
+    say(f"tiny generate {name}")
     res = _run(model, ctl, prompts, G)
     st = res.state
     ct, at = res.conf_trace.cpu().numpy(), res.argmax_trace.cpu().numpy()
@@ -84,7 +88,9 @@ def test_tiny_generate_matches_oracle(tiny, gating):
     free = oc.generate(pred, prompts.numpy(), G, cfg.mask_id, oracle_params(ctl))
     if near == 0:
         assert_state_equal(st, res.forwards, free, s_tol=TOL)
-    say(f"tiny gating={gating}: forwards {res.forwards}, argmax near-ties {near}")
+    say(f"tiny {name}: forwards {res.forwards}, argmax near-ties {near}")
+    if ctl.fixed:
+        assert res.forwards == [ctl.T] * (G // bl)
 
 
 def test_tiny_step_resume_equals_generate(tiny):

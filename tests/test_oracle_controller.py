@@ -295,3 +295,66 @@ def test_batch_lockstep_equals_per_sequence_runs():
     # the lockstep block runs as many forwards as its slowest sequence
     per = [oc.generate(pred_for([s]), prompts[s:s + 1], G, 99, p).forwards for s in range(B)]
     assert batch.forwards == [max(f[b] for f in per) for b in range(nb)]
+
+
+# ------------------------------------------------ fixed-schedule baseline (R19)
+FIXED = oc.FIXED
+
+
+def test_fixed_schedule_hand_trace():
+    # S9, block of 4, one token per step.  t0: c = (.1 .5 .3 .5): the tie at .5
+    # goes to position 1.  t1: masked 0, 2, 3 with (.9 .2 .1): position 0 (the .9
+    # at the already committed position 1 is not eligible).  t2: masked 2, 3 with
+    # (.1 .4): position 3.  t3: position 2.  Four forwards, all reason FIXED.
+    p = CaiParams(block_len=4, fixed=True)
+    confs = [[.1, .5, .3, .5], [.9, .9, .2, .1], [.3, .2, .1, .4], [0., 0., 0., 0.]]
+    stt = oc.generate(lambda x, blk, t: (np.array([confs[t]], np.float32), np.array([[10 + t, 20 + t, 30 + t, 40 + t]])),
+                      np.zeros((1, 2), np.int64), 4, 99, p)
+    assert stt.forwards == [4]
+    assert stt.commit_step[0].tolist() == [1, 0, 3, 2]
+    assert stt.reason[0].tolist() == [FIXED] * 4
+    assert stt.x[0, 2:].tolist() == [11, 20, 33, 42]      # each token takes the argmax of its commit step
+
+
+@pytest.mark.parametrize("bl,T,expect", [(32, 32, [1] * 32), (32, 16, [2] * 16), (4, 3, [2, 1, 1]),
+                                         (32, 12, [3] * 8 + [2] * 4), (8, 8, [1] * 8)])
+def test_fixed_schedule_commit_counts(bl, T, expect):
+    p = CaiParams(block_len=bl, steps_per_block=T, fixed=True)
+    got = [oc.fixed_commits(t, p) for t in range(T)]
+    assert got == expect and sum(got) == bl
+
+
+@settings(max_examples=60, deadline=None)
+@given(seed=st.integers(0, 2**31 - 1), bl=st.sampled_from([4, 8, 32]), div=st.sampled_from([1, 2, 3]),
+       B=st.integers(1, 3), nb=st.integers(1, 2), grid=st.booleans())
+def test_fixed_schedule_commits_dominate_the_rest(seed, bl, div, B, nb, grid):
+    # Brute-force restatement: after every step, each token committed in that
+    # step beats every token still masked (higher confidence, or equal and a
+    # lower position); the step commits k_t tokens; every block takes T forwards.
+    rng = np.random.default_rng(seed)
+    T = max(1, bl // div)
+    p = CaiParams(block_len=bl, steps_per_block=T, fixed=True)
+    G, P = bl * nb, 2
+    trace = []
+
+    def predict(x, blk, t):
+        if grid:
+            c = rng.choice(np.float32([0.1, 0.5, 0.9]), (B, bl))
+        else:
+            c = rng.random((B, bl)).astype(np.float32)
+        return c, rng.integers(0, 99, (B, bl))
+
+    stt = oc.generate(predict, rng.integers(0, 99, (B, P)), G, 99, p,
+                      on_step=lambda *a: trace.append((a[0], a[1], a[3])))
+    assert stt.forwards == [T] * nb
+    assert np.all(stt.reason == FIXED)
+    for blk, t, conf in trace:
+        sl = slice(blk * bl, (blk + 1) * bl)
+        for seq in range(B):
+            cs = stt.commit_step[seq, sl]
+            now = [i for i in range(bl) if cs[i] == t]
+            later = [i for i in range(bl) if cs[i] > t]
+            assert len(now) == oc.fixed_commits(t, p)
+            for i in now:
+                for j in later:
+                    assert conf[seq, i] > conf[seq, j] or (conf[seq, i] == conf[seq, j] and i < j)
