@@ -169,23 +169,44 @@ void run_embed(const dllm_model* m, const int32_t* x, int B, int L, void* ws, co
   launch_rope_table(at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), L, c.head_dim, c.rope_base, s);
 }
 
-void gemm_bf16(const dllm_model* m, GemmArgs g, void* ws, const Layout& lay, hipStream_t s, int kind) {
+void gemm_bf16(const dllm_model* m, GemmArgs g, void* ws, const Layout& lay, hipStream_t s, int kind,
+               PendingResid* defer = nullptr) {
   g.splitk_buf = at<float>(ws, lay.splitk);
   ProfScope p(m, kind, s);
-  launch_gemm_bf16(g, s);
+  launch_gemm_bf16(g, s, defer);
 }
 
-void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay,
+// RMSNorm of every row of h into out; split-K partials still pending from the
+// previous residual GEMM (pend non-null with split > 0) are added to h first,
+// in the same pass, and then cleared.
+void norm_rows_bf16(const dllm_model* m, float* h, PendingResid* pend, const void* gain, void* out, int B, int L,
                     hipStream_t s) {
+  const auto& c = m->cfg;
+  ProfScope p(m, PK_NORM, s);
+  if (pend && pend->split > 0) {
+    launch_resid_rmsnorm(h, *pend, static_cast<const bf16_t*>(gain), static_cast<bf16_t*>(out), B * L, c.d_model,
+                         c.rms_eps, s);
+    *pend = PendingResid{};
+  } else {
+    launch_rmsnorm(h, gain, out, 1, B, L, L, 0, c.d_model, c.rms_eps, s);
+  }
+}
+
+// One layer (part 0: attention half, 1: MLP half, 2: both).  carry_in holds
+// split-K partials the previous layer's down projection left pending (added by
+// this layer's first norm); with carry_out non-null the down projection leaves
+// its own partials there for the next layer instead of reducing them.  The
+// output projection's partials are folded into the MLP norm when both halves
+// run here.  Without carries h is complete when the call returns.
+void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay,
+                    hipStream_t s, PendingResid* carry_in = nullptr, PendingResid* carry_out = nullptr) {
   const auto& c = m->cfg;
   const int base = 1 + 9 * layer;
   const int M = B * L, d = c.d_model, hd = c.head_dim;
   float* h = at<float>(ws, lay.h);
+  PendingResid mid;  // output-projection partials, consumed by the MLP norm
   if (part == 0 || part == 2) {
-    {
-      ProfScope p(m, PK_NORM, s);
-      launch_rmsnorm(h, W(m, base + 0), at<void>(ws, lay.a_attn), 1, B, L, L, 0, d, c.rms_eps, s);
-    }
+    norm_rows_bf16(m, h, carry_in, W(m, base + 0), at<void>(ws, lay.a_attn), B, L, s);
     GemmArgs g{};
     g.epi = EPI_QKV_ROPE;
     g.M = M;
@@ -220,13 +241,10 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     o.W0 = Wb(m, base + 4);
     o.n0 = d;
     o.resid = h;
-    gemm_bf16(m, o, ws, lay, s, PK_GEMM);
+    gemm_bf16(m, o, ws, lay, s, PK_GEMM, part == 2 ? &mid : nullptr);
   }
   if (part == 1 || part == 2) {
-    {
-      ProfScope p(m, PK_NORM, s);
-      launch_rmsnorm(h, W(m, base + 5), at<void>(ws, lay.a_mlp), 1, B, L, L, 0, d, c.rms_eps, s);
-    }
+    norm_rows_bf16(m, h, part == 1 ? carry_in : &mid, W(m, base + 5), at<void>(ws, lay.a_mlp), B, L, s);
     GemmArgs g{};
     g.epi = EPI_SWIGLU;
     g.M = M;
@@ -248,7 +266,7 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     dn.W0 = Wb(m, base + 8);
     dn.n0 = d;
     dn.resid = h;
-    gemm_bf16(m, dn, ws, lay, s, PK_GEMM);
+    gemm_bf16(m, dn, ws, lay, s, PK_GEMM, carry_out);
   }
 }
 
@@ -431,7 +449,15 @@ void forward_all(const dllm_model* m, const int32_t* x, int B, int L, int row0, 
     ProfScope p(m, PK_NORM, s);
     run_embed(m, x, B, L, ws, lay, s);
   }
-  for (int l = 0; l < m->cfg.n_layers; ++l) run_layer(m, l, 2, B, L, ws, lay, s);
+  if (m->cfg.dtype == DLLM_BF16) {
+    // each layer's down-projection partials are added by the next layer's first
+    // norm; the last layer reduces its own, so h is complete for the head
+    PendingResid carry;
+    const int nl = m->cfg.n_layers;
+    for (int l = 0; l < nl; ++l) run_layer_bf16(m, l, 2, B, L, ws, lay, s, &carry, l + 1 < nl ? &carry : nullptr);
+  } else {
+    for (int l = 0; l < m->cfg.n_layers; ++l) run_layer(m, l, 2, B, L, ws, lay, s);
+  }
   run_head(m, B, L, row0, rows, conf, argmax, logits, ws, lay, s);
 }
 

@@ -464,7 +464,8 @@ size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi) {
   return p.split > 1 ? (size_t)p.split * M * N * sizeof(float) : 0;
 }
 
-void launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
+void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
+  if (defer) *defer = PendingResid{};
   if (a.M == 0) return;
   if (a.N % 256 != 0 || a.K % BK != 0) throw HipError("gemm_bf16: N % 256 and K % 64 must be 0");
   if (a.epi == EPI_QKV_ROPE && (a.n0 % 256 != 0 || a.n1 % 256 != 0))
@@ -477,7 +478,9 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
     default: throw HipError("gemm_bf16: unknown epilogue");
   }
   DLLM_LAUNCH_CHECK("gemm_bf16");
-  if (p.split > 1) {
+  if (p.split > 1 && defer) {
+    *defer = PendingResid{a.splitk_buf, p.split};
+  } else if (p.split > 1) {
     const long MN = (long)a.M * a.N;
     hipLaunchKernelGGL(splitk_resid_kernel, dim3(ceil_div(MN / 4, 256)), dim3(256), 0, s, a.splitk_buf, a.resid, MN,
                        p.split);

@@ -157,6 +157,76 @@ void launch_rmsnorm_t(const float* h, const TG* g, TO* out, int B, int rows, int
   }
 }
 
+// rmsnorm_vec_kernel preceded by the split-K residual update of its row: each
+// float4 of the row is h + ((p_0 + p_1) + ... + p_{S-1}), the same operations in
+// the same order as splitk_resid_kernel, written back to h and kept for the norm.
+template <int NV>
+__global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ part,
+                                                            int S, long MN, const bf16_t* __restrict__ g,
+                                                            bf16_t* __restrict__ out, int d, float eps) {
+  const int r = blockIdx.x;
+  float* row = h + (size_t)r * d;
+  const int d4 = d / 4;
+  float4 v[NV];
+  double ss = 0.0;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int c = threadIdx.x + 256 * j;
+    if (c < d4) {
+      const size_t i = (size_t)r * d4 + c;
+      float4 acc = reinterpret_cast<const float4*>(part)[i];
+      for (int z = 1; z < S; ++z) {
+        const float4 p = reinterpret_cast<const float4*>(part + (size_t)z * MN)[i];
+        acc.x += p.x;
+        acc.y += p.y;
+        acc.z += p.z;
+        acc.w += p.w;
+      }
+      float4 x = Vec4<float>::load(row, c);
+      x.x += acc.x;
+      x.y += acc.y;
+      x.z += acc.z;
+      x.w += acc.w;
+      Vec4<float>::store(row, c, x);
+      v[j] = x;
+      ss += (double)x.x * x.x + (double)x.y * x.y + (double)x.z * x.z + (double)x.w * x.w;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  __shared__ double prt[4];
+  if ((threadIdx.x & 63) == 0) prt[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const double tot = (prt[0] + prt[1]) + (prt[2] + prt[3]);
+  const float rstd = (float)(1.0 / sqrt(tot / (double)d + (double)eps));
+  bf16_t* dst = out + (size_t)r * d;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int c = threadIdx.x + 256 * j;
+    if (c < d4) {
+      const float4 gg = Vec4<bf16_t>::load(g, c);
+      Vec4<bf16_t>::store(dst, c, make_float4(v[j].x * rstd * gg.x, v[j].y * rstd * gg.y, v[j].z * rstd * gg.z,
+                                              v[j].w * rstd * gg.w));
+    }
+  }
+}
+
+void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, bf16_t* out, int M, int d, float eps,
+                          hipStream_t s) {
+  if (M == 0) return;
+  if (d % 4 != 0 || d > 8192 || ((uintptr_t)h | (uintptr_t)pend.part | (uintptr_t)g | (uintptr_t)out) % 16 != 0)
+    throw HipError("resid_rmsnorm: needs d % 4 == 0, d <= 8192 and 16-byte aligned rows");
+  const long MN = (long)M * d;
+  const int nv = ceil_div(d, 1024);
+  if (nv <= 2)
+    hipLaunchKernelGGL(resid_rmsnorm_kernel<2>, dim3(M), dim3(256), 0, s, h, pend.part, pend.split, MN, g, out, d, eps);
+  else if (nv <= 4)
+    hipLaunchKernelGGL(resid_rmsnorm_kernel<4>, dim3(M), dim3(256), 0, s, h, pend.part, pend.split, MN, g, out, d, eps);
+  else
+    hipLaunchKernelGGL(resid_rmsnorm_kernel<8>, dim3(M), dim3(256), 0, s, h, pend.part, pend.split, MN, g, out, d, eps);
+  DLLM_LAUNCH_CHECK("resid_rmsnorm");
+}
+
 void launch_rmsnorm(const float* h, const void* g, void* out, int dtype, int B, int rows, int L, int row0, int d,
                     float eps, hipStream_t s) {
   if (B * rows == 0) return;

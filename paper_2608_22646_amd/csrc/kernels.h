@@ -54,7 +54,21 @@ struct GemmArgs {
   float* splitk_buf;
 };
 int device_cu_count();  // compute units of the current device (256 if it cannot be queried)
-void launch_gemm_bf16(const GemmArgs& a, hipStream_t s);
+// Split-K partial tiles of a residual GEMM whose reduction into the residual
+// has been left to the next RMSNorm (split 0: nothing pending).
+struct PendingResid {
+  const float* part = nullptr;  // [split, M, N] float32
+  int split = 0;
+};
+// With defer non-null, a split-K residual GEMM leaves its partials pending
+// there instead of launching the reduction (defer->split = 0 otherwise).
+void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer = nullptr);
+// Completes a deferred residual update and normalises in one pass, for every
+// row m < M (bf16 model, d % 4 == 0, d <= 8192):
+//   h[m, :] += sum_z part[z, m, :]   (z in order, as the split-K reduction does)
+//   out[m, :] = bf16(RMSNorm(h[m, :]) * g)
+void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, bf16_t* out, int M, int d, float eps,
+                          hipStream_t s);
 // Bytes of split-K scratch a launch of this shape needs (0 if it does not split).
 size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi);
 

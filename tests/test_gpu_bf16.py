@@ -46,6 +46,32 @@ def test_forward_stages(small, Bn, P, G):
     say(f"  head: {hs}")
 
 
+def forward_equals_layer_calls(model, cfg, Bn, P, G, seed):
+    """dllm_forward (which folds each residual GEMM's split-K partials into the
+    next RMSNorm) against embed + one dllm_layer call per layer + dllm_head
+    (every split-K reduction by its own kernel): the same float operations in
+    the same order, so conf, argmax and logits must be bitwise identical."""
+    L, rows = P + G, min(32, G)
+    x = synth.make_ints((Bn, L), seed, 0, cfg.vocab - 1).cuda()
+    conf_f, arg_f, lg_f = model.forward(x, P, rows, logits=True)
+    ws = model.workspace(Bn, L, rows)
+    model.embed(x, ws)
+    for l in range(cfg.n_layers):
+        model.layer(l, 2, Bn, L, ws)
+    conf_l, arg_l, lg_l = model.head(Bn, L, P, rows, ws, logits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(arg_f, arg_l)
+    assert torch.equal(conf_f.view(torch.int32), conf_l.view(torch.int32))
+    assert torch.equal(lg_f.view(torch.int32), lg_l.view(torch.int32))
+
+
+@pytest.mark.parametrize("Bn,P,G", [(2, 40, 64), (1, 9, 32), (2, 1036, 64)])
+def test_forward_matches_layer_by_layer(small, Bn, P, G):
+    model, _ = small
+    say(f"bf16 fused forward vs layer calls B={Bn} L={P + G}")
+    forward_equals_layer_calls(model, SMALL, Bn, P, G, seed=9)
+
+
 def _head_model(V, d, mask_id_at_top=True):
     cfg = synth.ModelConfig("head-fixture", n_layers=0, d_model=d, n_heads=2, n_kv_heads=2, head_dim=128, d_ff=128,
                             vocab=V, rope_base=1e4, dtype="bf16", rms_eps=1e-30)

@@ -96,6 +96,15 @@ def test_full_size_stages_and_head(models, name):
     say(f"  head {hs}")
 
 
+@pytest.mark.parametrize("name", ["llada_b1", "dream_b1"])
+def test_full_size_forward_matches_layer_by_layer(models, name):
+    from test_gpu_bf16 import forward_equals_layer_calls
+    wl = synth.WORKLOADS[name]
+    _, model = models(wl.model)
+    say(f"{name}: fused forward vs layer calls")
+    forward_equals_layer_calls(model, wl.model, wl.batch, wl.prompt_len, wl.gen_len, seed=23)
+
+
 @pytest.mark.parametrize("name,preset", [(n, None) for n in WORKLOADS] + [("dream_b1", "cai"),
                                                                           ("llada_b1", "fixed_schedule")])
 def test_full_size_decode_replay(models, name, preset):
