@@ -378,6 +378,202 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
 #endif
 }
 
+
+// Key-split variant for launches too small to give every SIMD a wave: eight
+// waves share 128 queries -- wave w owns queries 32 (w % 4) .. +31 and the key
+// tiles 2u + w / 4 -- so each query is processed by two waves over alternate
+// 64-key tiles.  The ring holds pairs of tiles (two stages of 64 KiB); at the
+// end the second wave of each pair hands its running (max, sum, output) to
+// the first through LDS, which merges them (rescaling both to the larger
+// maximum) and writes the result.
+__global__ void __launch_bounds__(512, 1) attn_split_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
+                                                          const f16_t* __restrict__ vt, bf16_t* __restrict__ out,
+                                                          int L, int Hq, int Hkv) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int NW = 8, QG = 4, S = 2, PAIR = 2 * STAGE;
+  constexpr int PER_PAIR = 64 / NW;  // 2 x (16 K + 16 V^T) DMA instructions per pair
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qw = wave % QG, kg = wave / QG;
+  const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
+  const int q0 = blockIdx.x * (QW * QG) + qw * QW;
+  const int lq = lane & 31, half = lane >> 5;
+  const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
+  const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
+
+  bf16x8_t qf[8];
+  {
+    const int qi = q0 + lq;
+    const bf16_t* qrow = q + (((size_t)b * Hq + h) * L + (qi < L ? qi : 0)) * HD;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16 + half * 8);
+      if (qi >= L) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+  }
+
+  // DMA as in attn_stream_kernel, for both tiles of a pair: instruction i of a
+  // tile is issued by wave i % NW (two K and two V^T instructions per wave)
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, 0, L * HD * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, 0, HD * L * 2, 0x00020000);
+  constexpr int PK = 16 / NW;
+  uint32_t vok[PK], vov[PK];
+#pragma unroll
+  for (int j = 0; j < PK; ++j) {
+    const int i = wave + NW * j;
+    const int key = 4 * i + (lane >> 4), kc = (lane & 15) ^ (key & 15);
+    vok[j] = (uint32_t)((key * HD + kc * 8) * 2);
+    const int d = 8 * i + (lane >> 3), vc = (lane & 7) ^ ((d >> 1) & 7);
+    vov[j] = (uint32_t)(((size_t)d * L + vc * 8) * 2);
+  }
+  auto issue = [&](int u) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      char* base = lds + (u % S) * PAIR + sub * STAGE;
+      const int t0 = (2 * u + sub) * KT;
+#pragma unroll
+      for (int j = 0; j < PK; ++j) {
+        const int i = wave + NW * j;
+        // out-of-range tiles (past this head's K / V^T) read zeros
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(base + i * 1024), 16, vok[j] + t0 * HD * 2, 0, 0,
+                                                 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(base + K_BYTES + i * 1024), 16, vov[j] + t0 * 2, 0,
+                                                 0, 0);
+      }
+    }
+  };
+
+  f32x16_t o[4];
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ds][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float sc = 1.4426950408889634f / sqrtf((float)HD);
+
+  const int ntiles = (L + KT - 1) / KT, npairs = (ntiles + 1) / 2;
+  issue(0);
+  for (int u = 0; u < npairs; ++u) {
+    wait_vmcnt_a<0>();
+    barrier_nofence_a();  // pair u visible; slot (u + 1) % 2 free
+    if (u + 1 < npairs) issue(u + 1);
+    const int t = 2 * u + kg;
+    if (t >= ntiles) continue;  // odd tile count: the second group has nothing in the last pair
+    const char* base = lds + (u % S) * PAIR + kg * STAGE;
+
+    f32x16_t s2[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s2[st][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + lq, ks * 2 + half));
+        s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s2[st], 0, 0, 0);
+      }
+    }
+    const int t0 = t * KT;
+    float mt = -INFINITY;
+    if (t0 + KT <= L) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s2[st][r]);
+    } else {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = t0 + st * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (key >= L) s2[st][r] = -INFINITY;
+          mt = fmaxf(mt, s2[st][r]);
+        }
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sc;
+    if (__ballot(mt > m_run + 8.0f) != 0ull) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[ds][r] *= alpha;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(fmaf(s2[st][r], sc, -m_run));
+        s2[st][r] = p;
+        psum += p;
+      }
+    l_run += psum;
+
+#pragma unroll
+    for (int jk = 0; jk < 4; ++jk) {
+      f16x8_t pf;
+      const int st = jk >> 1, r0 = (jk & 1) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[st][r0 + e];
+      const int kA = jk * 16 + 4 * half, kB = kA + 8;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) {
+        const int d = ds * 32 + lq;
+        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kA >> 3) + (kA & 7) * 2);
+        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kB >> 3) + (kB & 7) * 2);
+        const f16x8_t vf = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
+        o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
+      }
+    }
+  }
+
+  // hand-over through LDS (the ring is idle once every wave has passed here):
+  // per query wave, 64 floats of o and (m, l) per lane
+  __syncthreads();
+  float* xo = reinterpret_cast<float*>(lds) + (size_t)qw * (66 * 64);
+  if (kg == 1) {
+#pragma unroll
+    for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xo[(ds * 16 + r) * 64 + lane] = o[ds][r];
+    xo[64 * 64 + lane] = m_run;
+    xo[65 * 64 + lane] = l_run;
+  }
+  __syncthreads();
+  if (kg == 1) return;
+  {
+    const float m1 = xo[64 * 64 + lane], l1 = xo[65 * 64 + lane];
+    const float m = fmaxf(m_run, m1);
+    // a group that saw no key (m = -inf) contributes nothing
+    const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - m);
+    const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - m);
+    l_run = l_run * a0 + l1 * a1;
+#pragma unroll
+    for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[ds][r] = o[ds][r] * a0 + xo[(ds * 16 + r) * 64 + lane] * a1;
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  const int qi = q0 + lq;
+  if (qi >= L) return;
+  bf16_t* orow = out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      const int d = ds * 32 + 8 * rg + 4 * half;
+      uint2 w;
+      w.x = pack_bf16x2(o[ds][rg * 4 + 0] * inv, o[ds][rg * 4 + 1] * inv);
+      w.y = pack_bf16x2(o[ds][rg * 4 + 2] * inv, o[ds][rg * 4 + 3] * inv);
+      *reinterpret_cast<uint2*>(orow + d) = w;
+    }
+#endif
+}
+
 }  // namespace
 
 void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int L, int Hq, int Hkv,
@@ -385,9 +581,21 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
   if (B * L == 0) return;
   if (L % 8 == 0) {
     // streaming kernel: 8 waves (256 queries) per workgroup when that still gives
-    // two or more workgroups per CU over the launch, else 4 waves
+    // two or more workgroups per CU over the launch, else 4 waves; when even the
+    // 4-wave grid leaves SIMDs without a wave, the key-split kernel (two waves
+    // per query over alternate key tiles)
     const bool wide = (long)((L + 255) / 256) * Hq * B >= 512;
     const size_t lds = 3 * (size_t)STAGE;
+    if ((long)((L + 127) / 128) * Hq * B * 4 < 4L * device_cu_count() && L > KT) {
+      constexpr size_t lds_split = 2 * 2 * (size_t)STAGE;
+      static const hipError_t as = hipFuncSetAttribute((const void*)attn_split_kernel,
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_split);
+      hip_check(as, "hipFuncSetAttribute(attn_split)");
+      hipLaunchKernelGGL(attn_split_kernel, dim3(ceil_div(L, QW * 4), Hq, B), dim3(512), lds_split, s, q, k, vt, out,
+                         L, Hq, Hkv);
+      DLLM_LAUNCH_CHECK("attn_split");
+      return;
+    }
     if (wide) {
       static const hipError_t a8 =
           hipFuncSetAttribute((const void*)attn_stream_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
