@@ -180,6 +180,44 @@ def ablation(args):
                       "variants": rows}), flush=True)
 
 
+def sweep_gen(args):
+    """tokens/s of the workload's model, batch and prompt at generation lengths
+    64-512 (the paper's throughput-vs-length table), one warm-up decode each."""
+    import dataclasses
+    import torch
+    from paper_2608_22646_amd import binding as Bd
+    from paper_2608_22646_amd import synth
+
+    base = synth.WORKLOADS[args.workload]
+    cfg = base.model
+    model = Bd.Model(cfg, synth.make_weights(cfg, "cuda"))
+    rows = []
+    for G in (64, 128, 256, 512):
+        wl = dataclasses.replace(base, name=f"{base.name}_g{G}", gen_len=G)
+        B, P, bl = wl.batch, wl.prompt_len, wl.block_len
+        prompts = synth.make_prompts(wl, "cuda")
+        ctl = Bd.Controller.gating(wl.gating, block_len=bl)
+        ws = model.workspace(B, P + G, bl)
+        st = Bd.DecodeState(B, P, G, "cuda")
+        model.generate(ctl, prompts, G, ws=ws, st=st)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        res = model.generate(ctl, prompts, G, ws=ws, st=st)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        rows.append({"gen_len": G, "forwards_per_decode": res.total_forwards, "tokens_per_s": B * G / dt,
+                     "ms_per_decode": dt * 1e3, "ms_per_forward": dt * 1e3 / res.total_forwards})
+        log(f"G={G}: {res.total_forwards} forwards, {B * G / dt:.1f} tokens/s")
+        del ws, st
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "generated tokens/s vs generation length", "n_gpus": 1,
+                      "data": "synthetic (seeded random-init weights of the model shape, uniform random prompts)",
+                      "config": {"workload": f"{base.name}: {cfg.name} random-init, batch {base.batch}, "
+                                             f"prompt {base.prompt_len}, block {base.block_len}, "
+                                             f"gating {'on' if base.gating else 'off'}"},
+                      "lengths": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -189,6 +227,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=25.0)
     ap.add_argument("--copy-calib", action="store_true", help="run only the copy used to calibrate HBM counters")
+    ap.add_argument("--sweep-gen", action="store_true",
+                    help="decode the workload's model and prompt at generation lengths 64, 128, 256 and 512 and "
+                         "print one JSON line of tokens/s per length")
     ap.add_argument("--ablation", action="store_true",
                     help="decode the workload under each controller preset (component ablation, fixed-threshold "
                          "decoding, fixed-schedule baseline) and print one JSON line of forwards and tokens/s")
@@ -203,6 +244,9 @@ def main():
         return
     if args.ablation:
         ablation(args)
+        return
+    if args.sweep_gen:
+        sweep_gen(args)
         return
 
     import torch

@@ -96,6 +96,24 @@ def test_full_size_stages_and_head(models, name):
     say(f"  head {hs}")
 
 
+@pytest.mark.parametrize("G", [64, 512])
+def test_full_size_decode_replay_gen_lengths(models, G):
+    # the generation-length sweep's extremes (LLaDA-8B shape, batch 1, prompt 256)
+    import dataclasses
+    wl = dataclasses.replace(synth.WORKLOADS["llada_b1"], name=f"llada_b1_g{G}", gen_len=G)
+    _, model = models(wl.model)
+    ctl = B.Controller.gating(wl.gating, block_len=wl.block_len)
+    prompts = synth.make_prompts(wl)
+    say(f"llada_b1 G={G}: decode")
+    res = model.generate(ctl, prompts.cuda(), G, trace=True)
+    torch.cuda.synchronize()
+    ref = replay(res.conf_trace.cpu().numpy(), res.argmax_trace.cpu().numpy(), prompts.numpy(), G,
+                 wl.model.mask_id, ctl)
+    assert_state_equal(res.state, res.forwards, ref)
+    check_invariants(res.state, res.forwards, wl.prompt_len, G, wl.block_len, ctl.T, wl.model.mask_id, ctl)
+    say(f"  forwards per block {res.forwards}")
+
+
 @pytest.mark.parametrize("name", ["llada_b1", "dream_b1"])
 def test_full_size_forward_matches_layer_by_layer(models, name):
     from test_gpu_bf16 import forward_equals_layer_calls
