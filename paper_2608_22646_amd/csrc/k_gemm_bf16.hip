@@ -4,21 +4,23 @@
 //
 // Bv is a "virtual" weight matrix whose rows come from up to three tensors, so
 // q/k/v and gate/up never need to be concatenated in memory:
-//   QKV    : rows [0, n0) of Wq, then n1 rows of Wk, then Wv; the epilogue applies
-//            rotate-half RoPE to q and k and writes q [B,Hq,L,hd], k [B,Hkv,L,hd]
-//            as bf16 and v^T [B,Hkv,hd,L] as the bf16-rounded values in IEEE half.
-//   SWIGLU : 32-row chunks alternate between Wgate and Wup (gate rows f..f+31, then
-//            up rows f..f+31), so one lane holds gate and up of the same column f;
-//            the epilogue writes silu(gate) * up as bf16 [M, F].
+//   QKV    : rows [0, n0) of Wq, then n1 rows of Wk, then Wv; inside each q and k
+//            head the rows are reordered so that every 32-row block holds 16
+//            dimensions d and the matching d + 64 (the rotate-half pair).  The
+//            epilogue applies RoPE and writes q [B,Hq,L,hd], k [B,Hkv,L,hd] as
+//            bf16 and v^T [B,Hkv,hd,L] as the bf16-rounded values in IEEE half.
+//   SWIGLU : 16-row chunks alternate between Wgate and Wup (gate rows f..f+15,
+//            then up rows f..f+15); the epilogue writes silu(gate) * up as bf16
+//            [M, F].
 //   RESID  : plain W; the epilogue adds the result to the float32 residual.
 //
-// Tiling: 128 x 256 x 64 per 256-thread workgroup, 2 x 2 wavefronts, each wave owns
-// a 64 x 128 block of 32x32 MFMA tiles (v_mfma_f32_32x32x16_bf16).  Tiles of A and
-// Bv stream from memory straight into a 3-stage LDS ring (buffer_load_dwordx4 ...
-// lds, no staging registers): two k-tiles are in flight while the third is
-// consumed, with one barrier per k-step.  LDS rows are 128 bytes (64 bf16); the
-// 16-byte chunk c of row r is stored at slot c ^ ((r >> 1) & 7), so the sixteen
-// rows read by sixteen consecutive lanes cover all 64 LDS banks.
+// Tiling: BM x BN x 64 per workgroup of 4 or 8 wavefronts, each wave owning a
+// 64 x 128 or 64 x 96 block of 32x32 MFMA tiles (v_mfma_f32_32x32x16_bf16).
+// Tiles of A and Bv stream from memory straight into a 2- or 3-stage LDS ring
+// (buffer_load_dwordx4 ... lds, no staging registers), with one barrier per
+// k-step.  LDS rows are 128 bytes (64 bf16); the 16-byte chunk c of row r is
+// stored at slot c ^ ((r >> 1) & 7), so the sixteen rows read by sixteen
+// consecutive lanes cover all 64 LDS banks.
 //
 // MFMA register layouts (64 lanes, lane = l):
 //   A operand : row l%32, k = 8*(l/32) .. +7       B operand : col l%32, same k
@@ -34,19 +36,31 @@ namespace {
 
 constexpr int BK = 64;
 
-// Virtual weight row n -> (tensor index, row inside that tensor).  QKV regions
-// are whole 256-row tiles (Hq and Hkv even), so a tile reads a single tensor;
-// SwiGLU rows interleave gate and up every 32 rows.
+// Virtual weight row n -> (tensor index, row inside that tensor).  Every 32-row
+// block of the virtual matrix is self-contained for its epilogue: its rows 0..15
+// and 16..31 are the two operands that meet in one output (gate and up of the
+// same 16 columns f; the rotate-half pair d and d + 64 of the same head for q
+// and k), so the pair sits in lanes l and l ^ 16 of one MFMA result and any
+// wave tile that is a multiple of 32 columns wide can finish it.  Region
+// boundaries (Hq*hd, Hkv*hd rows) are multiples of 128, so no 8-row DMA group
+// crosses tensors.
 template <int EPI>
 __device__ __forceinline__ int2 vrow(const GemmArgs& g, int n) {
   if (EPI == EPI_QKV_ROPE) {
-    if (n < g.n0) return make_int2(0, n);
-    if (n < g.n0 + g.n1) return make_int2(1, n - g.n0);
-    return make_int2(2, n - g.n0 - g.n1);
+    int t = 0;
+    if (n >= g.n0 + g.n1) {
+      return make_int2(2, n - g.n0 - g.n1);  // v: identity
+    } else if (n >= g.n0) {
+      t = 1;
+      n -= g.n0;
+    }
+    const int c = n & 127, blk = c >> 5, w = c & 31;
+    const int dim = (w < 16) ? 16 * blk + w : 64 + 16 * blk + (w - 16);
+    return make_int2(t, (n & ~127) + dim);
   }
   if (EPI == EPI_SWIGLU) {
-    const int chunk = n >> 5;
-    return make_int2(chunk & 1, ((chunk >> 1) << 5) + (n & 31));
+    const int chunk = n >> 4;
+    return make_int2(chunk & 1, ((chunk >> 1) << 4) + (n & 15));
   }
   return make_int2(0, n);
 }
@@ -64,7 +78,7 @@ struct Tile {
   static constexpr int TI = WM / 32, TJ = WN / 32;          // MFMA tiles per wave
   static constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;   // LDS-DMA instructions per wave per stage
   static constexpr int LDS_STAGE = (BM + BN) * 128;
-  static_assert(WN == 128, "the QKV and SwiGLU epilogues need 128-column wave tiles");
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tiles are whole 32 x 32 MFMA blocks");
   static_assert(IA * NW * 8 == BM && IB * NW * 8 == BN, "tile rows must split evenly over the DMA loads");
   static_assert(NW % 2 == 0, "the DMA swizzle assumes an even wave count");
 };
@@ -72,6 +86,10 @@ struct Tile {
 using TileS = Tile<128, 256, 2, 2, 3>;
 // 256 x 256, 8 waves of 64 x 128 (two per SIMD), two stages (large M: fewer bytes per flop)
 using TileL = Tile<256, 256, 4, 2, 2>;
+// 256 x 192, 8 waves of 64 x 96: at M = 512, N = 24576 it makes exactly 256 tiles
+using TileM = Tile<256, 192, 4, 2, 2>;
+// 128 x 192, 4 waves of 64 x 96, three stages
+using TileSM = Tile<128, 192, 2, 2, 3>;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -236,13 +254,16 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
 }
 
 // Epilogue of one unit of a tile: the accumulator rows 8c .. 8c+7 ... that a
-// lane holds for row block i, i.e. v[j][e] = acc[i][j][4c + e] for the TJ = 4
+// lane holds for row block i, i.e. v[j][e] = acc[i][j][4c + e] for the TJ
 // column blocks j of the wave (rows 8c + 4 (lane/32) + e, columns j*32 + lane%32
-// of the wave's 32-row x 128-column block i).
+// of the wave's 32-row block i).  For SwiGLU and q/k the two operands of an
+// output sit in lanes l and l ^ 16 (see vrow): after one exchange of two values
+// the lane with column < 16 holds both operands of rows e = 0, 1 and its partner
+// those of rows e = 2, 3, and each finishes its two rows (one SwiGLU output, or
+// both rotated dimensions d and d + 64).
 template <class TL, int EPI>
 __device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, int m0, int n0, int i, int c,
                                          const float (&v)[TL::TJ][4]) {
-  static_assert(TL::TJ == 4, "epilogues need 128-column wave tiles");
   const int wm = wave / (TL::BN / TL::WN), wn = wave % (TL::BN / TL::WN);
   const int lhalf = lane >> 5, col_in = lane & 31;
   const int mrow = m0 + wm * TL::WM + i * 32 + 8 * c + 4 * lhalf;  // + e
@@ -254,7 +275,7 @@ __device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, 
       const int m = mrow + e;
       if (m >= g.M) continue;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < TL::TJ; ++j) {
         const int n = ncol0 + j * 32 + col_in;
         if (EPI == EPI_RESID)
           g.resid[(size_t)m * g.N + n] += v[j][e];
@@ -265,57 +286,71 @@ __device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, 
     return;
   }
 
-  if (EPI == EPI_SWIGLU) {  // column blocks alternate gate, up: (0, 1) and (2, 3) pair
+  const bool hi = col_in >= 16;   // holds the second operand of the pair
+  const int w = col_in & 15;
+  const int e0 = hi ? 2 : 0;      // first of the two rows this lane finishes
+  // own[k] / oth[k]: this lane's and the partner's value of pair row e0 + k
+  auto exchange = [&](int j, float (&own)[2], float (&oth)[2]) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const float send = hi ? v[j][k] : v[j][2 + k];  // the rows the partner finishes
+      own[k] = hi ? v[j][2 + k] : v[j][k];
+      oth[k] = __shfl_xor(send, 16, 64);
+    }
+  };
+
+  if (EPI == EPI_SWIGLU) {  // lo lanes hold gate, hi lanes up, of column f
     const int F = g.N / 2;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int m = mrow + e;
-      if (m >= g.M) continue;
+    for (int j = 0; j < TL::TJ; ++j) {
+      float own[2], oth[2];
+      exchange(j, own, oth);
+      const int f = (((ncol0 + j * 32) >> 5) << 4) + w;
 #pragma unroll
-      for (int j = 0; j < 4; j += 2) {
-        const int chunk = (ncol0 + j * 32) >> 5;  // even: gate
-        const int f = ((chunk >> 1) << 5) + col_in;
-        const float gt = v[j][e], up = v[j + 1][e];
+      for (int k = 0; k < 2; ++k) {
+        const int m = mrow + e0 + k;
+        if (m >= g.M) continue;
+        const float gt = hi ? oth[k] : own[k], up = hi ? own[k] : oth[k];
         g.out[(size_t)m * F + f] = f2bf(gt / (1.0f + expf(-gt)) * up);
       }
     }
     return;
   }
 
-  // EPI_QKV_ROPE: this wave's 128 columns are exactly one head (hd = 128).
   if (EPI == EPI_QKV_ROPE) {
     constexpr int HD = 128, HALF = 64;
     const int nq = g.Hq * HD, nk_ = g.Hkv * HD;
-    if (ncol0 < nq + nk_) {
-      const bool isq = ncol0 < nq;
-      const int head = isq ? ncol0 / HD : (ncol0 - nq) / HD;
-      const int H = isq ? g.Hq : g.Hkv;
-      bf16_t* dst = isq ? g.q : g.k;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int m = mrow + e;
-        if (m >= g.M) continue;
-        const int b = m / g.L, pos = m - b * g.L;
-        bf16_t* o = dst + (((size_t)b * H + head) * g.L + pos) * HD;
+    for (int j = 0; j < TL::TJ; ++j) {
+      const int vb = ncol0 + j * 32;  // first virtual column of the block (wave-uniform)
+      if (vb < nq + nk_) {
+        // lo lanes hold x1 = dimension d, hi lanes x2 = dimension d + 64 of one head
+        float own[2], oth[2];
+        exchange(j, own, oth);
+        const bool isq = vb < nq;
+        const int rel = isq ? vb : vb - nq;
+        const int head = rel / HD, d = 16 * ((rel % HD) >> 5) + w;
+        const int H = isq ? g.Hq : g.Hkv;
+        bf16_t* dst = isq ? g.q : g.k;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int jj = j * 32 + col_in;  // < 64: pairs with jj + 64 (column block j + 2)
-          const float cs = g.cosb[(size_t)pos * HALF + jj], sn = g.sinb[(size_t)pos * HALF + jj];
-          const float x1 = v[j][e], x2 = v[j + 2][e];
-          o[jj] = f2bf(x1 * cs - x2 * sn);
-          o[jj + HALF] = f2bf(x2 * cs + x1 * sn);
+        for (int k = 0; k < 2; ++k) {
+          const int m = mrow + e0 + k;
+          if (m >= g.M) continue;
+          const int b = m / g.L, pos = m - b * g.L;
+          const float cs = g.cosb[(size_t)pos * HALF + d], sn = g.sinb[(size_t)pos * HALF + d];
+          const float x1 = hi ? oth[k] : own[k], x2 = hi ? own[k] : oth[k];
+          bf16_t* o = dst + (((size_t)b * H + head) * g.L + pos) * HD;
+          o[d] = f2bf(x1 * cs - x2 * sn);
+          o[d + HALF] = f2bf(x2 * cs + x1 * sn);
         }
-      }
-    } else {
-      const int head = (ncol0 - nq - nk_) / HD;
+      } else {
+        const int rel = vb - nq - nk_;
+        const int head = rel / HD, cj = rel % HD + col_in;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int m = mrow + e;
-        if (m >= g.M) continue;
-        const int b = m / g.L, pos = m - b * g.L;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int cj = j * 32 + col_in;
+        for (int e = 0; e < 4; ++e) {
+          const int m = mrow + e;
+          if (m >= g.M) continue;
+          const int b = m / g.L, pos = m - b * g.L;
           // v is a bf16 value; it is stored as IEEE half (exact in half's range)
           // for the half-precision P.V product of the attention kernel
           g.vt[(((size_t)b * g.Hkv + head) * HD + cj) * g.L + pos] = f2h(bf2f(f2bf(v[j][e])));
@@ -395,10 +430,12 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
 }
 
 // resid[m, n] += sum_z part[z, m, n], z in order.
-__global__ void splitk_resid_kernel(const float* __restrict__ part, float* __restrict__ resid, long MN, int S) {
+template <int S>
+__global__ void splitk_resid_kernel(const float* __restrict__ part, float* __restrict__ resid, long MN) {
   const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= MN) return;
   float4 acc = *reinterpret_cast<const float4*>(part + i);
+#pragma unroll
   for (int z = 1; z < S; ++z) {
     const float4 v = *reinterpret_cast<const float4*>(part + (size_t)z * MN + i);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
@@ -412,17 +449,24 @@ struct Plan {
   int bm, bn, split;
 };
 
-// Pick the tile (128 x 256 on 4 waves or 256 x 256 on 8 waves) and, for the
-// residual GEMMs, a K split, by the number of rounds of workgroups over the
-// 256 compute units weighted by each tile's measured per-CU throughput
-// (the larger tile moves fewer bytes per flop: ~1.3x faster per flop).
+// Pick the tile and, for the residual GEMMs, a K split, by the number of rounds
+// of workgroups over the 256 compute units weighted by each tile's measured
+// per-CU throughput relative to the 128 x 256 tile (larger tiles move fewer
+// LDS bytes per flop and run two waves per SIMD).  The 192-wide tiles exist for
+// the widths where 256-wide tiles leave a quarter of the CUs idle (batch-1
+// q/k/v and gate/up); per k-step they are hardly faster than the 256-wide ones,
+// hence their lower per-flop speed.
 Plan plan(int M, int N, int K, int epi) {
-  const double rel_speed[2] = {1.0, 1.3};
-  const int bms[2] = {128, 256};
-  Plan best{128, 256, 1};
+  struct Cand {
+    int bm, bn;
+    double rel_speed;
+  };
+  const Cand cands[] = {{128, 256, 1.0}, {256, 256, 1.3}, {256, 192, 1.08}, {128, 192, 0.95}};
+  Plan best{0, 0, 0};
   double best_cost = 1e30;
-  for (int c = 0; c < 2; ++c) {
-    const long tiles = (long)((M + bms[c] - 1) / bms[c]) * (N / 256);
+  for (const Cand& c : cands) {
+    if (N % c.bn != 0) continue;
+    const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
     int split = 1;
     if (epi == EPI_RESID) {
       while (split < 8 && tiles * split * 2 <= 256 + 64 && (K / BK) % (split * 2) == 0 && (K / BK) / (split * 2) >= 4)
@@ -430,12 +474,13 @@ Plan plan(int M, int N, int K, int epi) {
     }
     const long wgs = tiles * split;
     const double rounds = (double)((wgs + 255) / 256);
-    const double cost = rounds * (double)bms[c] / split / rel_speed[c];
+    const double cost = rounds * (double)c.bm * c.bn / 256.0 / split / c.rel_speed;
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
-      best = Plan{bms[c], 256, split};
+      best = Plan{c.bm, c.bn, split};
     }
   }
+  if (best.bm == 0) throw HipError("gemm_bf16: N must be a multiple of 192 or 256");
   return best;
 }
 
@@ -451,10 +496,14 @@ void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
 
 template <int EPI>
 void launch_epi(const GemmArgs& g, const Plan& p, hipStream_t s) {
-  if (p.bm == 256)
+  if (p.bm == 256 && p.bn == 256)
     launch_tile<TileL, EPI>(g, p.split, s);
-  else
+  else if (p.bm == 256)
+    launch_tile<TileM, EPI>(g, p.split, s);
+  else if (p.bn == 256)
     launch_tile<TileS, EPI>(g, p.split, s);
+  else
+    launch_tile<TileSM, EPI>(g, p.split, s);
 }
 
 }  // namespace
@@ -467,9 +516,9 @@ size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi) {
 void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   if (defer) *defer = PendingResid{};
   if (a.M == 0) return;
-  if (a.N % 256 != 0 || a.K % BK != 0) throw HipError("gemm_bf16: N % 256 and K % 64 must be 0");
-  if (a.epi == EPI_QKV_ROPE && (a.n0 % 256 != 0 || a.n1 % 256 != 0))
-    throw HipError("gemm_bf16: q and k/v regions must be multiples of 256 rows");
+  if (a.K % BK != 0) throw HipError("gemm_bf16: K % 64 must be 0");
+  if (a.epi == EPI_QKV_ROPE && (a.n0 % 128 != 0 || a.n1 % 128 != 0))
+    throw HipError("gemm_bf16: q and k/v regions must be whole 128-row heads");
   const Plan p = plan(a.M, a.N, a.K, a.epi);
   switch (a.epi) {
     case EPI_QKV_ROPE: launch_epi<EPI_QKV_ROPE>(a, p, s); break;
@@ -482,8 +531,13 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
     *defer = PendingResid{a.splitk_buf, p.split};
   } else if (p.split > 1) {
     const long MN = (long)a.M * a.N;
-    hipLaunchKernelGGL(splitk_resid_kernel, dim3(ceil_div(MN / 4, 256)), dim3(256), 0, s, a.splitk_buf, a.resid, MN,
-                       p.split);
+    const dim3 grid(ceil_div(MN / 4, 256));
+    switch (p.split) {
+      case 2: hipLaunchKernelGGL(splitk_resid_kernel<2>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN); break;
+      case 4: hipLaunchKernelGGL(splitk_resid_kernel<4>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN); break;
+      case 8: hipLaunchKernelGGL(splitk_resid_kernel<8>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN); break;
+      default: throw HipError("splitk_resid: split must be 2, 4 or 8");
+    }
     DLLM_LAUNCH_CHECK("splitk_resid");
   }
 }

@@ -1,6 +1,8 @@
 // Embedding gather, RoPE table, RMSNorm and decoding-state initialisation.
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace dllm {
 
 int device_cu_count() {
@@ -160,9 +162,9 @@ void launch_rmsnorm_t(const float* h, const TG* g, TO* out, int B, int rows, int
 // rmsnorm_vec_kernel preceded by the split-K residual update of its row: each
 // float4 of the row is h + ((p_0 + p_1) + ... + p_{S-1}), the same operations in
 // the same order as splitk_resid_kernel, written back to h and kept for the norm.
-template <int NV>
+template <int NV, int S>
 __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ part,
-                                                            int S, long MN, const bf16_t* __restrict__ g,
+                                                            long MN, const bf16_t* __restrict__ g,
                                                             bf16_t* __restrict__ out, int d, float eps) {
   const int r = blockIdx.x;
   float* row = h + (size_t)r * d;
@@ -175,6 +177,7 @@ __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ 
     if (c < d4) {
       const size_t i = (size_t)r * d4 + c;
       float4 acc = reinterpret_cast<const float4*>(part)[i];
+#pragma unroll
       for (int z = 1; z < S; ++z) {
         const float4 p = reinterpret_cast<const float4*>(part + (size_t)z * MN)[i];
         acc.x += p.x;
@@ -218,12 +221,25 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
     throw HipError("resid_rmsnorm: needs d % 4 == 0, d <= 8192 and 16-byte aligned rows");
   const long MN = (long)M * d;
   const int nv = ceil_div(d, 1024);
+  // the split count is a template parameter so that every partial's loads are in flight at once
+  auto go = [&](auto nvc, auto sc) {
+    hipLaunchKernelGGL((resid_rmsnorm_kernel<decltype(nvc)::value, decltype(sc)::value>), dim3(M), dim3(256), 0, s, h,
+                       pend.part, MN, g, out, d, eps);
+  };
+  auto by_split = [&](auto nvc) {
+    switch (pend.split) {
+      case 2: go(nvc, std::integral_constant<int, 2>{}); break;
+      case 4: go(nvc, std::integral_constant<int, 4>{}); break;
+      case 8: go(nvc, std::integral_constant<int, 8>{}); break;
+      default: throw HipError("resid_rmsnorm: split must be 2, 4 or 8");
+    }
+  };
   if (nv <= 2)
-    hipLaunchKernelGGL(resid_rmsnorm_kernel<2>, dim3(M), dim3(256), 0, s, h, pend.part, pend.split, MN, g, out, d, eps);
+    by_split(std::integral_constant<int, 2>{});
   else if (nv <= 4)
-    hipLaunchKernelGGL(resid_rmsnorm_kernel<4>, dim3(M), dim3(256), 0, s, h, pend.part, pend.split, MN, g, out, d, eps);
+    by_split(std::integral_constant<int, 4>{});
   else
-    hipLaunchKernelGGL(resid_rmsnorm_kernel<8>, dim3(M), dim3(256), 0, s, h, pend.part, pend.split, MN, g, out, d, eps);
+    by_split(std::integral_constant<int, 8>{});
   DLLM_LAUNCH_CHECK("resid_rmsnorm");
 }
 

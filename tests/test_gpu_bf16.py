@@ -20,12 +20,29 @@ SMALL = synth.ModelConfig("small-bf16", n_layers=2, d_model=512, n_heads=4, n_kv
                           norm_gain_std=0.1)
 
 
-@pytest.fixture(scope="module")
-def small():
-    w_cpu = synth.make_weights(SMALL, "cpu")
-    model = B.Model(SMALL, [w.to("cuda") for w in w_cpu])
+# Widths that are multiples of 192 as well as 256, so the GEMMs also run their
+# 192-wide tiles: q/k/v = 768 virtual rows (a 192-column tile spans q and k, or
+# k and v), gate/up = 2304, and Hq*hd = 256 != d_model.
+SMALL192 = synth.ModelConfig("small192-bf16", n_layers=2, d_model=768, n_heads=2, n_kv_heads=2, head_dim=128,
+                             d_ff=1152, vocab=3000, rope_base=10000.0, dtype="bf16",
+                             lm_head_std=5 / math.sqrt(768), norm_gain_std=0.1)
+
+
+def _load(cfg):
+    w_cpu = synth.make_weights(cfg, "cpu")
+    model = B.Model(cfg, [w.to("cuda") for w in w_cpu])
     wnp = [w.to(torch.float32).numpy() for w in w_cpu]
     return model, wnp
+
+
+@pytest.fixture(scope="module")
+def small():
+    return _load(SMALL)
+
+
+@pytest.fixture(scope="module")
+def small192():
+    return _load(SMALL192)
 
 
 @pytest.mark.parametrize("Bn,P,G", [(2, 40, 64), (1, 9, 32), (2, 1036, 64)])
@@ -43,6 +60,24 @@ def test_forward_stages(small, Bn, P, G):
         st = check_layer(model, SMALL, wnp, ws, Bn, L, l, rows=rows)
         say(f"  layer {l}: " + ", ".join(f"{k}={v:.2e}" for k, v in st.items()))
     hs = check_head(model, SMALL, wnp, ws, Bn, L, P, min(32, G))
+    say(f"  head: {hs}")
+
+
+@pytest.mark.parametrize("Bn,P,G", [(2, 40, 64), (2, 1936, 64)])
+def test_forward_stages_192_wide_tiles(small192, Bn, P, G):
+    """M = 208 (128 x 192 tiles) and 4000 (256 x 192 tiles for gate/up, ragged in
+    M); every q/k/v, SwiGLU and residual epilogue on 192-column tiles."""
+    model, wnp = small192
+    L = P + G
+    say(f"bf16 stages (192-wide tiles) B={Bn} L={L}")
+    x = synth.make_ints((Bn, L), 6, 0, SMALL192.vocab - 1).cuda()
+    ws = model.workspace(Bn, L, 32)
+    model.embed(x, ws)
+    rows = None if Bn * L <= 300 else np.sort(np.random.default_rng(1).choice(Bn * L, 96, replace=False))
+    for l in range(SMALL192.n_layers):
+        st = check_layer(model, SMALL192, wnp, ws, Bn, L, l, rows=rows)
+        say(f"  layer {l}: " + ", ".join(f"{k}={v:.2e}" for k, v in st.items()))
+    hs = check_head(model, SMALL192, wnp, ws, Bn, L, P, min(32, G))
     say(f"  head: {hs}")
 
 
@@ -70,6 +105,13 @@ def test_forward_matches_layer_by_layer(small, Bn, P, G):
     model, _ = small
     say(f"bf16 fused forward vs layer calls B={Bn} L={P + G}")
     forward_equals_layer_calls(model, SMALL, Bn, P, G, seed=9)
+
+
+@pytest.mark.parametrize("Bn,P,G", [(2, 40, 64), (2, 1936, 64)])
+def test_forward_matches_layer_by_layer_192(small192, Bn, P, G):
+    model, _ = small192
+    say(f"bf16 fused forward vs layer calls (192-wide tiles) B={Bn} L={P + G}")
+    forward_equals_layer_calls(model, SMALL192, Bn, P, G, seed=10)
 
 
 def _head_model(V, d, mask_id_at_top=True):
