@@ -253,14 +253,11 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
   }
 }
 
-// Epilogue of one unit of a tile: the accumulator rows 8c .. 8c+7 ... that a
-// lane holds for row block i, i.e. v[j][e] = acc[i][j][4c + e] for the TJ
-// column blocks j of the wave (rows 8c + 4 (lane/32) + e, columns j*32 + lane%32
-// of the wave's 32-row block i).  For SwiGLU and q/k the two operands of an
-// output sit in lanes l and l ^ 16 (see vrow): after one exchange of two values
-// the lane with column < 16 holds both operands of rows e = 0, 1 and its partner
-// those of rows e = 2, 3, and each finishes its two rows (one SwiGLU output, or
-// both rotated dimensions d and d + 64).
+// Epilogue of one unit of a tile for the float32 residual (or a plain bf16
+// store): the accumulator rows 8c .. 8c+7 ... that a lane holds for row block
+// i, i.e. v[j][e] = acc[i][j][4c + e] for the TJ column blocks j of the wave
+// (rows 8c + 4 (lane/32) + e, columns j*32 + lane%32 of the wave's 32-row
+// block i); 32 lanes cover 128 contiguous bytes of a residual row.
 template <class TL, int EPI>
 __device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, int m0, int n0, int i, int c,
                                          const float (&v)[TL::TJ][4]) {
@@ -268,92 +265,171 @@ __device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, 
   const int lhalf = lane >> 5, col_in = lane & 31;
   const int mrow = m0 + wm * TL::WM + i * 32 + 8 * c + 4 * lhalf;  // + e
   const int ncol0 = n0 + wn * TL::WN;                               // + j*32 + col_in
-
-  if (EPI == EPI_RESID || EPI == EPI_STORE) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int m = mrow + e;
-      if (m >= g.M) continue;
+  for (int e = 0; e < 4; ++e) {
+    const int m = mrow + e;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < TL::TJ; ++j) {
+      const int n = ncol0 + j * 32 + col_in;
+      if (EPI == EPI_RESID)
+        g.resid[(size_t)m * g.N + n] += v[j][e];
+      else
+        g.out[(size_t)m * g.N + n] = f2bf(v[j][e]);
+    }
+  }
+}
+
+// LDS staging of the SwiGLU and q/k/v epilogues.  Their outputs are 16-bit and,
+// written straight from the MFMA layout, would go out as 2-byte stores (v^T
+// even touching 32 cache lines per instruction).  Instead each wave writes its
+// finished values into the LDS ring (free once the main loop is done) in the
+// destination's order, and the workgroup then stores 16-byte chunks.
+template <class TL>
+struct Stage {
+  // SwiGLU: [BM][BN/2] bf16, rows padded by 16 bytes (conflict-free writes)
+  static constexpr int SW_ROW = TL::BN + 16;
+  static constexpr int SW_BYTES = TL::BM * SW_ROW;
+  // q/k/v: one area per 32-column block; a q/k block holds [BM][32] bf16
+  // (64-byte rows: dimensions d .. d+15, then d+64 .. d+79), a v block
+  // [32][BM] half (v^T, each column padded by 16 bytes)
+  static constexpr int VROW = (TL::BM + 8) * 2;
+  static constexpr int BLK = (TL::BM * 64 > 32 * VROW) ? TL::BM * 64 : 32 * VROW;
+  static constexpr int QKV_BYTES = TL::BN / 32 * BLK;
+};
+
+template <class TL, int EPI>
+constexpr size_t lds_bytes() {
+  const size_t ring = (size_t)TL::S * TL::LDS_STAGE;
+  const size_t st = EPI == EPI_SWIGLU ? Stage<TL>::SW_BYTES : EPI == EPI_QKV_ROPE ? Stage<TL>::QKV_BYTES : 0;
+  return ring > st ? ring : st;
+}
+
+template <class TL, int EPI>
+__device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, int wave, int lane, int m0, int n0,
+                                                const f32x16_t (&acc)[TL::TI][TL::TJ]) {
+  using St = Stage<TL>;
+  constexpr int HD = 128, HALF = 64;
+  const int wm = wave / (TL::BN / TL::WN), wn = wave % (TL::BN / TL::WN);
+  const int lhalf = lane >> 5, col_in = lane & 31, w = col_in & 15;
+  // For SwiGLU and q/k the two operands of an output sit in lanes l and l ^ 16
+  // (see vrow): after one exchange of two values the lane with column < 16
+  // holds both operands of rows e = 0, 1 and its partner those of rows 2, 3.
+  const bool hi = col_in >= 16;
+  const int e0 = hi ? 2 : 0;
+  const int nq = g.Hq * HD, nkv = g.Hkv * HD;
+
+  wait_vm_lds<0>();
+  barrier_nofence();  // every wave is done reading the ring
+
+#pragma unroll
+  for (int i = 0; i < TL::TI; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int rl0 = wm * TL::WM + i * 32 + 8 * c + 4 * lhalf;  // tile row of e = 0
 #pragma unroll
       for (int j = 0; j < TL::TJ; ++j) {
-        const int n = ncol0 + j * 32 + col_in;
-        if (EPI == EPI_RESID)
-          g.resid[(size_t)m * g.N + n] += v[j][e];
-        else
-          g.out[(size_t)m * g.N + n] = f2bf(v[j][e]);
-      }
-    }
-    return;
-  }
-
-  const bool hi = col_in >= 16;   // holds the second operand of the pair
-  const int w = col_in & 15;
-  const int e0 = hi ? 2 : 0;      // first of the two rows this lane finishes
-  // own[k] / oth[k]: this lane's and the partner's value of pair row e0 + k
-  auto exchange = [&](int j, float (&own)[2], float (&oth)[2]) {
+        const int tcol = wn * TL::WN + j * 32;  // tile column of the block (wave-uniform)
+        float v[4];
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const float send = hi ? v[j][k] : v[j][2 + k];  // the rows the partner finishes
-      own[k] = hi ? v[j][2 + k] : v[j][k];
-      oth[k] = __shfl_xor(send, 16, 64);
-    }
-  };
-
-  if (EPI == EPI_SWIGLU) {  // lo lanes hold gate, hi lanes up, of column f
-    const int F = g.N / 2;
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * c + e];
+        const bool pair = EPI == EPI_SWIGLU || n0 + tcol < nq + nkv;
+        float own[2] = {0.f, 0.f}, oth[2] = {0.f, 0.f};
+        if (pair) {
 #pragma unroll
-    for (int j = 0; j < TL::TJ; ++j) {
-      float own[2], oth[2];
-      exchange(j, own, oth);
-      const int f = (((ncol0 + j * 32) >> 5) << 4) + w;
-#pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        const int m = mrow + e0 + k;
-        if (m >= g.M) continue;
-        const float gt = hi ? oth[k] : own[k], up = hi ? own[k] : oth[k];
-        g.out[(size_t)m * F + f] = f2bf(gt / (1.0f + expf(-gt)) * up);
-      }
-    }
-    return;
-  }
-
-  if (EPI == EPI_QKV_ROPE) {
-    constexpr int HD = 128, HALF = 64;
-    const int nq = g.Hq * HD, nk_ = g.Hkv * HD;
-#pragma unroll
-    for (int j = 0; j < TL::TJ; ++j) {
-      const int vb = ncol0 + j * 32;  // first virtual column of the block (wave-uniform)
-      if (vb < nq + nk_) {
-        // lo lanes hold x1 = dimension d, hi lanes x2 = dimension d + 64 of one head
-        float own[2], oth[2];
-        exchange(j, own, oth);
-        const bool isq = vb < nq;
-        const int rel = isq ? vb : vb - nq;
-        const int head = rel / HD, d = 16 * ((rel % HD) >> 5) + w;
-        const int H = isq ? g.Hq : g.Hkv;
-        bf16_t* dst = isq ? g.q : g.k;
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-          const int m = mrow + e0 + k;
-          if (m >= g.M) continue;
-          const int b = m / g.L, pos = m - b * g.L;
-          const float cs = g.cosb[(size_t)pos * HALF + d], sn = g.sinb[(size_t)pos * HALF + d];
-          const float x1 = hi ? oth[k] : own[k], x2 = hi ? own[k] : oth[k];
-          bf16_t* o = dst + (((size_t)b * H + head) * g.L + pos) * HD;
-          o[d] = f2bf(x1 * cs - x2 * sn);
-          o[d + HALF] = f2bf(x2 * cs + x1 * sn);
+          for (int k = 0; k < 2; ++k) {
+            const float send = hi ? v[k] : v[2 + k];  // the rows the partner finishes
+            own[k] = hi ? v[2 + k] : v[k];
+            oth[k] = __shfl_xor(send, 16, 64);
+          }
         }
-      } else {
-        const int rel = vb - nq - nk_;
-        const int head = rel / HD, cj = rel % HD + col_in;
+        if (EPI == EPI_SWIGLU) {  // lo lanes hold gate, hi lanes up
+          const int fl = (tcol >> 1) + w;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int m = mrow + e;
-          if (m >= g.M) continue;
+          for (int k = 0; k < 2; ++k) {
+            const float gt = hi ? oth[k] : own[k], up = hi ? own[k] : oth[k];
+            *reinterpret_cast<bf16_t*>(lds + (rl0 + e0 + k) * St::SW_ROW + fl * 2) =
+                f2bf(gt / (1.0f + expf(-gt)) * up);
+          }
+        } else {
+          char* blk = lds + (tcol >> 5) * St::BLK;
+          if (pair) {  // q or k: lo lanes hold x1 = dimension d, hi lanes x2 = d + 64
+            const int rel = n0 + tcol < nq ? n0 + tcol : n0 + tcol - nq;
+            const int d = 16 * ((rel % HD) >> 5) + w;
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+              const int rl = rl0 + e0 + k;
+              const int m = min(m0 + rl, g.M - 1);  // rows past M are staged but never stored
+              const int pos = m % g.L;
+              const float cs = g.cosb[(size_t)pos * HALF + d], sn = g.sinb[(size_t)pos * HALF + d];
+              const float x1 = hi ? oth[k] : own[k], x2 = hi ? own[k] : oth[k];
+              *reinterpret_cast<bf16_t*>(blk + rl * 64 + w * 2) = f2bf(x1 * cs - x2 * sn);
+              *reinterpret_cast<bf16_t*>(blk + rl * 64 + (16 + w) * 2) = f2bf(x2 * cs + x1 * sn);
+            }
+          } else {  // v: four consecutive rows of column col_in, as IEEE half of the bf16 value
+            uint2 pk;
+            pk.x = (uint32_t)f2h(bf2f(f2bf(v[0]))) | ((uint32_t)f2h(bf2f(f2bf(v[1]))) << 16);
+            pk.y = (uint32_t)f2h(bf2f(f2bf(v[2]))) | ((uint32_t)f2h(bf2f(f2bf(v[3]))) << 16);
+            *reinterpret_cast<uint2*>(blk + col_in * St::VROW + rl0 * 2) = pk;
+          }
+        }
+      }
+    }
+
+  __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+  barrier_nofence();
+
+  const int tid = threadIdx.x;
+  if (EPI == EPI_SWIGLU) {
+    const int F = g.N / 2, f0 = n0 / 2;
+    constexpr int CH = TL::BN / 16;  // 16-byte chunks per row
+    for (int it = tid; it < TL::BM * CH; it += TL::NTH) {
+      const int r = it / CH, q = it - r * CH, m = m0 + r;
+      if (m < g.M)
+        *reinterpret_cast<uint4*>(g.out + (size_t)m * F + f0 + 8 * q) =
+            *reinterpret_cast<const uint4*>(lds + r * St::SW_ROW + 16 * q);
+    }
+    return;
+  }
+#pragma unroll 1
+  for (int jb = 0; jb < TL::BN / 32; ++jb) {
+    const int vb = n0 + jb * 32;
+    const char* blk = lds + jb * St::BLK;
+    if (vb < nq + nkv) {
+      const bool isq = vb < nq;
+      const int rel = isq ? vb : vb - nq;
+      const int head = rel / HD, d0 = 16 * ((rel % HD) >> 5);
+      const int H = isq ? g.Hq : g.Hkv;
+      bf16_t* dst = isq ? g.q : g.k;
+      for (int it = tid; it < TL::BM * 4; it += TL::NTH) {
+        const int r = it >> 2, q = it & 3, m = m0 + r;
+        if (m >= g.M) continue;
+        const int b = m / g.L, pos = m - b * g.L;
+        const int dim = (q < 2 ? d0 : HALF + d0) + 8 * (q & 1);
+        *reinterpret_cast<uint4*>(dst + (((size_t)b * H + head) * g.L + pos) * HD + dim) =
+            *reinterpret_cast<const uint4*>(blk + r * 64 + 16 * q);
+      }
+    } else {
+      const int rel = vb - nq - nkv;
+      const int head = rel / HD, cj0 = rel % HD;
+      constexpr int RC = TL::BM / 8;  // 8-row chunks per column
+      for (int it = tid; it < 32 * RC; it += TL::NTH) {
+        const int c = it / RC, t = it - c * RC, m = m0 + 8 * t;
+        if (m >= g.M) continue;
+        const uint4 val = *reinterpret_cast<const uint4*>(blk + c * St::VROW + 16 * t);
+        if ((g.L & 7) == 0 && m + 7 < g.M) {
+          // eight positions of one sequence, 16-byte aligned (L % 8 == 0, m % 8 == 0)
           const int b = m / g.L, pos = m - b * g.L;
-          // v is a bf16 value; it is stored as IEEE half (exact in half's range)
-          // for the half-precision P.V product of the attention kernel
-          g.vt[(((size_t)b * g.Hkv + head) * HD + cj) * g.L + pos] = f2h(bf2f(f2bf(v[j][e])));
+          *reinterpret_cast<uint4*>(g.vt + (((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos) = val;
+        } else {
+          const uint32_t wd[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int mm = m + e;
+            if (mm >= g.M) break;
+            const int b = mm / g.L, pos = mm - b * g.L;
+            g.vt[(((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos] = (f16_t)(wd[e >> 1] >> (16 * (e & 1)));
+          }
         }
       }
     }
@@ -425,7 +501,10 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
       }
     return;
   }
-  epilogue<TL, EPI>(g, wave, lane, o.x, o.y, acc);
+  if (EPI == EPI_SWIGLU || EPI == EPI_QKV_ROPE)
+    epilogue_staged<TL, EPI>(g, lds, wave, lane, o.x, o.y, acc);
+  else
+    epilogue<TL, EPI>(g, wave, lane, o.x, o.y, acc);
 #endif
 }
 
@@ -487,7 +566,7 @@ Plan plan(int M, int N, int K, int epi) {
 template <class TL, int EPI>
 void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
   const int tiles = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
-  const size_t lds = (size_t)TL::S * TL::LDS_STAGE;
+  const size_t lds = lds_bytes<TL, EPI>();
   static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<TL, EPI>,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hip_check(attr, "hipFuncSetAttribute(gemm_bf16)");
