@@ -305,6 +305,30 @@ constexpr size_t lds_bytes() {
   return ring > st ? ring : st;
 }
 
+// The value lane l ^ 16 holds (v_permlane16_swap: a VALU exchange of the odd
+// and even 16-lane rows; with both operands equal its two results are the
+// values of the lower and the upper row at this position).
+__device__ __forceinline__ float swap16(float x, bool hi) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(hi ? r[0] : r[1]);
+}
+
+// (sequence, position) of token row m = b L + pos, by a float reciprocal and a
+// one-step fixup: exact for m < 2^24 and B < 2^16 (the estimate of m / L is
+// then off by less than one), several times cheaper than an integer division.
+__device__ __forceinline__ int2 seq_pos(int m, int L, float inv_l) {
+  int b = (int)((float)m * inv_l);
+  int p = m - b * L;
+  if (p < 0) {
+    p += L;
+    --b;
+  } else if (p >= L) {
+    p -= L;
+    ++b;
+  }
+  return make_int2(b, p);
+}
+
 template <class TL, int EPI>
 __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, int wave, int lane, int m0, int n0,
                                                 const f32x16_t (&acc)[TL::TI][TL::TJ]) {
@@ -322,8 +346,38 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
   wait_vm_lds<0>();
   barrier_nofence();  // every wave is done reading the ring
 
+  const float inv_l = 1.0f / (float)g.L;
 #pragma unroll
-  for (int i = 0; i < TL::TI; ++i)
+  for (int i = 0; i < TL::TI; ++i) {
+    // q/k: the RoPE table values of this lane's two finished rows in each of
+    // the four 8-row groups of row block i, for every q/k column block, all
+    // loaded before the first is used
+    float cs[4][TL::TJ][2], sn[4][TL::TJ][2];
+    if (EPI == EPI_QKV_ROPE) {
+      int pos[4][2];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          // rows past M are staged but never stored
+          const int m = min(m0 + wm * TL::WM + i * 32 + 8 * c + 4 * lhalf + e0 + k, g.M - 1);
+          pos[c][k] = seq_pos(m, g.L, inv_l).y;
+        }
+#pragma unroll
+      for (int j = 0; j < TL::TJ; ++j) {
+        const int vb = n0 + wn * TL::WN + j * 32;
+        if (vb >= nq + nkv) continue;
+        const int rel = vb < nq ? vb : vb - nq;
+        const int d = 16 * ((rel % HD) >> 5) + w;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int k = 0; k < 2; ++k) {
+            cs[c][j][k] = g.cosb[(size_t)pos[c][k] * HALF + d];
+            sn[c][j][k] = g.sinb[(size_t)pos[c][k] * HALF + d];
+          }
+      }
+    }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int rl0 = wm * TL::WM + i * 32 + 8 * c + 4 * lhalf;  // tile row of e = 0
@@ -340,7 +394,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
           for (int k = 0; k < 2; ++k) {
             const float send = hi ? v[k] : v[2 + k];  // the rows the partner finishes
             own[k] = hi ? v[2 + k] : v[k];
-            oth[k] = __shfl_xor(send, 16, 64);
+            oth[k] = swap16(send, hi);
           }
         }
         if (EPI == EPI_SWIGLU) {  // lo lanes hold gate, hi lanes up
@@ -348,23 +402,20 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
 #pragma unroll
           for (int k = 0; k < 2; ++k) {
             const float gt = hi ? oth[k] : own[k], up = hi ? own[k] : oth[k];
+            // silu with the hardware exp2 and reciprocal: the result is rounded to bf16
             *reinterpret_cast<bf16_t*>(lds + (rl0 + e0 + k) * St::SW_ROW + fl * 2) =
-                f2bf(gt / (1.0f + expf(-gt)) * up);
+                f2bf(__fdividef(gt, 1.0f + __expf(-gt)) * up);
           }
         } else {
           char* blk = lds + (tcol >> 5) * St::BLK;
           if (pair) {  // q or k: lo lanes hold x1 = dimension d, hi lanes x2 = d + 64
-            const int rel = n0 + tcol < nq ? n0 + tcol : n0 + tcol - nq;
-            const int d = 16 * ((rel % HD) >> 5) + w;
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
               const int rl = rl0 + e0 + k;
-              const int m = min(m0 + rl, g.M - 1);  // rows past M are staged but never stored
-              const int pos = m % g.L;
-              const float cs = g.cosb[(size_t)pos * HALF + d], sn = g.sinb[(size_t)pos * HALF + d];
               const float x1 = hi ? oth[k] : own[k], x2 = hi ? own[k] : oth[k];
-              *reinterpret_cast<bf16_t*>(blk + rl * 64 + w * 2) = f2bf(x1 * cs - x2 * sn);
-              *reinterpret_cast<bf16_t*>(blk + rl * 64 + (16 + w) * 2) = f2bf(x2 * cs + x1 * sn);
+              const float c_ = cs[c][j][k], s_ = sn[c][j][k];
+              *reinterpret_cast<bf16_t*>(blk + rl * 64 + w * 2) = f2bf(x1 * c_ - x2 * s_);
+              *reinterpret_cast<bf16_t*>(blk + rl * 64 + (16 + w) * 2) = f2bf(x2 * c_ + x1 * s_);
             }
           } else {  // v: four consecutive rows of column col_in, as IEEE half of the bf16 value
             uint2 pk;
@@ -375,6 +426,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
         }
       }
     }
+  }
 
   __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
   barrier_nofence();
@@ -404,7 +456,8 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
       for (int it = tid; it < TL::BM * 4; it += TL::NTH) {
         const int r = it >> 2, q = it & 3, m = m0 + r;
         if (m >= g.M) continue;
-        const int b = m / g.L, pos = m - b * g.L;
+        const int2 bp = seq_pos(m, g.L, inv_l);
+        const int b = bp.x, pos = bp.y;
         const int dim = (q < 2 ? d0 : HALF + d0) + 8 * (q & 1);
         *reinterpret_cast<uint4*>(dst + (((size_t)b * H + head) * g.L + pos) * HD + dim) =
             *reinterpret_cast<const uint4*>(blk + r * 64 + 16 * q);
@@ -419,7 +472,8 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
         const uint4 val = *reinterpret_cast<const uint4*>(blk + c * St::VROW + 16 * t);
         if ((g.L & 7) == 0 && m + 7 < g.M) {
           // eight positions of one sequence, 16-byte aligned (L % 8 == 0, m % 8 == 0)
-          const int b = m / g.L, pos = m - b * g.L;
+          const int2 bp = seq_pos(m, g.L, inv_l);
+          const int b = bp.x, pos = bp.y;
           *reinterpret_cast<uint4*>(g.vt + (((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos) = val;
         } else {
           const uint32_t wd[4] = {val.x, val.y, val.z, val.w};
@@ -427,7 +481,8 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
           for (int e = 0; e < 8; ++e) {
             const int mm = m + e;
             if (mm >= g.M) break;
-            const int b = mm / g.L, pos = mm - b * g.L;
+            const int2 bp = seq_pos(mm, g.L, inv_l);
+            const int b = bp.x, pos = bp.y;
             g.vt[(((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos] = (f16_t)(wd[e >> 1] >> (16 * (e & 1)));
           }
         }
@@ -528,35 +583,37 @@ struct Plan {
   int bm, bn, split;
 };
 
-// Pick the tile and, for the residual GEMMs, a K split, by the number of rounds
-// of workgroups over the 256 compute units weighted by each tile's measured
-// per-CU throughput relative to the 128 x 256 tile (larger tiles move fewer
-// LDS bytes per flop and run two waves per SIMD).  The 192-wide tiles exist for
-// the widths where 256-wide tiles leave a quarter of the CUs idle (batch-1
-// q/k/v and gate/up); per k-step they are hardly faster than the 256-wide ones,
-// hence their lower per-flop speed.
+// Pick the tile and, for the residual GEMMs, a K split, by a time model:
+// rounds of workgroups over the 256 compute units x k-steps per workgroup x
+// the tile's k-step time (measured on random bf16 data at M = 512: larger
+// tiles move fewer LDS bytes per flop and run two waves per SIMD), plus, for
+// the residual GEMMs, the memory time of the float32 partials (written here,
+// read back by the reduction) or of the residual's read-modify-write, at the
+// ~8 TB/s they move at (measured: much of it stays in the last-level cache).  The 192-wide
+// tiles exist for the widths where 256-wide tiles leave CUs idle (batch-1
+// q/k/v and gate/up).
 Plan plan(int M, int N, int K, int epi) {
   struct Cand {
     int bm, bn;
-    double rel_speed;
+    double t_kstep_us;
   };
-  const Cand cands[] = {{128, 256, 1.0}, {256, 256, 1.3}, {256, 192, 1.08}, {128, 192, 0.95}};
+  const Cand cands[] = {{128, 256, 1.04}, {256, 256, 1.71}, {256, 192, 1.37}, {128, 192, 0.87}};
+  constexpr double BYTES_PER_US = 8.0e6;
   Plan best{0, 0, 0};
-  double best_cost = 1e30;
+  double best_t = 1e30;
+  const int ksteps = K / BK;
   for (const Cand& c : cands) {
     if (N % c.bn != 0) continue;
     const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
-    int split = 1;
-    if (epi == EPI_RESID) {
-      while (split < 8 && tiles * split * 2 <= 256 + 64 && (K / BK) % (split * 2) == 0 && (K / BK) / (split * 2) >= 4)
-        split *= 2;
-    }
-    const long wgs = tiles * split;
-    const double rounds = (double)((wgs + 255) / 256);
-    const double cost = rounds * (double)c.bm * c.bn / 256.0 / split / c.rel_speed;
-    if (cost < best_cost - 1e-9) {
-      best_cost = cost;
-      best = Plan{c.bm, c.bn, split};
+    for (int split = 1; split <= 8; split *= 2) {
+      if (split > 1 && (epi != EPI_RESID || ksteps % split != 0 || ksteps / split < 4)) break;
+      const long rounds = (tiles * split + 255) / 256;
+      double t = (double)rounds * (ksteps / split) * c.t_kstep_us;
+      if (epi == EPI_RESID) t += 8.0 * split * (double)M * N / BYTES_PER_US;
+      if (t < best_t - 1e-9) {
+        best_t = t;
+        best = Plan{c.bm, c.bn, split};
+      }
     }
   }
   if (best.bm == 0) throw HipError("gemm_bf16: N must be a multiple of 192 or 256");
@@ -598,6 +655,8 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   if (a.K % BK != 0) throw HipError("gemm_bf16: K % 64 must be 0");
   if (a.epi == EPI_QKV_ROPE && (a.n0 % 128 != 0 || a.n1 % 128 != 0))
     throw HipError("gemm_bf16: q and k/v regions must be whole 128-row heads");
+  if (a.epi == EPI_QKV_ROPE && (a.M >= (1 << 24) || a.B >= (1 << 16)))
+    throw HipError("gemm_bf16: q/k/v epilogue needs B * L < 2^24 and B < 2^16");
   const Plan p = plan(a.M, a.N, a.K, a.epi);
   switch (a.epi) {
     case EPI_QKV_ROPE: launch_epi<EPI_QKV_ROPE>(a, p, s); break;
