@@ -60,7 +60,7 @@ namespace {
 struct Layout {
   size_t h, a_attn, q, k, vt, attn, a_mlp, u, hb, cosb, sinb;
   size_t raw, gate, up, logits;                  // fp32 path
-  size_t part_m, part_s, part_i, ticket;         // bf16 head
+  size_t part_m, part_s, part_i, ticket, hbf;    // bf16 head
   size_t splitk;                                 // bf16 split-K GEMM partials
   size_t conf, argmax, all_done;                 // step scratch
   size_t total;
@@ -99,6 +99,7 @@ Layout make_layout(const dllm_model_cfg& c, int B, int L, int rows) {
     o.part_s = take(tiles * R * 4);
     o.part_i = take(tiles * R * 4);
     o.ticket = take(4);
+    o.hbf = take((size_t)HEAD_FRAG_ROWS * d * 2);
     const int qkv_n = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
     const size_t sk = std::max(std::max(gemm_bf16_splitk_bytes((int)M, qkv_n, c.d_model, EPI_QKV_ROPE),
                                         gemm_bf16_splitk_bytes((int)M, c.d_model, c.n_heads * c.head_dim, EPI_RESID)),
@@ -329,10 +330,17 @@ void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf
   const auto& c = m->cfg;
   const int nl = c.n_layers;
   const int R = B * rows;
+  // bf16: up to HEAD_FRAG_ROWS head rows also go to an MFMA-operand-order copy
+  // for the streaming head kernel
+  bf16_t* hbf = c.dtype == DLLM_BF16 && R <= HEAD_FRAG_ROWS ? at<bf16_t>(ws, lay.hbf) : nullptr;
   {
     ProfScope p(m, PK_NORM, s);
-    launch_rmsnorm(at<float>(ws, lay.h), W(m, 1 + 9 * nl), at<void>(ws, lay.hb), c.dtype, B, rows, L, row0,
-                   c.d_model, c.rms_eps, s);
+    if (c.dtype == DLLM_BF16)
+      launch_rmsnorm_head(at<float>(ws, lay.h), static_cast<const bf16_t*>(W(m, 1 + 9 * nl)), at<bf16_t>(ws, lay.hb),
+                          hbf, B, rows, L, row0, c.d_model, c.rms_eps, s);
+    else
+      launch_rmsnorm(at<float>(ws, lay.h), W(m, 1 + 9 * nl), at<void>(ws, lay.hb), c.dtype, B, rows, L, row0,
+                     c.d_model, c.rms_eps, s);
   }
   ProfScope p(m, PK_HEAD, s);
   if (c.dtype == DLLM_F32) {
@@ -342,6 +350,7 @@ void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf
   } else {
     HeadArgs a{};
     a.hb = at<bf16_t>(ws, lay.hb);
+    a.hbf = hbf;
     a.W = m->head_tiled;
     a.R = R;
     a.V = c.vocab;

@@ -7,28 +7,34 @@
 // The logits never leave registers (unless a debug buffer is given); the kernel
 // is bound by streaming W (V x d bf16) from HBM once.
 //
-// W is read from a tiled copy made once per model: for vocabulary tile t of
-// HEAD_TILE rows and k-block kb of 64, the [HEAD_TILE, 64] block is stored
-// contiguously, blocks in (t, kb) order.  A ring slice (VT rows x 64 k) is then
-// one contiguous 16-32 KB run of HBM: streaming 128-byte pieces of hundreds of
-// rows 8 KB apart instead reaches only about 70% of the contiguous rate.
+// W is read from a tiled copy made once per model, in MFMA fragment order: for
+// vocabulary tile t of HEAD_TILE rows and k-block kb of 64, the [HEAD_TILE, 64]
+// block is stored contiguously (blocks in (t, kb) order), and inside it each
+// 32-row x 16-k operand of v_mfma_f32_32x32x16_bf16 is one 1 KiB run in lane
+// order (group of 32 rows g, then k-slice s, then lane l = row % 32 + 32 *
+// (8-column half), 16 bytes per lane).  A (tile, 64-k) slice is then one
+// contiguous run of HBM, and a wave's A operand is one 1 KiB load.
 //
-// Persistent grid: G workgroups (one or two per CU) walk vocabulary tiles of
-// VT = 32 NW rows (NW waves), tile = blockIdx.x + i*G.  The tiles' (tile,
-// k-step of 64) slices stream through an S-stage LDS ring filled by
-// buffer_load_dwordx4 ... lds (whole 128-byte lines per eight lanes),
-// continuing across tile boundaries, so S-1 slices are always in flight; the
-// ring depth and tile height are chosen per head-row count so that W is most of
-// each slice (the hb rows ride along) and the ring fills the CU's LDS.  Wave w
-// owns 32 vocabulary rows of the tile and every head row (groups of 32):
-// A = W rows, B = hb rows of the MFMA, so a lane ends up with 16 vocabulary
-// entries of one head row.  Per tile those are merged across the lane pair and
-// the waves into a per-row running
-// (max, sum, argmax) that thread r keeps in registers over all of the
-// workgroup's tiles.  At the end each workgroup publishes one partial per row
-// (device-coherent sc1 stores, no cache flush); the last workgroup to finish
-// (atomic ticket) merges the G partials in workgroup order, so the result is
-// independent of scheduling, writes conf / argmax and re-arms the ticket.
+// Two kernels share that layout and the final merge:
+//  * head_stream_kernel (up to 32 head rows): every wave streams the 1 KiB
+//    operands of its own 32 vocabulary rows straight into registers, P slices
+//    in flight, with no LDS ring and no barrier in the loop; the head rows'
+//    operands come from the (cache-resident) hb rows alongside.
+//  * head_bf16_kernel (more head rows): the tiles' (tile, k-step of 64)
+//    slices stream through an S-stage LDS ring filled by buffer_load_dwordx4
+//    ... lds, continuing across tile boundaries, so S-1 slices are always in
+//    flight; the ring depth and tile height are chosen per head-row count so
+//    that W is most of each slice (the hb rows ride along, row-major and
+//    swizzled) and the ring fills the CU's LDS.
+// In both, persistent workgroups walk vocabulary tiles (tile = blockIdx.x +
+// i*G); wave w owns 32 vocabulary rows of the tile and every head row (groups
+// of 32): A = W rows, B = hb rows of the MFMA, so a lane ends up with 16
+// vocabulary entries of one head row.  Per tile those are merged across the
+// lane pair into per-row running (max, sum, argmax) statistics.  At the end
+// each workgroup publishes one partial per row (device-coherent sc1 stores,
+// no cache flush); the last workgroup to finish (atomic ticket) merges the G
+// partials in workgroup order, so the result is independent of scheduling,
+// writes conf / argmax and re-arms the ticket.
 #include "kernels.h"
 
 namespace dllm {
@@ -39,6 +45,7 @@ constexpr int BK = 64;
 constexpr int MAX_WG = 512;  // partial slots per row in the workspace
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr int CPOL_SC1 = 16;  // cache-policy bit: coherent at device (agent) scope
+constexpr int CPOL_NT = 2;    // cache-policy bit: non-temporal (W is streamed once)
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -78,10 +85,104 @@ __device__ __forceinline__ void barrier_nofence_h() {
 // all 64 banks (two rows per 256-byte bank line, eight slots each).
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4); }
 
+// Bytes of the tiled copy (head_bf16_packed_bytes), device side.
+__device__ __forceinline__ size_t head_bf16_packed_bytes_dev(int V, int d) {
+  return (size_t)((V + HEAD_TILE - 1) / HEAD_TILE) * HEAD_TILE * (size_t)d * 2;
+}
+
+// Statistics of one 32-row vocabulary group for head row `row` from the MFMA
+// result (lane holds vocabulary entries v0 + 8 (r/4) + 4 half + r%4, r < 16),
+// merged across the lane pair: valid in the half == 0 lane.  Writes the logits
+// too when a debug buffer is given.
+__device__ __forceinline__ Stat tile_stat(const HeadArgs& a, const f32x16_t& acc, int row, int v0, int half) {
+  Stat st{-INFINITY, 0.f, 0x7fffffff};
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int v = v0 + 8 * (r >> 2) + 4 * half + (r & 3);
+    const float x = acc[r];
+    if (a.logits && row < a.R && v < a.V) a.logits[(size_t)row * a.V + v] = x;
+    if (v < a.V && v != a.mask_id && x > st.m) {
+      st.m = x;
+      st.i = v;
+    }
+  }
+  float s = 0.f;
+  if (st.m != -INFINITY) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int v = v0 + 8 * (r >> 2) + 4 * half + (r & 3);
+      if (v < a.V && v != a.mask_id) s += exp2f((acc[r] - st.m) * LOG2E);
+    }
+  }
+  st.s = s;
+  Stat other;
+  other.m = __shfl_xor(st.m, 32, 64);
+  other.s = __shfl_xor(st.s, 32, 64);
+  other.i = __shfl_xor(st.i, 32, 64);
+  return half == 0 ? merge(st, other) : merge(other, st);
+}
+
+// Thread tid < R holds this workgroup's statistics of head row tid.  Publishes
+// them (one partial per (workgroup, row), device-coherent sc1 stores), takes a
+// ticket, and the last workgroup merges the G partials of every row in
+// workgroup order and writes conf / argmax.  fin: NT Stats of idle LDS.
+template <int NT>
+__device__ __forceinline__ void publish_and_merge(const HeadArgs& a, const Stat& run, int tid, Stat* fin,
+                                                  int& last_flag) {
+  const int G = gridDim.x;
+  const __amdgpu_buffer_rsrc_t rm = __builtin_amdgcn_make_buffer_rsrc((void*)a.part_m, 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)a.part_s, 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ri = __builtin_amdgcn_make_buffer_rsrc((void*)a.part_i, 0, 0x7fffffff, 0x00020000);
+  if (tid < a.R) {
+    const uint32_t off = (uint32_t)(((size_t)blockIdx.x * a.R + tid) * 4);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(run.m), rm, off, 0, CPOL_SC1);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(run.s), rs, off, 0, CPOL_SC1);
+    __builtin_amdgcn_raw_buffer_store_b32((uint32_t)run.i, ri, off, 0, CPOL_SC1);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) last_flag = atomicAdd(a.ticket, 1) == G - 1;
+  __syncthreads();
+  if (!last_flag) return;
+
+  // last workgroup: TPR threads per row merge strided runs of the G partials,
+  // then the runs are combined in order; both orders are fixed.  The loads of
+  // a run are issued 16 at a time so their latencies overlap.
+  constexpr int TPR_MAX = 8, LB = 16;
+  const int tpr = a.R <= NT / TPR_MAX ? TPR_MAX : (a.R <= NT / 4 ? 4 : (a.R <= NT / 2 ? 2 : 1));
+  const int row = tid / tpr, sub = tid % tpr;
+  Stat st{-INFINITY, 0.f, 0x7fffffff};
+  if (row < a.R) {
+    for (int g0 = sub; g0 < G; g0 += LB * tpr) {
+      Stat p[LB];
+#pragma unroll
+      for (int j = 0; j < LB; ++j) {
+        const int gwg = min(g0 + j * tpr, G - 1);
+        const uint32_t off = (uint32_t)(((size_t)gwg * a.R + row) * 4);
+        p[j].m = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rm, off, 0, CPOL_SC1));
+        p[j].s = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, CPOL_SC1));
+        p[j].i = (int)__builtin_amdgcn_raw_buffer_load_b32(ri, off, 0, CPOL_SC1);
+      }
+#pragma unroll
+      for (int j = 0; j < LB; ++j)
+        if (g0 + j * tpr < G) st = merge(st, p[j]);
+    }
+  }
+  fin[tid] = st;
+  __syncthreads();
+  if (row < a.R && sub == 0) {
+    Stat t = fin[tid];
+    for (int j = 1; j < tpr; ++j) t = merge(t, fin[tid + j]);
+    a.conf[row] = 1.0f / t.s;
+    a.argmax[row] = t.i;
+  }
+  if (tid == 0) *a.ticket = 0;
+}
+
 template <int RG, int VT, int NW, int S>
 __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  static_assert(VT == 32 * NW && S >= 3 && HEAD_TILE % VT == 0, "tile shape");
+  static_assert(VT == 32 * NW && S >= 3 && HEAD_TILE % VT == 0 && VT / 8 / NW == 4, "tile shape");
   constexpr int NT = 64 * NW;
   constexpr int HR = 32 * RG;                           // head rows covered
   constexpr int STAGE = (VT + HR) * 128;                // W slice + hb slice
@@ -100,9 +201,11 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
   const int my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / G + 1 : 0;
   const int units = my_tiles * nk;
 
-  // DMA sources: instruction i of wave w fills rows 8 (NW i + w) .. +7 of the
-  // slice; lane l loads row + l/8, logical chunk (l%8) ^ ((row >> 1) & 7) into
-  // slot l%8 (NW even: row >> 1 = 4 (w & 1) + (l/8) / 2 modulo 8 for every i).
+  // DMA sources: W instruction i of wave w copies the 1 KiB operand block
+  // j = NW i + w of the slice (group j / 4, k-slice j % 4) to LDS offset j KiB.
+  // hb instruction i of wave w fills rows 8 (NW i + w) .. +7 of the hb part;
+  // lane l loads row + l/8, logical chunk (l%8) ^ ((row >> 1) & 7) into slot
+  // l%8 (NW even: row >> 1 = 4 (w & 1) + (l/8) / 2 modulo 8 for every i).
   const int dr = lane >> 3, dc = (lane & 7) ^ (((wave & 1) << 2) | (dr >> 1));
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc((void*)a.hb, 0, 0x7fffffff, 0x00020000);
@@ -117,10 +220,11 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
     char* base = lds + (u % S) * STAGE;
 #pragma unroll
     for (int i = 0; i < IW; ++i) {
-      const int lt = tile / (HEAD_TILE / VT), r0 = (tile % (HEAD_TILE / VT)) * VT;
-      const int row = r0 + 8 * (NW * i + wave) + dr;  // row within the layout tile
-      const uint32_t vo = (uint32_t)((((size_t)lt * nk + kk) * HEAD_TILE + row) * 128 + dc * 16);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(base + 8 * (NW * i + wave) * 128), 16, vo, 0, 0, 0);
+      const int lt = tile / (HEAD_TILE / VT), g0 = (tile % (HEAD_TILE / VT)) * (VT / 32);
+      const int j = NW * i + wave;
+      const uint32_t vo =
+          (uint32_t)((((size_t)lt * nk + kk) * HEAD_TILE * 128) + ((size_t)g0 * 4 + j) * 1024 + lane * 16);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(base + j * 1024), 16, vo, 0, 0, CPOL_NT);
     }
 #pragma unroll
     for (int i = 0; i < IH_HI; ++i)
@@ -157,7 +261,7 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int ch = ks * 2 + half;
-      const bf16x8_t wf = *reinterpret_cast<const bf16x8_t*>(base + swz(wave * 32 + lr, ch));
+      const bf16x8_t wf = *reinterpret_cast<const bf16x8_t*>(base + ((4 * wave + ks) * 64 + lane) * 16);
 #pragma unroll
       for (int gi = 0; gi < RG; ++gi) {
         const bf16x8_t hf = *reinterpret_cast<const bf16x8_t*>(base + VT * 128 + swz(gi * 32 + lr, ch));
@@ -171,34 +275,12 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
     const int v0 = tile * VT + wave * 32;
 #pragma unroll
     for (int gi = 0; gi < RG; ++gi) {
-      const int row = gi * 32 + lr;
-      Stat st{-INFINITY, 0.f, 0x7fffffff};
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = v0 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float x = acc[gi][r];
-        if (a.logits && row < a.R && v < a.V) a.logits[(size_t)row * a.V + v] = x;
-        if (v < a.V && v != a.mask_id && x > st.m) {
-          st.m = x;
-          st.i = v;
-        }
-      }
-      float s = 0.f;
-      if (st.m != -INFINITY) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = v0 + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (v < a.V && v != a.mask_id) s += exp2f((acc[gi][r] - st.m) * LOG2E);
-        }
-      }
-      st.s = s;
-      Stat other;
-      other.m = __shfl_xor(st.m, 32, 64);
-      other.s = __shfl_xor(st.s, 32, 64);
-      other.i = __shfl_xor(st.i, 32, 64);
-      st = half == 0 ? merge(st, other) : merge(other, st);
-      if (half == 0) wst[wave][row] = st;
+      const Stat st = tile_stat(a, acc[gi], gi * 32 + lr, v0, half);
+      if (half == 0) wst[wave][gi * 32 + lr] = st;
     }
+    // debug logits stores count in vmcnt too: drain them so the ring's counts
+    // keep describing its loads only
+    if (a.logits) wait_vm_lds<0>();
     // LDS barrier that leaves the ring's DMA in flight (__syncthreads would
     // wait for it); wst is next written after the following unit's barrier
     wait_vm_lds<63>();
@@ -211,55 +293,104 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
     }
   }
 
-  // ---- publish this workgroup's partial per row, then the last one merges
-  const __amdgpu_buffer_rsrc_t rm = __builtin_amdgcn_make_buffer_rsrc((void*)a.part_m, 0, 0x7fffffff, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)a.part_s, 0, 0x7fffffff, 0x00020000);
-  const __amdgpu_buffer_rsrc_t ri = __builtin_amdgcn_make_buffer_rsrc((void*)a.part_i, 0, 0x7fffffff, 0x00020000);
-  if (tid < a.R) {
-    const uint32_t off = (uint32_t)(((size_t)blockIdx.x * a.R + tid) * 4);
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(run.m), rm, off, 0, CPOL_SC1);
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(run.s), rs, off, 0, CPOL_SC1);
-    __builtin_amdgcn_raw_buffer_store_b32((uint32_t)run.i, ri, off, 0, CPOL_SC1);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (tid == 0) last_flag = atomicAdd(a.ticket, 1) == G - 1;
-  __syncthreads();
-  if (!last_flag) return;
+  publish_and_merge<NT>(a, run, tid, reinterpret_cast<Stat*>(lds), last_flag);
+#endif
+}
 
-  // last workgroup: TPR threads per row merge strided runs of the G partials,
-  // then the runs are combined in order; both orders are fixed.  The loads of
-  // a run are issued 16 at a time so their latencies overlap.
-  constexpr int TPR_MAX = 8, LB = 16;
-  const int tpr = a.R <= NT / TPR_MAX ? TPR_MAX : (a.R <= NT / 4 ? 4 : (a.R <= NT / 2 ? 2 : 1));
-  Stat* fin = reinterpret_cast<Stat*>(lds);  // the ring is idle now
-  const int row = tid / tpr, sub = tid % tpr;
-  Stat st{-INFINITY, 0.f, 0x7fffffff};
-  if (row < a.R) {
-    for (int g0 = sub; g0 < G; g0 += LB * tpr) {
-      Stat p[LB];
+// Streaming kernel for up to 32 head rows: NW = 4 waves per workgroup, one
+// per SIMD; a workgroup tile is 32 GW NW vocabulary rows and wave w owns its GW
+// groups w GW .. w GW + GW - 1 of 32 rows.  The wave walks the tiles' 16-k
+// slices in order; per slice it loads the GW 1 KiB W operands and the 1 KiB hb
+// operand (the operand-order copy) into a P-deep register ring, so one hb load
+// serves GW MFMAs.  Loads complete in issue order, so before slice u only the
+// (GW + 1) (P - 1) loads of the slices after it may be outstanding.  W reads
+// past the tiled copy (a last tile that extends beyond it) return zeros
+// through the buffer bound.
+template <int GW, int P>
+__global__ void __launch_bounds__(256, 1) head_stream_kernel(HeadArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int NW = 4, NT = 64 * NW, TROWS = 32 * GW * NW;
+  static_assert(HEAD_TILE % (32 * GW) == 0 && (GW + 1) * (P - 1) < 64, "tile shape");
+  __shared__ Stat wst[NW][32];
+  __shared__ Stat fin[NT];
+  __shared__ int last_flag;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 31, half = lane >> 5;
+  const int G = gridDim.x;
+  const int ntiles = (a.V + TROWS - 1) / TROWS;
+  const int nk = a.d / BK, ns = 4 * nk;
+  const int my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / G + 1 : 0;
+  const int units = my_tiles * ns;
+
+  const uint32_t wbytes = (uint32_t)head_bf16_packed_bytes_dev(a.V, a.d);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, 0, wbytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc((void*)a.hbf, 0, 0x7fffffff, 0x00020000);
+  // first vocabulary row of group j of this wave in tile t: t TROWS + (wave GW + j) 32;
+  // in the copy: layout tile r / HEAD_TILE, group (r % HEAD_TILE) / 32
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  u32x4_t wbuf[P][GW], hbuf[P];
+  auto load = [&](int u, int slot) {
+    const int t = blockIdx.x + (u / ns) * G, sl = u % ns;
 #pragma unroll
-      for (int j = 0; j < LB; ++j) {
-        const int gwg = min(g0 + j * tpr, G - 1);
-        const uint32_t off = (uint32_t)(((size_t)gwg * a.R + row) * 4);
-        p[j].m = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rm, off, 0, CPOL_SC1));
-        p[j].s = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, CPOL_SC1));
-        p[j].i = (int)__builtin_amdgcn_raw_buffer_load_b32(ri, off, 0, CPOL_SC1);
-      }
-#pragma unroll
-      for (int j = 0; j < LB; ++j)
-        if (g0 + j * tpr < G) st = merge(st, p[j]);
+    for (int j = 0; j < GW; ++j) {
+      const int r0 = t * TROWS + (wave * GW + j) * 32;
+      const int lt = r0 / HEAD_TILE, g8 = (r0 % HEAD_TILE) / 32;
+      const uint32_t wo =
+          (uint32_t)((((size_t)lt * nk + (sl >> 2)) * (HEAD_TILE / 32) + g8) * 4 + (sl & 3)) * 1024 + lane * 16;
+      wbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rw, wo, 0, CPOL_NT);
     }
+    hbuf[slot] = __builtin_amdgcn_raw_buffer_load_b128(rh, (uint32_t)(sl * 1024 + lane * 16), 0, 0);
+  };
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (p < units) load(p, p);
+
+  Stat run{-INFINITY, 0.f, 0x7fffffff};  // lane lr (half 0): running stats of head row lr
+  f32x16_t acc[GW];
+#pragma unroll
+  for (int j = 0; j < GW; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+  // ns is a multiple of P (the launcher checks d % (16 P) == 0), so slice u sits
+  // in ring slot u % P = p
+  for (int ti = 0; ti < my_tiles; ++ti) {
+    for (int s0 = 0; s0 < ns; s0 += P) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        const int u = ti * ns + s0 + p;
+        if (u + P - 1 < units)
+          wait_vm_lds<(GW + 1) * (P - 1)>();
+        else
+          wait_vm_lds<0>();  // the last slices: fewer later loads were issued
+#pragma unroll
+        for (int j = 0; j < GW; ++j)
+          acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wbuf[p][j]),
+                                                          __builtin_bit_cast(bf16x8_t, hbuf[p]), acc[j], 0, 0, 0);
+        if (u + P < units) load(u + P, p);
+      }
+    }
+    // end of a tile: this wave's vocabulary rows are complete
+    const int t = blockIdx.x + ti * G;
+#pragma unroll
+    for (int j = 0; j < GW; ++j) {
+      const Stat st = tile_stat(a, acc[j], lr, t * TROWS + (wave * GW + j) * 32, half);
+      run = merge(run, st);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+    }
+    // debug logits stores count in vmcnt too: drain them so the counts above
+    // keep describing loads only
+    if (a.logits) wait_vm_lds<0>();
   }
-  fin[tid] = st;
+  if (half == 0) wst[wave][lr] = run;
   __syncthreads();
-  if (row < a.R && sub == 0) {
-    Stat t = fin[tid];
-    for (int j = 1; j < tpr; ++j) t = merge(t, fin[tid + j]);
-    a.conf[row] = 1.0f / t.s;
-    a.argmax[row] = t.i;
+  Stat wg{-INFINITY, 0.f, 0x7fffffff};
+  if (tid < a.R) {
+    wg = wst[0][tid];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) wg = merge(wg, wst[w][tid]);
   }
-  if (tid == 0) *a.ticket = 0;
+  publish_and_merge<NT>(a, wg, tid, fin, last_flag);
 #endif
 }
 
@@ -267,15 +398,19 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
 __global__ void pack_head_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wt, int V, int d, size_t nvec) {
   const int nk = d / 64;
   for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < nvec; idx += (size_t)gridDim.x * blockDim.x) {
-    const int c8 = (int)(idx % 8);
-    size_t t = idx / 8;
-    const int r = (int)(t % HEAD_TILE);
-    t /= HEAD_TILE;
+    // destination vector idx = ((lt * nk + kb) * 8 + g) * 4 + s) * 64 + l
+    const int l = (int)(idx % 64);
+    size_t t = idx / 64;
+    const int sl = (int)(t % 4);
+    t /= 4;
+    const int g = (int)(t % (HEAD_TILE / 32));
+    t /= HEAD_TILE / 32;
     const int kb = (int)(t % nk);
     const size_t lt = t / nk;
-    const size_t row = lt * HEAD_TILE + r;
+    const size_t row = lt * HEAD_TILE + g * 32 + (l & 31);
+    const int k = kb * 64 + sl * 16 + (l >> 5) * 8;
     bf16x8_t v = {};
-    if (row < (size_t)V) v = *reinterpret_cast<const bf16x8_t*>(W + row * d + kb * 64 + c8 * 8);
+    if (row < (size_t)V) v = *reinterpret_cast<const bf16x8_t*>(W + row * d + k);
     *reinterpret_cast<bf16x8_t*>(Wt + idx * 8) = v;
   }
 }
@@ -328,7 +463,30 @@ void launch_head_bf16(const HeadArgs& a, hipStream_t s) {
   // (head-row groups, vocab tile, waves, ring stages).  Eight waves per CU
   // stream faster than four whatever the ring depth, so 256-row tiles are kept
   // even where the tile count divides unevenly over the CUs.
-  if (rg <= 1) HeadCfg<1, 256, 8, 4>::launch(a, s);
+  if (a.R <= HEAD_FRAG_ROWS && a.hbf && a.d % 256 == 0) {
+    // streaming kernel, one workgroup per CU: the tile height (128, 256 or 512
+    // rows: GW = 1, 2, 4 groups per wave) that minimises the largest number of
+    // rows a CU streams, weighted by the hb loads per W load (1 / GW; measured:
+    // one per W load costs ~25% of the streaming rate); taller on ties
+    const int cus = std::min(device_cu_count(), MAX_WG);
+    int best_gw = 4;
+    double best = 1e30;
+    for (int gw = 4; gw >= 1; gw /= 2) {
+      const long tiles = (a.V + 128L * gw - 1) / (128L * gw);
+      const double t = (double)((tiles + cus - 1) / cus) * gw * (1.0 + 0.25 / gw);
+      if (t < best - 1e-9) {
+        best = t;
+        best_gw = gw;
+      }
+    }
+    const int grid = (int)std::min<long>((a.V + 128L * best_gw - 1) / (128L * best_gw), cus);
+    if (best_gw == 4)
+      hipLaunchKernelGGL((head_stream_kernel<4, 8>), dim3(grid), dim3(256), 0, s, a);
+    else if (best_gw == 2)
+      hipLaunchKernelGGL((head_stream_kernel<2, 16>), dim3(grid), dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((head_stream_kernel<1, 16>), dim3(grid), dim3(256), 0, s, a);
+  } else if (rg <= 1) HeadCfg<1, 256, 8, 4>::launch(a, s);
   else if (rg <= 2) HeadCfg<2, 256, 8, 3>::launch(a, s);
   else if (rg <= 4) HeadCfg<4, 128, 4, 3>::launch(a, s);
   else HeadCfg<8, 128, 4, 3>::launch(a, s);

@@ -243,6 +243,64 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
   DLLM_LAUNCH_CHECK("resid_rmsnorm");
 }
 
+// rmsnorm_vec_kernel for the bf16 head rows, also writing the rows in MFMA
+// B-operand order (row r < 32, columns 4c .. 4c+3 are eight contiguous bytes:
+// slice c / 4, lane r + 32 ((c / 2) % 2), elements 4 (c % 2) ..).
+template <int NV>
+__global__ void __launch_bounds__(256) rmsnorm_head_kernel(const float* __restrict__ h, const bf16_t* __restrict__ g,
+                                                           bf16_t* __restrict__ out, bf16_t* __restrict__ outf,
+                                                           int rows, int L, int row0, int d, float eps) {
+  const int r = blockIdx.x;
+  const int b = r / rows, i = r % rows;
+  const float* src = h + ((size_t)b * L + row0 + i) * d;
+  const int d4 = d / 4;
+  float4 v[NV];
+  double ss = 0.0;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int c = threadIdx.x + 256 * j;
+    if (c < d4) {
+      v[j] = Vec4<float>::load(src, c);
+      ss += (double)v[j].x * v[j].x + (double)v[j].y * v[j].y + (double)v[j].z * v[j].z + (double)v[j].w * v[j].w;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  __shared__ double part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const double tot = (part[0] + part[1]) + (part[2] + part[3]);
+  const float rstd = (float)(1.0 / sqrt(tot / (double)d + (double)eps));
+  bf16_t* dst = out + (size_t)r * d;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int c = threadIdx.x + 256 * j;
+    if (c < d4) {
+      const float4 gg = Vec4<bf16_t>::load(g, c);
+      const float4 y = make_float4(v[j].x * rstd * gg.x, v[j].y * rstd * gg.y, v[j].z * rstd * gg.z,
+                                   v[j].w * rstd * gg.w);
+      Vec4<bf16_t>::store(dst, c, y);
+      if (outf) Vec4<bf16_t>::store(outf, ((size_t)(c >> 2) * 64 + r + 32 * ((c >> 1) & 1)) * 2 + (c & 1), y);
+    }
+  }
+}
+
+void launch_rmsnorm_head(const float* h, const bf16_t* g, bf16_t* out, bf16_t* outf, int B, int rows, int L,
+                         int row0, int d, float eps, hipStream_t s) {
+  if (B * rows == 0) return;
+  if (d % 4 != 0 || d > 8192 || ((uintptr_t)h | (uintptr_t)g | (uintptr_t)out | (uintptr_t)outf) % 16 != 0)
+    throw HipError("rmsnorm_head: needs d % 4 == 0, d <= 8192 and 16-byte aligned rows");
+  if (outf && B * rows > HEAD_FRAG_ROWS) throw HipError("rmsnorm_head: operand-order copy holds 32 rows");
+  const int nv = ceil_div(d, 1024);
+  if (nv <= 2)
+    hipLaunchKernelGGL(rmsnorm_head_kernel<2>, dim3(B * rows), dim3(256), 0, s, h, g, out, outf, rows, L, row0, d, eps);
+  else if (nv <= 4)
+    hipLaunchKernelGGL(rmsnorm_head_kernel<4>, dim3(B * rows), dim3(256), 0, s, h, g, out, outf, rows, L, row0, d, eps);
+  else
+    hipLaunchKernelGGL(rmsnorm_head_kernel<8>, dim3(B * rows), dim3(256), 0, s, h, g, out, outf, rows, L, row0, d, eps);
+  DLLM_LAUNCH_CHECK("rmsnorm_head");
+}
+
 void launch_rmsnorm(const float* h, const void* g, void* out, int dtype, int B, int rows, int L, int row0, int d,
                     float eps, hipStream_t s) {
   if (B * rows == 0) return;

@@ -76,13 +76,25 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
                       int Hkv, hipStream_t s);
 
 // The bf16 LM head is read from a tiled copy: vocabulary tiles of HEAD_TILE rows,
-// each stored as d/64 consecutive [HEAD_TILE, 64] blocks, rows past V zero.
+// each stored as d/64 consecutive [HEAD_TILE, 64] blocks, rows past V zero;
+// inside a block, each 32-row x 16-k MFMA A operand is 1 KiB in lane order.
 constexpr int HEAD_TILE = 256;
+// Head-row counts up to HEAD_FRAG_ROWS use the streaming LM-head kernel, which
+// reads the normed rows from a copy in MFMA B-operand order: for 16-k slice s,
+// lane l = row + 32 * ((k / 8) % 2) holds bf16 k = 16 s + 8 (l / 32) .. +7
+// (rows >= R unused), 1 KiB per slice.
+constexpr int HEAD_FRAG_ROWS = 32;
+// Final RMSNorm of the head rows (bf16 model, d % 4 == 0, d <= 8192): out[B*rows,
+// d] row-major as launch_rmsnorm, and, when outf is non-null (B * rows <=
+// HEAD_FRAG_ROWS), the same values in the operand order above.
+void launch_rmsnorm_head(const float* h, const bf16_t* g, bf16_t* out, bf16_t* outf, int B, int rows, int L,
+                         int row0, int d, float eps, hipStream_t s);
 size_t head_bf16_packed_bytes(int V, int d);
 void launch_pack_head_bf16(const bf16_t* W, bf16_t* Wt, int V, int d, hipStream_t s);
 
 struct HeadArgs {
   const bf16_t* hb;   // [R, d]
+  const bf16_t* hbf;  // R <= HEAD_FRAG_ROWS: the same rows in MFMA operand order (launch_rmsnorm_head)
   const bf16_t* W;    // tiled copy of the [V, d] LM head (launch_pack_head_bf16)
   int R, V, d, mask_id;
   float* conf; int32_t* argmax; float* logits;  // logits optional

@@ -120,7 +120,10 @@ def _head_model(V, d, mask_id_at_top=True):
     return cfg
 
 
-@pytest.mark.parametrize("Bn,rows,V", [(1, 32, 4096), (2, 32, 4000), (8, 32, 4096), (3, 20, 2176)])
+# up to 32 head rows use the streaming kernel (R = 32, 20: ragged vocabulary
+# tiles); more use the LDS-ring kernel (R = 64, 60, 256)
+@pytest.mark.parametrize("Bn,rows,V", [(1, 32, 4096), (1, 32, 4000), (1, 20, 2176), (2, 32, 4000), (8, 32, 4096),
+                                       (3, 20, 2176)])
 def test_head_exact_logit_fixture(Bn, rows, V):
     """Hidden rows of +-1 (RMSNorm is then the identity) and integer weights make
     every logit an exact small integer in float32, so the argmax (with ties going
