@@ -70,10 +70,17 @@ __device__ __forceinline__ int2 vrow(const GemmArgs& g, int n) {
 // all 64 banks (two rows per 256-byte bank line, eight slots each).
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4); }
 
-template <int BM_, int BN_, int WAVES_M, int WAVES_N, int STAGES_>
+// KG = 2 splits every k-step between two groups of waves that own the same
+// output blocks (group g takes the k-slices 2g, 2g + 1 of each 64-wide step):
+// a tile that four waves would cover then runs two waves per SIMD, so one
+// wave's LDS reads overlap the other's MFMAs, at the LDS bytes per flop of the
+// four-wave tile.  The second group's accumulators are added to the first's
+// through LDS after the main loop.
+template <int BM_, int BN_, int WAVES_M, int WAVES_N, int STAGES_, int KG_ = 1>
 struct Tile {
-  static constexpr int BM = BM_, BN = BN_, S = STAGES_;
-  static constexpr int NW = WAVES_M * WAVES_N, NTH = 64 * NW;
+  static constexpr int BM = BM_, BN = BN_, S = STAGES_, KG = KG_;
+  static constexpr int NWT = WAVES_M * WAVES_N;             // waves per k-group (one output block each)
+  static constexpr int NW = NWT * KG, NTH = 64 * NW;
   static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   static constexpr int TI = WM / 32, TJ = WN / 32;          // MFMA tiles per wave
   static constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;   // LDS-DMA instructions per wave per stage
@@ -81,6 +88,7 @@ struct Tile {
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tiles are whole 32 x 32 MFMA blocks");
   static_assert(IA * NW * 8 == BM && IB * NW * 8 == BN, "tile rows must split evenly over the DMA loads");
   static_assert(NW % 2 == 0, "the DMA swizzle assumes an even wave count");
+  static_assert(KG == 1 || KG == 2, "one or two k-groups");
 };
 // 128 x 256, 4 waves of 64 x 128, three stages (small M: more tiles to spread over 256 CUs)
 using TileS = Tile<128, 256, 2, 2, 3>;
@@ -90,6 +98,8 @@ using TileL = Tile<256, 256, 4, 2, 2>;
 using TileM = Tile<256, 192, 4, 2, 2>;
 // 128 x 192, 4 waves of 64 x 96, three stages
 using TileSM = Tile<128, 192, 2, 2, 3>;
+// the same on 8 waves in two k-groups
+using TileSM2 = Tile<128, 192, 2, 2, 3, 2>;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -138,7 +148,8 @@ template <class TL, int EPI>
 __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave, int lane, int m0, int n0, int kt0,
                                          int nk, f32x16_t (&acc)[TL::TI][TL::TJ]) {
   constexpr int BM = TL::BM, BN = TL::BN, S = TL::S, NW = TL::NW;
-  const int wm = wave / (BN / TL::WN), wn = wave % (BN / TL::WN);
+  const int wt = wave % TL::NWT, kg = wave / TL::NWT;
+  const int wm = wt / (BN / TL::WN), wn = wt % (BN / TL::WN);
   const int kbeg = kt0 * BK;
 
   // LDS-DMA loads: instruction i of wave w fills tile rows 8 (NW i + w) .. +7
@@ -181,18 +192,20 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
 
   constexpr int PER_STAGE = TL::IA + TL::IB;  // DMA instructions per wave per stage
   constexpr int NS = BK / 16, NF = TL::TI + TL::TJ, NM = TL::TI * TL::TJ;
-  static_assert(NM >= NF && NS % 2 == 0, "pipeline needs at least as many MFMAs as fragment reads per slice");
+  constexpr int NSW = NS / TL::KG;  // k-slices of a step that this wave's group computes
+  static_assert(NM >= NF && NSW % 2 == 0, "pipeline needs at least as many MFMAs as fragment reads per slice");
   const int lrow = lane & 31, lhalf = lane >> 5;
+  const int ks0 = kg * NSW;  // the group's first slice (even, so register sets alternate across steps)
 
-  // Fragments of the four 16-wide k-slices of a tile go through two register
-  // sets: slice ks + 1 is read while the MFMAs of slice ks run.  The barrier
-  // that publishes tile kt + 1 sits before the last slice of tile kt, so the
-  // first fragments of tile kt + 1 are read under that slice's MFMAs and the
-  // k-step boundary costs no exposed LDS latency; the slot tile kt occupied is
-  // refilled (tile kt + S) right after that barrier.
+  // Fragments of the group's 16-wide k-slices of a tile go through two
+  // register sets: slice kl + 1 is read while the MFMAs of slice kl run.  The
+  // barrier that publishes tile kt + 1 sits before the group's last slice of
+  // tile kt, so the first fragments of tile kt + 1 are read under that slice's
+  // MFMAs and the k-step boundary costs no exposed LDS latency; the slot tile
+  // kt occupied is refilled (tile kt + S) right after that barrier.
   bf16x8_t af[2][TL::TI], bfr[2][TL::TJ];
-  auto frag = [&](const char* base, int ks) {
-    const int ch = ks * 2 + lhalf, set = ks & 1;
+  auto frag = [&](const char* base, int kl) {
+    const int ch = (ks0 + kl) * 2 + lhalf, set = kl & 1;
 #pragma unroll
     for (int i = 0; i < TL::TI; ++i)
       af[set][i] = *reinterpret_cast<const bf16x8_t*>(base + swz(wm * TL::WM + i * 32 + lrow, ch));
@@ -217,9 +230,9 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
   for (int kt = 0; kt < nk; ++kt) {
     const char* base = lds + (kt % S) * TL::LDS_STAGE;
 #pragma unroll
-    for (int ks = 0; ks < NS; ++ks) {
+    for (int ks = 0; ks < NSW; ++ks) {
       bool next = false;
-      if (ks + 1 < NS) {
+      if (ks + 1 < NSW) {
         frag(base, ks + 1);
         next = true;
       } else if (kt + 1 < nk) {
@@ -261,7 +274,7 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
 template <class TL, int EPI>
 __device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, int m0, int n0, int i, int c,
                                          const float (&v)[TL::TJ][4]) {
-  const int wm = wave / (TL::BN / TL::WN), wn = wave % (TL::BN / TL::WN);
+  const int wm = (wave % TL::NWT) / (TL::BN / TL::WN), wn = (wave % TL::NWT) % (TL::BN / TL::WN);
   const int lhalf = lane >> 5, col_in = lane & 31;
   const int mrow = m0 + wm * TL::WM + i * 32 + 8 * c + 4 * lhalf;  // + e
   const int ncol0 = n0 + wn * TL::WN;                               // + j*32 + col_in
@@ -298,11 +311,19 @@ struct Stage {
   static constexpr int QKV_BYTES = TL::BN / 32 * BLK;
 };
 
+// k-group merge area: the second group's accumulators, [NWT][TI*TJ][4][64 lanes] float4
+template <class TL>
+constexpr size_t merge_bytes() {
+  return TL::KG == 1 ? 0 : (size_t)TL::NWT * TL::TI * TL::TJ * 4 * 64 * 16;
+}
+
 template <class TL, int EPI>
 constexpr size_t lds_bytes() {
   const size_t ring = (size_t)TL::S * TL::LDS_STAGE;
   const size_t st = EPI == EPI_SWIGLU ? Stage<TL>::SW_BYTES : EPI == EPI_QKV_ROPE ? Stage<TL>::QKV_BYTES : 0;
-  return ring > st ? ring : st;
+  const size_t mg = merge_bytes<TL>();
+  const size_t a = ring > st ? ring : st;
+  return a > mg ? a : mg;
 }
 
 // The value lane l ^ 16 holds (v_permlane16_swap: a VALU exchange of the odd
@@ -334,7 +355,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
                                                 const f32x16_t (&acc)[TL::TI][TL::TJ]) {
   using St = Stage<TL>;
   constexpr int HD = 128, HALF = 64;
-  const int wm = wave / (TL::BN / TL::WN), wn = wave % (TL::BN / TL::WN);
+  const int wm = (wave % TL::NWT) / (TL::BN / TL::WN), wn = (wave % TL::NWT) % (TL::BN / TL::WN);
   const int lhalf = lane >> 5, col_in = lane & 31, w = col_in & 15;
   // For SwiGLU and q/k the two operands of an output sit in lanes l and l ^ 16
   // (see vrow): after one exchange of two values the lane with column < 16
@@ -347,6 +368,9 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
   barrier_nofence();  // every wave is done reading the ring
 
   const float inv_l = 1.0f / (float)g.L;
+  // with two k-groups only the first holds the finished tile; the second
+  // joins the barriers and the stores
+  if (wave < TL::NWT) {
 #pragma unroll
   for (int i = 0; i < TL::TI; ++i) {
     // q/k: the RoPE table values of this lane's two finished rows in each of
@@ -426,6 +450,8 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
         }
       }
     }
+  }
+
   }
 
   __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
@@ -533,14 +559,54 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
   int lin = blockIdx.x;
   if ((tiles & 7) == 0) lin = (blockIdx.x & 7) * (tiles >> 3) + (blockIdx.x >> 3);
   const int2 o = tile_origin<TL>(g, lin);
-  const int nk = g.K / gridDim.z / BK;
+  // K slice z of S: k-steps [z KS / S, (z + 1) KS / S)
+  const int ks_total = g.K / BK;
+  const int kt0 = (int)((long)blockIdx.z * ks_total / gridDim.z);
+  const int nk = (int)((long)(blockIdx.z + 1) * ks_total / gridDim.z) - kt0;
 
   f32x16_t acc[TL::TI][TL::TJ];
   zero_acc<TL>(acc);
-  mma_tile<TL, EPI>(g, lds, wave, lane, o.x, o.y, blockIdx.z * nk, nk, acc);
+  mma_tile<TL, EPI>(g, lds, wave, lane, o.x, o.y, kt0, nk, acc);
+
+  if (TL::KG == 2) {
+    // acc(group 0) += acc(group 1) through LDS (the ring is idle once every
+    // wave has passed the barrier); lane-contiguous float4 rows
+    wait_vm_lds<0>();
+    barrier_nofence();
+    float4* xa = reinterpret_cast<float4*>(lds) + (size_t)(wave % TL::NWT) * (TL::TI * TL::TJ * 4 * 64) + lane;
+    if (wave >= TL::NWT) {
+#pragma unroll
+      for (int i = 0; i < TL::TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TL::TJ; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            xa[((i * TL::TJ + j) * 4 + q) * 64] =
+                make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+    }
+    wait_vm_lds<0>();
+    barrier_nofence();
+    if (wave < TL::NWT) {
+#pragma unroll
+      for (int i = 0; i < TL::TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TL::TJ; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float4 v = xa[((i * TL::TJ + j) * 4 + q) * 64];
+            acc[i][j][4 * q] += v.x;
+            acc[i][j][4 * q + 1] += v.y;
+            acc[i][j][4 * q + 2] += v.z;
+            acc[i][j][4 * q + 3] += v.w;
+          }
+    }
+    // the staged epilogues have barriers: every wave takes part; the others
+    // are done
+    if (wave >= TL::NWT && !(gridDim.z == 1 && (EPI == EPI_SWIGLU || EPI == EPI_QKV_ROPE))) return;
+  }
 
   if (gridDim.z > 1) {  // split-K partial tile
-    const int wm = wave / (TL::BN / TL::WN), wn = wave % (TL::BN / TL::WN);
+    const int wm = (wave % TL::NWT) / (TL::BN / TL::WN), wn = (wave % TL::NWT) % (TL::BN / TL::WN);
     const int lhalf = lane >> 5, col_in = lane & 31;
     float* part = g.splitk_buf + (size_t)blockIdx.z * g.M * g.N;
 #pragma unroll
@@ -580,10 +646,11 @@ __global__ void splitk_resid_kernel(const float* __restrict__ part, float* __res
 }
 
 struct Plan {
-  int bm, bn, split;
+  int bm, bn, kg, split;
 };
 
-// Pick the tile and, for the residual GEMMs, a K split, by a time model:
+// Pick the tile and, for the residual GEMMs, a K split (any count up to 8; the
+// k-steps are spread as evenly as they divide), by a time model:
 // rounds of workgroups over the 256 compute units x k-steps per workgroup x
 // the tile's k-step time (measured on random bf16 data at M = 512: larger
 // tiles move fewer LDS bytes per flop and run two waves per SIMD), plus, for
@@ -594,25 +661,26 @@ struct Plan {
 // q/k/v and gate/up).
 Plan plan(int M, int N, int K, int epi) {
   struct Cand {
-    int bm, bn;
+    int bm, bn, kg;
     double t_kstep_us;
   };
-  const Cand cands[] = {{128, 256, 1.04}, {256, 256, 1.71}, {256, 192, 1.37}, {128, 192, 0.87}};
+  const Cand cands[] = {{128, 256, 1, 1.04}, {256, 256, 1, 1.71}, {256, 192, 1, 1.37}, {128, 192, 1, 0.87},
+                        {128, 192, 2, 0.81}};
   constexpr double BYTES_PER_US = 8.0e6;
-  Plan best{0, 0, 0};
+  Plan best{0, 0, 0, 0};
   double best_t = 1e30;
   const int ksteps = K / BK;
   for (const Cand& c : cands) {
     if (N % c.bn != 0) continue;
     const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
-    for (int split = 1; split <= 8; split *= 2) {
-      if (split > 1 && (epi != EPI_RESID || ksteps % split != 0 || ksteps / split < 4)) break;
+    for (int split = 1; split <= 8; ++split) {
+      if (split > 1 && (epi != EPI_RESID || ksteps / split < 4)) break;
       const long rounds = (tiles * split + 255) / 256;
-      double t = (double)rounds * (ksteps / split) * c.t_kstep_us;
+      double t = (double)rounds * ((ksteps + split - 1) / split) * c.t_kstep_us;
       if (epi == EPI_RESID) t += 8.0 * split * (double)M * N / BYTES_PER_US;
       if (t < best_t - 1e-9) {
         best_t = t;
-        best = Plan{c.bm, c.bn, split};
+        best = Plan{c.bm, c.bn, c.kg, split};
       }
     }
   }
@@ -639,7 +707,7 @@ void launch_epi(const GemmArgs& g, const Plan& p, hipStream_t s) {
   else if (p.bn == 256)
     launch_tile<TileS, EPI>(g, p.split, s);
   else
-    launch_tile<TileSM, EPI>(g, p.split, s);
+    p.kg == 2 ? launch_tile<TileSM2, EPI>(g, p.split, s) : launch_tile<TileSM, EPI>(g, p.split, s);
 }
 
 }  // namespace
@@ -670,11 +738,18 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   } else if (p.split > 1) {
     const long MN = (long)a.M * a.N;
     const dim3 grid(ceil_div(MN / 4, 256));
+    auto go = [&](auto sc) {
+      hipLaunchKernelGGL(splitk_resid_kernel<decltype(sc)::value>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN);
+    };
     switch (p.split) {
-      case 2: hipLaunchKernelGGL(splitk_resid_kernel<2>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN); break;
-      case 4: hipLaunchKernelGGL(splitk_resid_kernel<4>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN); break;
-      case 8: hipLaunchKernelGGL(splitk_resid_kernel<8>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN); break;
-      default: throw HipError("splitk_resid: split must be 2, 4 or 8");
+      case 2: go(std::integral_constant<int, 2>{}); break;
+      case 3: go(std::integral_constant<int, 3>{}); break;
+      case 4: go(std::integral_constant<int, 4>{}); break;
+      case 5: go(std::integral_constant<int, 5>{}); break;
+      case 6: go(std::integral_constant<int, 6>{}); break;
+      case 7: go(std::integral_constant<int, 7>{}); break;
+      case 8: go(std::integral_constant<int, 8>{}); break;
+      default: throw HipError("splitk_resid: split must be 2 .. 8");
     }
     DLLM_LAUNCH_CHECK("splitk_resid");
   }

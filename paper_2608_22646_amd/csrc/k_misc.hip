@@ -229,9 +229,13 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
   auto by_split = [&](auto nvc) {
     switch (pend.split) {
       case 2: go(nvc, std::integral_constant<int, 2>{}); break;
+      case 3: go(nvc, std::integral_constant<int, 3>{}); break;
       case 4: go(nvc, std::integral_constant<int, 4>{}); break;
+      case 5: go(nvc, std::integral_constant<int, 5>{}); break;
+      case 6: go(nvc, std::integral_constant<int, 6>{}); break;
+      case 7: go(nvc, std::integral_constant<int, 7>{}); break;
       case 8: go(nvc, std::integral_constant<int, 8>{}); break;
-      default: throw HipError("resid_rmsnorm: split must be 2, 4 or 8");
+      default: throw HipError("resid_rmsnorm: split must be 2 .. 8");
     }
   };
   if (nv <= 2)
