@@ -379,27 +379,74 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
 }
 
 
-// Key-split variant for launches too small to give every SIMD a wave: eight
-// waves share 128 queries -- wave w owns queries 32 (w % 4) .. +31 and the key
-// tiles 2u + w / 4 -- so each query is processed by two waves over alternate
-// 64-key tiles.  The ring holds pairs of tiles (two stages of 64 KiB); at the
-// end the second wave of each pair hands its running (max, sum, output) to
-// the first through LDS, which merges them (rescaling both to the larger
-// maximum) and writes the result.
-__global__ void __launch_bounds__(512, 1) attn_split_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
-                                                          const f16_t* __restrict__ vt, bf16_t* __restrict__ out,
-                                                          int L, int Hq, int Hkv) {
+// Key-split variant with 32-key tiles for short launches (batch 1 at a few
+// hundred tokens): a workgroup owns 32 QG queries of one (sequence, head) and
+// runs QG x 4 waves -- wave w takes queries 32 (w % QG) .. +31 and the key
+// tiles 4u + w / QG, u = 0, 1, ... -- so the grid reaches every CU and each
+// wave's chain of dependent tiles is a quarter of the sequence.  A step brings
+// four 32-key tiles (K [32][128], V^T [128][32], 16 KiB each) into a 2-stage
+// LDS ring by LDS-DMA; at the end the four key groups' running (max, sum,
+// output) states are merged in group order through LDS.
+constexpr int KT2 = 32, KB2 = KT2 * HD * 2, TB2 = 2 * KB2, KGRP = 4, STEP2 = KGRP * TB2;
+
+__device__ __forceinline__ int v2_off(int d, int chunk) {  // V^T rows of 64 B, 4 chunks
+  return KB2 + d * 64 + ((chunk ^ ((d >> 2) & 3)) << 4);
+}
+
+template <int QG>
+__global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_t* __restrict__ q,
+                                                                    const bf16_t* __restrict__ k,
+                                                                    const f16_t* __restrict__ vt,
+                                                                    bf16_t* __restrict__ out, int L, int Hq, int Hkv) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int NW = 8, QG = 4, S = 2, PAIR = 2 * STAGE;
-  constexpr int PER_PAIR = 64 / NW;  // 2 x (16 K + 16 V^T) DMA instructions per pair
+  constexpr int NW = QG * KGRP, S = 2;
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qw = wave % QG, kg = wave / QG;
+  const int qg = wave % QG, kg = wave / QG;
   const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
-  const int q0 = blockIdx.x * (QW * QG) + qw * QW;
+  const int q0 = blockIdx.x * (QW * QG) + qg * QW;
   const int lq = lane & 31, half = lane >> 5;
   const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
   const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
+
+  // DMA of a step: 64 instructions of 1 KiB, instruction j (tile j / 16,
+  // part j % 16) issued by wave j % NW.  K part i < 8: keys 4i + l/16, slot
+  // l%16 holding chunk (l%16) ^ (key & 15); V^T part i >= 8: d rows
+  // 16 (i - 8) + l/4, slot l%4 holding chunk (l%4) ^ ((d >> 2) & 3).  Reads
+  // past the end of this head's K or V^T return zeros (buffer bound).
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, 0, L * HD * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, 0, HD * L * 2, 0x00020000);
+  constexpr int PJ = (64 + NW - 1) / NW;
+  uint32_t voff[PJ];
+#pragma unroll
+  for (int x = 0; x < PJ; ++x) {
+    const int j = wave + NW * x, part = j & 15;
+    if (part < 8) {
+      const int key = 4 * part + (lane >> 4), kc = (lane & 15) ^ (key & 15);
+      voff[x] = (uint32_t)((key * HD + kc * 8) * 2);
+    } else {
+      const int d = 16 * (part - 8) + (lane >> 2), vc = (lane & 3) ^ ((d >> 2) & 3);
+      voff[x] = (uint32_t)(((size_t)d * L + vc * 8) * 2);
+    }
+  }
+  auto issue = [&](int u) {
+    char* base = lds + (u % S) * STEP2;
+#pragma unroll
+    for (int x = 0; x < PJ; ++x) {
+      const int j = wave + NW * x;
+      if (j < 64) {
+        const int tile = j >> 4, part = j & 15, t0 = (KGRP * u + tile) * KT2;
+        char* dst = base + tile * TB2 + part * 1024;
+        if (part < 8)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)dst, 16, voff[x] + t0 * HD * 2, 0, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)dst, 16, voff[x] + t0 * 2, 0, 0, 0);
+      }
+    }
+  };
+
+  const int nsteps = (L + KGRP * KT2 - 1) / (KGRP * KT2);
+  issue(0);
 
   bf16x8_t qf[8];
   {
@@ -412,37 +459,6 @@ __global__ void __launch_bounds__(512, 1) attn_split_kernel(const bf16_t* __rest
     }
   }
 
-  // DMA as in attn_stream_kernel, for both tiles of a pair: instruction i of a
-  // tile is issued by wave i % NW (two K and two V^T instructions per wave)
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, 0, L * HD * 2, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, 0, HD * L * 2, 0x00020000);
-  constexpr int PK = 16 / NW;
-  uint32_t vok[PK], vov[PK];
-#pragma unroll
-  for (int j = 0; j < PK; ++j) {
-    const int i = wave + NW * j;
-    const int key = 4 * i + (lane >> 4), kc = (lane & 15) ^ (key & 15);
-    vok[j] = (uint32_t)((key * HD + kc * 8) * 2);
-    const int d = 8 * i + (lane >> 3), vc = (lane & 7) ^ ((d >> 1) & 7);
-    vov[j] = (uint32_t)(((size_t)d * L + vc * 8) * 2);
-  }
-  auto issue = [&](int u) {
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      char* base = lds + (u % S) * PAIR + sub * STAGE;
-      const int t0 = (2 * u + sub) * KT;
-#pragma unroll
-      for (int j = 0; j < PK; ++j) {
-        const int i = wave + NW * j;
-        // out-of-range tiles (past this head's K / V^T) read zeros
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(base + i * 1024), 16, vok[j] + t0 * HD * 2, 0, 0,
-                                                 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(base + K_BYTES + i * 1024), 16, vov[j] + t0 * 2, 0,
-                                                 0, 0);
-      }
-    }
-  };
-
   f32x16_t o[4];
 #pragma unroll
   for (int ds = 0; ds < 4; ++ds)
@@ -451,43 +467,38 @@ __global__ void __launch_bounds__(512, 1) attn_split_kernel(const bf16_t* __rest
   float m_run = -INFINITY, l_run = 0.f;
   const float sc = 1.4426950408889634f / sqrtf((float)HD);
 
-  const int ntiles = (L + KT - 1) / KT, npairs = (ntiles + 1) / 2;
-  issue(0);
-  for (int u = 0; u < npairs; ++u) {
+  for (int u = 0; u < nsteps; ++u) {
     wait_vmcnt_a<0>();
-    barrier_nofence_a();  // pair u visible; slot (u + 1) % 2 free
-    if (u + 1 < npairs) issue(u + 1);
-    const int t = 2 * u + kg;
-    if (t >= ntiles) continue;  // odd tile count: the second group has nothing in the last pair
-    const char* base = lds + (u % S) * PAIR + kg * STAGE;
+    barrier_nofence_a();  // step u visible; slot (u + 1) % 2 free
+    if (u + 1 < nsteps) issue(u + 1);
+    const int t0 = (KGRP * u + kg) * KT2;
+    if (t0 >= L) continue;  // this group has no keys left in the last step
+    const char* base = lds + (u % S) * STEP2 + kg * TB2;
 
-    f32x16_t s2[2];
+    // two independent accumulation chains (even and odd 16-dim slices)
+    f32x16_t s2, s2b;
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
+    for (int r = 0; r < 16; ++r) s2[r] = s2b[r] = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s2[st][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + lq, ks * 2 + half));
-        s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s2[st], 0, 0, 0);
-      }
+    for (int ks = 0; ks < 8; ks += 2) {
+      const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(base + k_off(lq, ks * 2 + half));
+      const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(base + k_off(lq, ks * 2 + 2 + half));
+      s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s2, 0, 0, 0);
+      s2b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks + 1], s2b, 0, 0, 0);
     }
-    const int t0 = t * KT;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s2[r] += s2b[r];
     float mt = -INFINITY;
-    if (t0 + KT <= L) {
+    if (t0 + KT2 <= L) {
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s2[st][r]);
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s2[r]);
     } else {
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = t0 + st * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (key >= L) s2[st][r] = -INFINITY;
-          mt = fmaxf(mt, s2[st][r]);
-        }
+      for (int r = 0; r < 16; ++r) {
+        const int key = t0 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (key >= L) s2[r] = -INFINITY;
+        mt = fmaxf(mt, s2[r]);
+      }
     }
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sc;
     if (__ballot(mt > m_run + 8.0f) != 0ull) {
@@ -502,65 +513,90 @@ __global__ void __launch_bounds__(512, 1) attn_split_kernel(const bf16_t* __rest
     }
     float psum = 0.f;
 #pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(fmaf(s2[st][r], sc, -m_run));
-        s2[st][r] = p;
-        psum += p;
-      }
+    for (int r = 0; r < 16; ++r) {
+      const float p = exp2f(fmaf(s2[r], sc, -m_run));
+      s2[r] = p;
+      psum += p;
+    }
     l_run += psum;
 
 #pragma unroll
-    for (int jk = 0; jk < 4; ++jk) {
+    for (int jk = 0; jk < 2; ++jk) {
       f16x8_t pf;
-      const int st = jk >> 1, r0 = (jk & 1) * 8;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[st][r0 + e];
+      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[jk * 8 + e];
+      // slots 0-3: keys 16jk + 4*half + [0,4); slots 4-7: keys 16jk + 8 + 4*half + [0,4)
       const int kA = jk * 16 + 4 * half, kB = kA + 8;
 #pragma unroll
       for (int ds = 0; ds < 4; ++ds) {
         const int d = ds * 32 + lq;
-        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kA >> 3) + (kA & 7) * 2);
-        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kB >> 3) + (kB & 7) * 2);
+        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v2_off(d, kA >> 3) + (kA & 7) * 2);
+        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v2_off(d, kB >> 3) + (kB & 7) * 2);
         const f16x8_t vf = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
         o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
       }
     }
   }
 
-  // hand-over through LDS (the ring is idle once every wave has passed here):
-  // per query wave, 64 floats of o and (m, l) per lane
+  // merge the four key groups of each query group in group order (the ring
+  // is idle once every wave has passed the barrier): groups 1..3 leave their
+  // 64 floats of o as 16 lane-contiguous float4 rows, then (m, l)
   __syncthreads();
-  float* xo = reinterpret_cast<float*>(lds) + (size_t)qw * (66 * 64);
-  if (kg == 1) {
+  constexpr int XW = 17 * 64 * 4;  // floats per handed-over wave
+  if (kg > 0) {
+    float4* xo = reinterpret_cast<float4*>(lds) + (size_t)(wave - QG) * (XW / 4) + lane;
 #pragma unroll
     for (int ds = 0; ds < 4; ++ds)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) xo[(ds * 16 + r) * 64 + lane] = o[ds][r];
-    xo[64 * 64 + lane] = m_run;
-    xo[65 * 64 + lane] = l_run;
+      for (int rq = 0; rq < 4; ++rq)
+        xo[(ds * 4 + rq) * 64] = make_float4(o[ds][4 * rq], o[ds][4 * rq + 1], o[ds][4 * rq + 2], o[ds][4 * rq + 3]);
+    xo[16 * 64] = make_float4(m_run, l_run, 0.f, 0.f);
   }
   __syncthreads();
-  if (kg == 1) return;
+  if (kg > 0) return;
   {
-    const float m1 = xo[64 * 64 + lane], l1 = xo[65 * 64 + lane];
-    const float m = fmaxf(m_run, m1);
+    const float4* x4 = reinterpret_cast<const float4*>(lds) + lane;
+    float me[KGRP - 1], le[KGRP - 1];
+    float m = m_run;
+#pragma unroll
+    for (int e = 1; e < KGRP; ++e) {
+      const float4 ml = x4[(size_t)(qg + QG * (e - 1)) * (XW / 4) + 16 * 64];
+      me[e - 1] = ml.x;
+      le[e - 1] = ml.y;
+      m = fmaxf(m, ml.x);
+    }
     // a group that saw no key (m = -inf) contributes nothing
     const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - m);
-    const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - m);
-    l_run = l_run * a0 + l1 * a1;
+    l_run *= a0;
 #pragma unroll
     for (int ds = 0; ds < 4; ++ds)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[ds][r] = o[ds][r] * a0 + xo[(ds * 16 + r) * 64 + lane] * a1;
+      for (int r = 0; r < 16; ++r) o[ds][r] *= a0;
+#pragma unroll
+    for (int e = 1; e < KGRP; ++e) {
+      const float4* xe = x4 + (size_t)(qg + QG * (e - 1)) * (XW / 4);
+      const float ae = me[e - 1] == -INFINITY ? 0.f : exp2f(me[e - 1] - m);
+      l_run += le[e - 1] * ae;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          const float4 v = xe[(ds * 4 + rq) * 64];
+          o[ds][4 * rq] += v.x * ae;
+          o[ds][4 * rq + 1] += v.y * ae;
+          o[ds][4 * rq + 2] += v.z * ae;
+          o[ds][4 * rq + 3] += v.w * ae;
+        }
+    }
   }
 
+  // normalise and stage the wave's 32 output rows (bf16, 272-byte pitch) in
+  // the hand-over slot of its group-1 partner, which only this wave reads,
+  // then store them as whole 256-byte rows
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
-  const int qi = q0 + lq;
-  if (qi >= L) return;
-  bf16_t* orow = out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
+  constexpr int OP = 272;
+  char* stg = lds + (size_t)qg * XW * 4;
 #pragma unroll
   for (int ds = 0; ds < 4; ++ds)
 #pragma unroll
@@ -569,8 +605,16 @@ __global__ void __launch_bounds__(512, 1) attn_split_kernel(const bf16_t* __rest
       uint2 w;
       w.x = pack_bf16x2(o[ds][rg * 4 + 0] * inv, o[ds][rg * 4 + 1] * inv);
       w.y = pack_bf16x2(o[ds][rg * 4 + 2] * inv, o[ds][rg * 4 + 3] * inv);
-      *reinterpret_cast<uint2*>(orow + d) = w;
+      *reinterpret_cast<uint2*>(stg + lq * OP + d * 2) = w;
     }
+  __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0): this wave's writes landed
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const int row = it * 4 + (lane >> 4), ch = lane & 15, qi = q0 + row;
+    if (qi < L)
+      *reinterpret_cast<uint4*>(out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD + ch * 8) =
+          *reinterpret_cast<const uint4*>(stg + row * OP + ch * 16);
+  }
 #endif
 }
 
@@ -582,18 +626,28 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
   if (L % 8 == 0) {
     // streaming kernel: 8 waves (256 queries) per workgroup when that still gives
     // two or more workgroups per CU over the launch, else 4 waves; when even the
-    // 4-wave grid leaves SIMDs without a wave, the key-split kernel (two waves
-    // per query over alternate key tiles)
+    // 4-wave grid leaves CUs without a workgroup, the key-split kernel (four
+    // waves per query over interleaved 32-key tiles)
     const bool wide = (long)((L + 255) / 256) * Hq * B >= 512;
     const size_t lds = 3 * (size_t)STAGE;
-    if ((long)((L + 127) / 128) * Hq * B * 4 < 4L * device_cu_count() && L > KT) {
-      constexpr size_t lds_split = 2 * 2 * (size_t)STAGE;
-      static const hipError_t as = hipFuncSetAttribute((const void*)attn_split_kernel,
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_split);
-      hip_check(as, "hipFuncSetAttribute(attn_split)");
-      hipLaunchKernelGGL(attn_split_kernel, dim3(ceil_div(L, QW * 4), Hq, B), dim3(512), lds_split, s, q, k, vt, out,
-                         L, Hq, Hkv);
-      DLLM_LAUNCH_CHECK("attn_split");
+    const long cus = device_cu_count();
+    if ((long)((L + 127) / 128) * Hq * B < cus && L > KT) {
+      // 64 queries per workgroup when that still fits the CUs, else 96
+      auto go = [&](auto qgc) {
+        constexpr int QG = decltype(qgc)::value;
+        constexpr size_t ring = 2 * (size_t)STEP2, merge = (size_t)3 * QG * 17 * 64 * 16;
+        constexpr size_t lds_kv = ring > merge ? ring : merge;
+        static const hipError_t a = hipFuncSetAttribute((const void*)attn_kv4_kernel<QG>,
+                                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_kv);
+        hip_check(a, "hipFuncSetAttribute(attn_kv4)");
+        hipLaunchKernelGGL(attn_kv4_kernel<QG>, dim3(ceil_div(L, QW * QG), Hq, B), dim3(64 * QG * KGRP), lds_kv, s, q,
+                           k, vt, out, L, Hq, Hkv);
+      };
+      if ((long)ceil_div(L, QW * 2) * Hq * B <= cus)
+        go(std::integral_constant<int, 2>{});
+      else
+        go(std::integral_constant<int, 3>{});
+      DLLM_LAUNCH_CHECK("attn_kv4");
       return;
     }
     if (wide) {
