@@ -299,7 +299,8 @@ __global__ void __launch_bounds__(64 * NW, 1) head_bf16_kernel(HeadArgs a) {
 
 // Streaming kernel for up to 32 head rows: NW = 4 waves per workgroup, one
 // per SIMD; a workgroup tile is 32 GW NW vocabulary rows and wave w owns its GW
-// groups w GW .. w GW + GW - 1 of 32 rows.  The wave walks the tiles' 16-k
+// groups w GW .. w GW + GW - 1 of 32 rows (each group lies inside one tile of
+// the copy, so any GW works).  The wave walks the tiles' 16-k
 // slices in order; per slice it loads the GW 1 KiB W operands and the 1 KiB hb
 // operand (the operand-order copy) into a P-deep register ring, so one hb load
 // serves GW MFMAs.  Loads complete in issue order, so before slice u only the
@@ -310,7 +311,7 @@ template <int GW, int P>
 __global__ void __launch_bounds__(256, 1) head_stream_kernel(HeadArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int NW = 4, NT = 64 * NW, TROWS = 32 * GW * NW;
-  static_assert(HEAD_TILE % (32 * GW) == 0 && (GW + 1) * (P - 1) < 64, "tile shape");
+  static_assert(HEAD_TILE % 32 == 0 && (GW + 1) * (P - 1) < 64, "tile shape");
   __shared__ Stat wst[NW][32];
   __shared__ Stat fin[NT];
   __shared__ int last_flag;
@@ -464,14 +465,16 @@ void launch_head_bf16(const HeadArgs& a, hipStream_t s) {
   // stream faster than four whatever the ring depth, so 256-row tiles are kept
   // even where the tile count divides unevenly over the CUs.
   if (a.R <= HEAD_FRAG_ROWS && a.hbf && a.d % 256 == 0) {
-    // streaming kernel, one workgroup per CU: the tile height (128, 256 or 512
-    // rows: GW = 1, 2, 4 groups per wave) that minimises the largest number of
-    // rows a CU streams, weighted by the hb loads per W load (1 / GW; measured:
-    // one per W load costs ~25% of the streaming rate); taller on ties
+    // streaming kernel, one workgroup per CU: the tile height (128, 256, 512 or
+    // 640 rows: GW = 1, 2, 4, 5 groups per wave) that minimises the largest
+    // number of rows a CU streams, weighted by the hb loads per W load (1 / GW;
+    // measured: one per W load costs ~25% of the streaming rate); shorter on
+    // ties.  GW = 5 serves vocabularies just over 4 x 128 rows per CU (V =
+    // 152064: 238 tiles of 640 rows in one round instead of 4-5 tiles of 128).
     const int cus = std::min(device_cu_count(), MAX_WG);
     int best_gw = 4;
     double best = 1e30;
-    for (int gw = 4; gw >= 1; gw /= 2) {
+    for (int gw : {4, 5, 2, 1}) {
       const long tiles = (a.V + 128L * gw - 1) / (128L * gw);
       const double t = (double)((tiles + cus - 1) / cus) * gw * (1.0 + 0.25 / gw);
       if (t < best - 1e-9) {
@@ -480,7 +483,9 @@ void launch_head_bf16(const HeadArgs& a, hipStream_t s) {
       }
     }
     const int grid = (int)std::min<long>((a.V + 128L * best_gw - 1) / (128L * best_gw), cus);
-    if (best_gw == 4)
+    if (best_gw == 5)
+      hipLaunchKernelGGL((head_stream_kernel<5, 8>), dim3(grid), dim3(256), 0, s, a);
+    else if (best_gw == 4)
       hipLaunchKernelGGL((head_stream_kernel<4, 8>), dim3(grid), dim3(256), 0, s, a);
     else if (best_gw == 2)
       hipLaunchKernelGGL((head_stream_kernel<2, 16>), dim3(grid), dim3(256), 0, s, a);
