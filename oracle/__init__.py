@@ -11,10 +11,11 @@ Modules
   forward    -- the bidirectional transformer forward (Section 2, Section 4.1)
   vocab      -- token confidence and greedy prediction (Box 1, Eq. first_conf)
   controller -- thresholds, budgets and Algorithm 1 (Boxes 2-7, Section 4.7)
+  kvcache    -- cross-step key/value reuse (Section 5's cached decoder)
 
 Parity status: every function is pinned by ``tests/test_oracle_*.py``
 against library routines, closed forms, hand-derived traces and invariants;
 the absolute decoding trajectory of a random-weight model has no printed
 counterpart in the paper and is pinned only through those pieces.
 """
-from . import controller, forward, vocab  # noqa: F401
+from . import controller, forward, kvcache, vocab  # noqa: F401
