@@ -265,6 +265,64 @@ int dllm_generate(const dllm_model* model, const dllm_cai_params* params, const 
                   float* conf_trace, int32_t* argmax_trace, void* workspace, size_t workspace_bytes,
                   void* stream);
 
+/*
+ * Cross-step key/value reuse (Section 5: the decoder runs on a KV cache
+ * refreshed every 16 steps for LLaDA and 8 for Dream; the paper does not
+ * define the cache further).  Reading implemented: local step t of a block is
+ * a refresh step when t % refresh_every == 0; a refresh step runs the full
+ * forward and stores every layer's keys (after RoPE) and values for all L
+ * positions; any other step runs only the current block's rows through the
+ * layers, attending over the stored keys/values of the other positions (as of
+ * the last refresh) and the block rows' fresh ones, which are written into the
+ * cache at the block positions.  An approximation for two or more layers.
+ *
+ * The cache is caller-owned device memory (256-byte aligned) of
+ * dllm_kv_cache_size() bytes for B sequences of L positions: per layer, keys
+ * [B, Hkv, L, hd] then values transposed [B, Hkv, hd, L] (float32 for a
+ * DLLM_F32 model; bf16 keys and IEEE-half values holding bf16 values for
+ * DLLM_BF16), each rounded up to 256 bytes.  Calls that use it need the same
+ * B and L.  Errors as for the calls above, plus DLLM_ENOMEM for a cache that
+ * is too small.
+ */
+int dllm_kv_cache_size(const dllm_model* model, int32_t B, int32_t L, size_t* bytes);
+
+/* refresh != 0: dllm_forward that also stores every layer's keys/values for
+ * all L positions into kv_cache.  refresh == 0: the forward of rows [row0,
+ * row0 + rows) of every sequence only, against the cache (conf/argmax/logits
+ * of those rows as for dllm_forward).  The workspace is the one for (B, L,
+ * rows). */
+int dllm_forward_kv(const dllm_model* model, const int32_t* x, int32_t B, int32_t L, int32_t row0, int32_t rows,
+                    int32_t refresh, float* conf, int32_t* argmax, float* logits, void* kv_cache, size_t kv_bytes,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Stages of the cached forward, for tests: dllm_embed_rows puts the embeddings
+ * of x[b, row0 + i] at the workspace's h[b*rows + i]; dllm_layer_kv runs one
+ * layer (part as for dllm_layer) on those B*rows rows, writing their
+ * keys/values into the layer's cache entries at positions row0 .. row0+rows-1
+ * and attending over all L cached positions (rows == L, row0 == 0: the full
+ * layer, filling the cache).  Workspace for (B, L, rows), or (B, L, 0) when
+ * rows == L. */
+int dllm_embed_rows(const dllm_model* model, const int32_t* x, int32_t B, int32_t L, int32_t row0, int32_t rows,
+                    void* workspace, size_t workspace_bytes, void* stream);
+int dllm_layer_kv(const dllm_model* model, int32_t layer, int32_t part, int32_t B, int32_t L, int32_t row0,
+                  int32_t rows, void* kv_cache, size_t kv_bytes, void* workspace, size_t workspace_bytes,
+                  void* stream);
+
+/* dllm_step with the cache: refresh != 0 runs the full forward and refreshes
+ * the cache, refresh == 0 the cached forward of the block rows. */
+int dllm_step_kv(const dllm_model* model, const dllm_cai_params* params, int32_t refresh, dllm_state* state,
+                 int32_t B, int32_t P, int32_t G, int32_t block, int32_t t, float* conf_out, int32_t* argmax_out,
+                 int32_t* all_done_host, void* kv_cache, size_t kv_bytes, void* workspace, size_t workspace_bytes,
+                 void* stream);
+
+/* dllm_generate with cross-step key/value reuse: step t of each block
+ * refreshes the cache when t % refresh_every == 0 (>= 1; 1 = every step, the
+ * same decisions as dllm_generate), else runs the cached forward. */
+int dllm_generate_kv(const dllm_model* model, const dllm_cai_params* params, int32_t refresh_every,
+                     const int32_t* prompt, int32_t B, int32_t P, int32_t G, dllm_state* state,
+                     int32_t* forwards_host, int32_t* total_forwards, float* conf_trace, int32_t* argmax_trace,
+                     void* kv_cache, size_t kv_bytes, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Per-kernel timing with HIP events recorded on the launch stream around each
  * launch of the selected kernel classes.  kind: 0 = q/k/v, output and down
  * GEMMs, 1 = attention, 2 = LM head + reduction, 3 = commit, 4 = norms and

@@ -76,6 +76,14 @@ _SIGS = {
                          _vp, _vp, _sz, _vp]),
     "dllm_generate": (_i32, [_vp, _c.POINTER(CaiParams), _vp, _i32, _i32, _i32, _c.POINTER(State), _vp, _vp,
                              _vp, _vp, _vp, _sz, _vp]),
+    "dllm_kv_cache_size": (_i32, [_vp, _i32, _i32, _c.POINTER(_sz)]),
+    "dllm_forward_kv": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
+    "dllm_embed_rows": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
+    "dllm_layer_kv": (_i32, [_vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _sz, _vp, _sz, _vp]),
+    "dllm_step_kv": (_i32, [_vp, _c.POINTER(CaiParams), _i32, _c.POINTER(State), _i32, _i32, _i32, _i32, _i32, _vp,
+                            _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
+    "dllm_generate_kv": (_i32, [_vp, _c.POINTER(CaiParams), _i32, _vp, _i32, _i32, _i32, _c.POINTER(State), _vp,
+                                _vp, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
     "dllm_prof_enable": (_i32, [_vp, _i32]),
     "dllm_prof_read": (_i32, [_vp, _i32, _c.POINTER(_f64), _c.POINTER(_c.c_int64)]),
 }
@@ -322,6 +330,70 @@ class Model:
             at = torch.full((nb, T, B, bl), -1, dtype=torch.int32, device=prompt.device)
         check(lib().dllm_generate(self.h, ctypes.byref(p), _ptr(prompt), B, P, G, ctypes.byref(c), fwd,
                                   ctypes.byref(tot), _ptr(ct), _ptr(at), _ptr(ws), ws.numel(), _stream(stream)))
+        return GenResult(st, list(fwd), tot.value, ct, at)
+
+    # cross-step key/value reuse ---------------------------------------------
+    def kv_cache(self, B, L, device="cuda"):
+        """A caller-owned, 256-byte aligned cache buffer for B sequences of L positions."""
+        n = ctypes.c_size_t()
+        check(lib().dllm_kv_cache_size(self.h, B, L, ctypes.byref(n)))
+        buf = torch.empty(n.value + 256, dtype=torch.uint8, device=device)
+        off = (-buf.data_ptr()) % 256
+        return buf[off:off + n.value]
+
+    def forward_kv(self, x, row0, rows, kv, refresh, ws=None, logits=False, stream=None):
+        """dllm_forward_kv: the refresh forward (refresh=True) or the cached forward of rows [row0, row0 + rows)."""
+        B, L = x.shape
+        ws = ws if ws is not None else self.workspace(B, L, rows, x.device)
+        dev = x.device
+        conf = torch.empty((B * rows,), dtype=torch.float32, device=dev)
+        arg = torch.empty((B * rows,), dtype=torch.int32, device=dev)
+        lg = torch.empty((B * rows, self.cfg.vocab), dtype=torch.float32, device=dev) if logits else None
+        check(lib().dllm_forward_kv(self.h, _ptr(x), B, L, row0, rows, int(bool(refresh)), _ptr(conf), _ptr(arg),
+                                    _ptr(lg), _ptr(kv), kv.numel(), _ptr(ws), ws.numel(), _stream(stream)))
+        return conf.view(B, rows), arg.view(B, rows), (lg.view(B, rows, -1) if logits else None)
+
+    def embed_rows(self, x, row0, rows, ws, stream=None):
+        B, L = x.shape
+        check(lib().dllm_embed_rows(self.h, _ptr(x), B, L, row0, rows, _ptr(ws), ws.numel(), _stream(stream)))
+
+    def layer_kv(self, layer, part, B, L, row0, rows, kv, ws, stream=None):
+        check(lib().dllm_layer_kv(self.h, layer, part, B, L, row0, rows, _ptr(kv), kv.numel(), _ptr(ws), ws.numel(),
+                                  _stream(stream)))
+
+    def step_kv(self, ctl: Controller, st: DecodeState, block, t, refresh, kv, ws, record=False, wait=True,
+                stream=None):
+        p = ctl.to_c()
+        c = st.c()
+        B, bl = st.B, ctl.block_len
+        conf = torch.empty((B, bl), dtype=torch.float32, device=st.x.device) if record else None
+        arg = torch.empty((B, bl), dtype=torch.int32, device=st.x.device) if record else None
+        flag = torch.zeros((1,), dtype=torch.int32).pin_memory() if wait else None
+        check(lib().dllm_step_kv(self.h, ctypes.byref(p), int(bool(refresh)), ctypes.byref(c), B, st.P, st.G, block,
+                                 t, _ptr(conf), _ptr(arg), _ptr(flag), _ptr(kv), kv.numel(), _ptr(ws), ws.numel(),
+                                 _stream(stream)))
+        return (int(flag.item()) if wait else None), conf, arg
+
+    def generate_kv(self, ctl: Controller, prompt, G, refresh_every, ws=None, st=None, kv=None, trace=False,
+                    stream=None):
+        """dllm_generate_kv: the decode with the cache refreshed at steps t % refresh_every == 0."""
+        B, P = prompt.shape
+        bl, T = ctl.block_len, ctl.T
+        nb = G // bl
+        st = st or DecodeState(B, P, G, prompt.device)
+        ws = ws if ws is not None else self.workspace(B, P + G, bl, prompt.device)
+        kv = kv if kv is not None else self.kv_cache(B, P + G, prompt.device)
+        p = ctl.to_c()
+        c = st.c()
+        fwd = (ctypes.c_int32 * nb)()
+        tot = ctypes.c_int32()
+        ct = at = None
+        if trace:
+            ct = torch.full((nb, T, B, bl), float("nan"), dtype=torch.float32, device=prompt.device)
+            at = torch.full((nb, T, B, bl), -1, dtype=torch.int32, device=prompt.device)
+        check(lib().dllm_generate_kv(self.h, ctypes.byref(p), refresh_every, _ptr(prompt), B, P, G, ctypes.byref(c),
+                                     fwd, ctypes.byref(tot), _ptr(ct), _ptr(at), _ptr(kv), kv.numel(), _ptr(ws),
+                                     ws.numel(), _stream(stream)))
         return GenResult(st, list(fwd), tot.value, ct, at)
 
     # profiling --------------------------------------------------------------

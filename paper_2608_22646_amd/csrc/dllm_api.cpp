@@ -100,11 +100,17 @@ Layout make_layout(const dllm_model_cfg& c, int B, int L, int rows) {
     o.part_i = take(tiles * R * 4);
     o.ticket = take(4);
     o.hbf = take((size_t)HEAD_FRAG_ROWS * d * 2);
+    // split-K partials of the full forward (B L rows) and of a cached step's
+    // forward (B rows rows)
     const int qkv_n = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
-    const size_t sk = std::max(std::max(gemm_bf16_splitk_bytes((int)M, qkv_n, c.d_model, EPI_QKV_ROPE),
-                                        gemm_bf16_splitk_bytes((int)M, c.d_model, c.n_heads * c.head_dim, EPI_RESID)),
-                               std::max(gemm_bf16_splitk_bytes((int)M, 2 * c.d_ff, c.d_model, EPI_SWIGLU),
-                                        gemm_bf16_splitk_bytes((int)M, c.d_model, c.d_ff, EPI_RESID)));
+    size_t sk = 0;
+    for (const int mm : {(int)M, (int)R}) {
+      if (mm == 0) continue;
+      sk = std::max({sk, gemm_bf16_splitk_bytes(mm, qkv_n, c.d_model, EPI_QKV_ROPE),
+                     gemm_bf16_splitk_bytes(mm, c.d_model, c.n_heads * c.head_dim, EPI_RESID),
+                     gemm_bf16_splitk_bytes(mm, 2 * c.d_ff, c.d_model, EPI_SWIGLU),
+                     gemm_bf16_splitk_bytes(mm, c.d_model, c.d_ff, EPI_RESID)});
+    }
     o.splitk = take(sk);
   }
   o.conf = take(R * 4);
@@ -163,10 +169,45 @@ const void* W(const dllm_model* m, int i) { return m->w[i]; }
 const bf16_t* Wb(const dllm_model* m, int i) { return static_cast<const bf16_t*>(m->w[i]); }
 const float* Wf(const dllm_model* m, int i) { return static_cast<const float*>(m->w[i]); }
 
+// ---------------------------------------------------------------- key/value cache
+// Per layer l: keys [B, Hkv, L, hd] (after RoPE) at l * 2 * S and values^T
+// [B, Hkv, hd, L] at l * 2 * S + S, S = the 256-byte-rounded size of one of
+// them (float32 for an fp32 model, bf16 keys and IEEE-half values for bf16).
+size_t kv_slab_bytes(const dllm_model_cfg& c, int B, int L) {
+  return align256((size_t)B * c.n_kv_heads * L * c.head_dim * (c.dtype == DLLM_F32 ? 4 : 2));
+}
+size_t kv_cache_bytes(const dllm_model_cfg& c, int B, int L) { return 2 * kv_slab_bytes(c, B, L) * c.n_layers; }
+
+// Rows of the sequences a layer works on, and where its keys/values go: a
+// full forward has Lq = L, pos0 = 0 and keeps them in the workspace (k, vt
+// null) or stores them in the cache; a cached step has the block's Lq rows at
+// positions pos0 .. pos0 + Lq - 1 and attends over the cache.
+struct LayerRows {
+  int Lq, pos0;
+  void* k;
+  void* vt;
+};
+
+LayerRows cache_rows(const dllm_model* m, void* kv, int layer, int B, int L, int Lq, int pos0) {
+  const size_t S = kv_slab_bytes(m->cfg, B, L);
+  char* base = static_cast<char*>(kv) + (size_t)layer * 2 * S;
+  return LayerRows{Lq, pos0, base, base + S};
+}
+
+void check_kv(const dllm_model* m, int B, int L, const void* kv, size_t bytes) {
+  require(kv != nullptr, DLLM_EINVAL, "kv_cache is NULL");
+  require(((uintptr_t)kv & 255) == 0, DLLM_EINVAL, "kv_cache must be 256-byte aligned");
+  const size_t need = kv_cache_bytes(m->cfg, B, L);
+  require(bytes >= need, DLLM_ENOMEM, "kv_cache too small: need " + std::to_string(need) + " bytes");
+}
+
 // ---------------------------------------------------------------- forward pieces
-void run_embed(const dllm_model* m, const int32_t* x, int B, int L, void* ws, const Layout& lay, hipStream_t s) {
+// h[b rows + i] = embedding of x[b, row0 + i] (rows = L, row0 = 0: every
+// position); RoPE tables for all L positions.
+void run_embed(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, void* ws, const Layout& lay,
+               hipStream_t s) {
   const auto& c = m->cfg;
-  launch_embed(x, W(m, 0), c.dtype, at<float>(ws, lay.h), B * L, c.d_model, s);
+  launch_embed(x, W(m, 0), c.dtype, at<float>(ws, lay.h), B, rows, L, row0, c.d_model, s);
   launch_rope_table(at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), L, c.head_dim, c.rope_base, s);
 }
 
@@ -193,21 +234,25 @@ void norm_rows_bf16(const dllm_model* m, float* h, PendingResid* pend, const voi
   }
 }
 
-// One layer (part 0: attention half, 1: MLP half, 2: both).  carry_in holds
-// split-K partials the previous layer's down projection left pending (added by
-// this layer's first norm); with carry_out non-null the down projection leaves
-// its own partials there for the next layer instead of reducing them.  The
-// output projection's partials are folded into the MLP norm when both halves
-// run here.  Without carries h is complete when the call returns.
+// One layer (part 0: attention half, 1: MLP half, 2: both) on the B * Lq rows
+// of h (rows: see LayerRows; null = the full sequence, keys/values in the
+// workspace).  carry_in holds split-K partials the previous layer's down
+// projection left pending (added by this layer's first norm); with carry_out
+// non-null the down projection leaves its own partials there for the next
+// layer instead of reducing them.  The output projection's partials are folded
+// into the MLP norm when both halves run here.  Without carries h is complete
+// when the call returns.
 void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay,
-                    hipStream_t s, PendingResid* carry_in = nullptr, PendingResid* carry_out = nullptr) {
+                    hipStream_t s, PendingResid* carry_in = nullptr, PendingResid* carry_out = nullptr,
+                    const LayerRows* rows = nullptr) {
   const auto& c = m->cfg;
   const int base = 1 + 9 * layer;
-  const int M = B * L, d = c.d_model, hd = c.head_dim;
+  const int Lq = rows ? rows->Lq : L, pos0 = rows ? rows->pos0 : 0;
+  const int M = B * Lq, d = c.d_model, hd = c.head_dim;
   float* h = at<float>(ws, lay.h);
   PendingResid mid;  // output-projection partials, consumed by the MLP norm
   if (part == 0 || part == 2) {
-    norm_rows_bf16(m, h, carry_in, W(m, base + 0), at<void>(ws, lay.a_attn), B, L, s);
+    norm_rows_bf16(m, h, carry_in, W(m, base + 0), at<void>(ws, lay.a_attn), B, Lq, s);
     GemmArgs g{};
     g.epi = EPI_QKV_ROPE;
     g.M = M;
@@ -220,18 +265,20 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     g.n0 = c.n_heads * hd;
     g.n1 = c.n_kv_heads * hd;
     g.q = at<bf16_t>(ws, lay.q);
-    g.k = at<bf16_t>(ws, lay.k);
-    g.vt = at<f16_t>(ws, lay.vt);
+    g.k = rows && rows->k ? static_cast<bf16_t*>(rows->k) : at<bf16_t>(ws, lay.k);
+    g.vt = rows && rows->vt ? static_cast<f16_t*>(rows->vt) : at<f16_t>(ws, lay.vt);
     g.cosb = at<float>(ws, lay.cosb);
     g.sinb = at<float>(ws, lay.sinb);
     g.B = B;
     g.L = L;
+    g.Lq = Lq;
+    g.pos0 = pos0;
     g.Hq = c.n_heads;
     g.Hkv = c.n_kv_heads;
     gemm_bf16(m, g, ws, lay, s, PK_GEMM);
     {
       ProfScope p(m, PK_ATTN, s);
-      launch_attn_bf16(g.q, g.k, g.vt, at<bf16_t>(ws, lay.attn), B, L, c.n_heads, c.n_kv_heads, s);
+      launch_attn_bf16(g.q, g.k, g.vt, at<bf16_t>(ws, lay.attn), B, Lq, L, c.n_heads, c.n_kv_heads, s);
     }
     GemmArgs o{};
     o.epi = EPI_RESID;
@@ -245,7 +292,7 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     gemm_bf16(m, o, ws, lay, s, PK_GEMM, part == 2 ? &mid : nullptr);
   }
   if (part == 1 || part == 2) {
-    norm_rows_bf16(m, h, part == 1 ? carry_in : &mid, W(m, base + 5), at<void>(ws, lay.a_mlp), B, L, s);
+    norm_rows_bf16(m, h, part == 1 ? carry_in : &mid, W(m, base + 5), at<void>(ws, lay.a_mlp), B, Lq, s);
     GemmArgs g{};
     g.epi = EPI_SWIGLU;
     g.M = M;
@@ -272,10 +319,13 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
 }
 
 void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay,
-                   hipStream_t s) {
+                   hipStream_t s, const LayerRows* rows = nullptr) {
   const auto& c = m->cfg;
   const int base = 1 + 9 * layer;
-  const int M = B * L, d = c.d_model, hd = c.head_dim, F = c.d_ff;
+  const int Lq = rows ? rows->Lq : L, pos0 = rows ? rows->pos0 : 0;
+  const int M = B * Lq, d = c.d_model, hd = c.head_dim, F = c.d_ff;
+  float* kk = rows && rows->k ? static_cast<float*>(rows->k) : at<float>(ws, lay.k);
+  float* vv = rows && rows->vt ? static_cast<float*>(rows->vt) : at<float>(ws, lay.vt);
   const int nq = c.n_heads * hd, nkv = c.n_kv_heads * hd, nraw = nq + 2 * nkv;
   float* h = at<float>(ws, lay.h);
   if (part == 0 || part == 2) {
@@ -283,7 +333,7 @@ void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void*
     float* raw = at<float>(ws, lay.raw);
     {
       ProfScope p(m, PK_NORM, s);
-      launch_rmsnorm(h, W(m, base + 0), a, 0, B, L, L, 0, d, c.rms_eps, s);
+      launch_rmsnorm(h, W(m, base + 0), a, 0, B, Lq, Lq, 0, d, c.rms_eps, s);
     }
     {
       ProfScope p(m, PK_GEMM, s);
@@ -291,12 +341,12 @@ void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void*
       launch_gemm_f32(a, Wf(m, base + 2), raw + nq, M, nkv, d, nraw, false, s);
       launch_gemm_f32(a, Wf(m, base + 3), raw + nq + nkv, M, nkv, d, nraw, false, s);
     }
-    launch_rope_split_f32(raw, at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), at<float>(ws, lay.q),
-                          at<float>(ws, lay.k), at<float>(ws, lay.vt), B, L, c.n_heads, c.n_kv_heads, hd, s);
+    launch_rope_split_f32(raw, at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), at<float>(ws, lay.q), kk, vv, B,
+                          Lq, L, pos0, c.n_heads, c.n_kv_heads, hd, s);
     {
       ProfScope p(m, PK_ATTN, s);
-      launch_attn_f32(at<float>(ws, lay.q), at<float>(ws, lay.k), at<float>(ws, lay.vt), at<float>(ws, lay.attn), B,
-                      L, c.n_heads, c.n_kv_heads, hd, s);
+      launch_attn_f32(at<float>(ws, lay.q), kk, vv, at<float>(ws, lay.attn), B, Lq, L, c.n_heads, c.n_kv_heads, hd,
+                      s);
     }
     ProfScope p(m, PK_GEMM, s);
     launch_gemm_f32(at<float>(ws, lay.attn), Wf(m, base + 4), h, M, d, nq, d, true, s);
@@ -305,7 +355,7 @@ void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void*
     float* a = at<float>(ws, lay.a_mlp);
     {
       ProfScope p(m, PK_NORM, s);
-      launch_rmsnorm(h, W(m, base + 5), a, 0, B, L, L, 0, d, c.rms_eps, s);
+      launch_rmsnorm(h, W(m, base + 5), a, 0, B, Lq, Lq, 0, d, c.rms_eps, s);
     }
     {
       ProfScope p(m, PK_GATEUP, s);
@@ -318,11 +368,12 @@ void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void*
   }
 }
 
-void run_layer(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay, hipStream_t s) {
+void run_layer(const dllm_model* m, int layer, int part, int B, int L, void* ws, const Layout& lay, hipStream_t s,
+               const LayerRows* rows = nullptr) {
   if (m->cfg.dtype == DLLM_BF16)
-    run_layer_bf16(m, layer, part, B, L, ws, lay, s);
+    run_layer_bf16(m, layer, part, B, L, ws, lay, s, nullptr, nullptr, rows);
   else
-    run_layer_f32(m, layer, part, B, L, ws, lay, s);
+    run_layer_f32(m, layer, part, B, L, ws, lay, s, rows);
 }
 
 void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf, int32_t* argmax, float* logits,
@@ -452,22 +503,48 @@ void fill_commit_args(const dllm_cai_params* p, dllm_state* st, CommitArgs* a, i
   a->fixed_k = (p->flags & DLLM_F_FIXED) ? p->block_len / T + (t < p->block_len % T ? 1 : 0) : 0;
 }
 
+// Every layer on the B * Lq rows of h (see LayerRows; kv null: the full
+// sequence with keys/values in the workspace).
+void run_layers(const dllm_model* m, int B, int L, int Lq, int pos0, void* kv, void* ws, const Layout& lay,
+                hipStream_t s) {
+  const int nl = m->cfg.n_layers;
+  // each layer's down-projection partials are added by the next layer's first
+  // norm; the last layer reduces its own, so h is complete for the head
+  PendingResid carry;
+  for (int l = 0; l < nl; ++l) {
+    LayerRows r{Lq, pos0, nullptr, nullptr};
+    if (kv) r = cache_rows(m, kv, l, B, L, Lq, pos0);
+    if (m->cfg.dtype == DLLM_BF16)
+      run_layer_bf16(m, l, 2, B, L, ws, lay, s, &carry, l + 1 < nl ? &carry : nullptr, &r);
+    else
+      run_layer_f32(m, l, 2, B, L, ws, lay, s, &r);
+  }
+}
+
+// The full forward over all L positions, head on rows [row0, row0 + rows);
+// with kv non-null every layer's keys/values are stored in the cache
+// (a refresh step).
 void forward_all(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, float* conf,
-                 int32_t* argmax, float* logits, void* ws, const Layout& lay, hipStream_t s) {
+                 int32_t* argmax, float* logits, void* ws, const Layout& lay, hipStream_t s, void* kv = nullptr) {
   {
     ProfScope p(m, PK_NORM, s);
-    run_embed(m, x, B, L, ws, lay, s);
+    run_embed(m, x, B, L, 0, L, ws, lay, s);
   }
-  if (m->cfg.dtype == DLLM_BF16) {
-    // each layer's down-projection partials are added by the next layer's first
-    // norm; the last layer reduces its own, so h is complete for the head
-    PendingResid carry;
-    const int nl = m->cfg.n_layers;
-    for (int l = 0; l < nl; ++l) run_layer_bf16(m, l, 2, B, L, ws, lay, s, &carry, l + 1 < nl ? &carry : nullptr);
-  } else {
-    for (int l = 0; l < m->cfg.n_layers; ++l) run_layer(m, l, 2, B, L, ws, lay, s);
-  }
+  run_layers(m, B, L, L, 0, kv, ws, lay, s);
   run_head(m, B, L, row0, rows, conf, argmax, logits, ws, lay, s);
+}
+
+// A cached step's forward: only rows [row0, row0 + rows) of each sequence go
+// through the layers, attending over the cache (whose entries at those
+// positions they overwrite); the head runs on all of them.
+void forward_cached(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, float* conf,
+                    int32_t* argmax, float* logits, void* kv, void* ws, const Layout& lay, hipStream_t s) {
+  {
+    ProfScope p(m, PK_NORM, s);
+    run_embed(m, x, B, L, row0, rows, ws, lay, s);
+  }
+  run_layers(m, B, L, rows, row0, kv, ws, lay, s);
+  run_head(m, B, rows, 0, rows, conf, argmax, logits, ws, lay, s);
 }
 
 int finish(const ApiError& e) {
@@ -594,7 +671,43 @@ int dllm_embed(const dllm_model* m, const int32_t* x, int32_t B, int32_t L, void
   require(x != nullptr, DLLM_EINVAL, "x is NULL");
   Layout lay;
   check_ws(m, B, L, 0, ws, ws_bytes, &lay);
-  run_embed(m, x, B, L, ws, lay, (hipStream_t)stream);
+  run_embed(m, x, B, L, 0, L, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_embed_rows(const dllm_model* m, const int32_t* x, int32_t B, int32_t L, int32_t row0, int32_t rows,
+                    void* ws, size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(x != nullptr, DLLM_EINVAL, "x is NULL");
+  require(row0 >= 0 && rows >= 1 && row0 + rows <= L, DLLM_ESHAPE, "rows out of range");
+  Layout lay;
+  check_ws(m, B, L, rows, ws, ws_bytes, &lay);
+  run_embed(m, x, B, L, row0, rows, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_kv_cache_size(const dllm_model* m, int32_t B, int32_t L, size_t* bytes) {
+  API_BEGIN
+  check_model(m);
+  require(bytes != nullptr, DLLM_EINVAL, "bytes is NULL");
+  require(B >= 1 && L >= 1, DLLM_ESHAPE, "bad sizes");
+  *bytes = kv_cache_bytes(m->cfg, B, L);
+  API_END
+}
+
+int dllm_layer_kv(const dllm_model* m, int32_t layer, int32_t part, int32_t B, int32_t L, int32_t row0,
+                  int32_t rows, void* kv, size_t kv_bytes, void* ws, size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(layer >= 0 && layer < m->cfg.n_layers, DLLM_EINVAL, "layer out of range");
+  require(part >= 0 && part <= 2, DLLM_EINVAL, "part must be 0, 1 or 2");
+  require(row0 >= 0 && rows >= 1 && row0 + rows <= L, DLLM_ESHAPE, "rows out of range");
+  check_kv(m, B, L, kv, kv_bytes);
+  Layout lay;
+  check_ws(m, B, L, rows == L ? 0 : rows, ws, ws_bytes, &lay);
+  const LayerRows r = cache_rows(m, kv, layer, B, L, rows, row0);
+  run_layer(m, layer, part, B, L, ws, lay, (hipStream_t)stream, &r);
   API_END
 }
 
@@ -634,6 +747,23 @@ int dllm_forward(const dllm_model* m, const int32_t* x, int32_t B, int32_t L, in
   API_END
 }
 
+int dllm_forward_kv(const dllm_model* m, const int32_t* x, int32_t B, int32_t L, int32_t row0, int32_t rows,
+                    int32_t refresh, float* conf, int32_t* argmax, float* logits, void* kv, size_t kv_bytes, void* ws,
+                    size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(x && conf && argmax, DLLM_EINVAL, "NULL argument");
+  require(row0 >= 0 && rows >= 1 && row0 + rows <= L, DLLM_ESHAPE, "rows out of range");
+  check_kv(m, B, L, kv, kv_bytes);
+  Layout lay;
+  check_ws(m, B, L, rows, ws, ws_bytes, &lay);
+  if (refresh)
+    forward_all(m, x, B, L, row0, rows, conf, argmax, logits, ws, lay, (hipStream_t)stream, kv);
+  else
+    forward_cached(m, x, B, L, row0, rows, conf, argmax, logits, kv, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
 int dllm_state_init(int32_t mask_id, const int32_t* prompt, int32_t B, int32_t P, int32_t G, dllm_state* st,
                     void* stream) {
   API_BEGIN
@@ -662,14 +792,20 @@ int dllm_commit(const dllm_cai_params* p, dllm_state* st, const float* conf, con
 }
 
 namespace {
+// One denoising step.  kv null: the full forward; else a refresh step (the
+// full forward storing the cache) when refresh is set, a cached step otherwise.
 void step_impl(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int B, int P, int G, int block, int t,
-               float* conf_out, int32_t* argmax_out, void* ws, const Layout& lay, hipStream_t s) {
+               float* conf_out, int32_t* argmax_out, void* ws, const Layout& lay, hipStream_t s, void* kv = nullptr,
+               bool refresh = true) {
   CommitArgs a{};
   fill_commit_args(p, st, &a, B, P, G, block, t, m->cfg.mask_id);
   const int bl = p->block_len;
   float* conf = conf_out ? conf_out : at<float>(ws, lay.conf);
   int32_t* arg = argmax_out ? argmax_out : at<int32_t>(ws, lay.argmax);
-  forward_all(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, ws, lay, s);
+  if (kv && !refresh)
+    forward_cached(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, kv, ws, lay, s);
+  else
+    forward_all(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, ws, lay, s, kv);
   a.conf = conf;
   a.argmax = arg;
   a.all_done = at<int32_t>(ws, lay.all_done);
@@ -697,17 +833,31 @@ int dllm_step(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int
   API_END
 }
 
-int dllm_generate(const dllm_model* m, const dllm_cai_params* p, const int32_t* prompt, int32_t B, int32_t P,
-                  int32_t G, dllm_state* st, int32_t* forwards_host, int32_t* total_forwards, float* conf_trace,
-                  int32_t* argmax_trace, void* ws, size_t ws_bytes, void* stream) {
+int dllm_step_kv(const dllm_model* m, const dllm_cai_params* p, int32_t refresh, dllm_state* st, int32_t B,
+                 int32_t P, int32_t G, int32_t block, int32_t t, float* conf_out, int32_t* argmax_out,
+                 int32_t* all_done_host, void* kv, size_t kv_bytes, void* ws, size_t ws_bytes, void* stream) {
   API_BEGIN
   check_model(m);
   check_params(p);
-  require(G >= 1 && G % p->block_len == 0, DLLM_ESHAPE, "G must be a positive multiple of block_len");
-  require(P >= 0 && (P == 0 || prompt), DLLM_EINVAL, "bad prompt");
+  check_kv(m, B, P + G, kv, kv_bytes);
   Layout lay;
   check_ws(m, B, P + G, p->block_len, ws, ws_bytes, &lay);
   hipStream_t s = (hipStream_t)stream;
+  step_impl(m, p, st, B, P, G, block, t, conf_out, argmax_out, ws, lay, s, kv, refresh != 0);
+  if (all_done_host) {
+    hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
+              "hipMemcpyAsync");
+    hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
+    *all_done_host = *m->pinned_flag;
+  }
+  API_END
+}
+
+namespace {
+// The block loop of dllm_generate / dllm_generate_kv (refresh_every 0: no cache).
+void generate_impl(const dllm_model* m, const dllm_cai_params* p, const int32_t* prompt, int B, int P, int G,
+                   dllm_state* st, int32_t* forwards_host, int32_t* total_forwards, float* conf_trace,
+                   int32_t* argmax_trace, void* kv, int refresh_every, void* ws, const Layout& lay, hipStream_t s) {
   const int bl = p->block_len, nb = G / bl, T = steps_T(p);
   launch_state_init(prompt, st->x, st->commit_step, st->reason, st->s, st->budget, st->ell, st->done, B, P, G,
                     m->cfg.mask_id, s);
@@ -717,7 +867,7 @@ int dllm_generate(const dllm_model* m, const dllm_cai_params* p, const int32_t* 
     for (int t = 0; t < T; ++t) {
       float* ct = conf_trace ? conf_trace + ((size_t)blk * T + t) * B * bl : nullptr;
       int32_t* at_ = argmax_trace ? argmax_trace + ((size_t)blk * T + t) * B * bl : nullptr;
-      step_impl(m, p, st, B, P, G, blk, t, ct, at_, ws, lay, s);
+      step_impl(m, p, st, B, P, G, blk, t, ct, at_, ws, lay, s, kv, refresh_every == 0 || t % refresh_every == 0);
       ++n;
       hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
                 "hipMemcpyAsync");
@@ -728,6 +878,39 @@ int dllm_generate(const dllm_model* m, const dllm_cai_params* p, const int32_t* 
     total += n;
   }
   if (total_forwards) *total_forwards = total;
+}
+}  // namespace
+
+int dllm_generate(const dllm_model* m, const dllm_cai_params* p, const int32_t* prompt, int32_t B, int32_t P,
+                  int32_t G, dllm_state* st, int32_t* forwards_host, int32_t* total_forwards, float* conf_trace,
+                  int32_t* argmax_trace, void* ws, size_t ws_bytes, void* stream) {
+  API_BEGIN
+  check_model(m);
+  check_params(p);
+  require(G >= 1 && G % p->block_len == 0, DLLM_ESHAPE, "G must be a positive multiple of block_len");
+  require(P >= 0 && (P == 0 || prompt), DLLM_EINVAL, "bad prompt");
+  Layout lay;
+  check_ws(m, B, P + G, p->block_len, ws, ws_bytes, &lay);
+  generate_impl(m, p, prompt, B, P, G, st, forwards_host, total_forwards, conf_trace, argmax_trace, nullptr, 0, ws,
+                lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_generate_kv(const dllm_model* m, const dllm_cai_params* p, int32_t refresh_every, const int32_t* prompt,
+                     int32_t B, int32_t P, int32_t G, dllm_state* st, int32_t* forwards_host, int32_t* total_forwards,
+                     float* conf_trace, int32_t* argmax_trace, void* kv, size_t kv_bytes, void* ws, size_t ws_bytes,
+                     void* stream) {
+  API_BEGIN
+  check_model(m);
+  check_params(p);
+  require(refresh_every >= 1, DLLM_EINVAL, "refresh_every must be >= 1");
+  require(G >= 1 && G % p->block_len == 0, DLLM_ESHAPE, "G must be a positive multiple of block_len");
+  require(P >= 0 && (P == 0 || prompt), DLLM_EINVAL, "bad prompt");
+  check_kv(m, B, P + G, kv, kv_bytes);
+  Layout lay;
+  check_ws(m, B, P + G, p->block_len, ws, ws_bytes, &lay);
+  generate_impl(m, p, prompt, B, P, G, st, forwards_host, total_forwards, conf_trace, argmax_trace, kv, refresh_every,
+                ws, lay, (hipStream_t)stream);
   API_END
 }
 

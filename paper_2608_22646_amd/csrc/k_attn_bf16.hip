@@ -38,7 +38,7 @@ __device__ __forceinline__ int v_off(int d, int chunk) {  // rows of 128 B, 8 ch
 
 __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                                                            const f16_t* __restrict__ vt, bf16_t* __restrict__ out,
-                                                           int L, int Hq, int Hkv) {
+                                                           int Lq, int L, int Hq, int Hkv) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
@@ -51,11 +51,11 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
   bf16x8_t qf[8];
   {
     const int qi = q0 + lq;
-    const bf16_t* qrow = q + (((size_t)b * Hq + h) * L + (qi < L ? qi : 0)) * HD;
+    const bf16_t* qrow = q + (((size_t)b * Hq + h) * Lq + (qi < Lq ? qi : 0)) * HD;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16 + half * 8);
-      if (qi >= L) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      if (qi >= Lq) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
     }
   }
 
@@ -174,8 +174,8 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
   const int qi = q0 + lq;
-  if (qi >= L) return;
-  bf16_t* orow = out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
+  if (qi >= Lq) return;
+  bf16_t* orow = out + ((size_t)b * Lq + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
 #pragma unroll
   for (int ds = 0; ds < 4; ++ds)
 #pragma unroll
@@ -218,7 +218,7 @@ template <int NW>
 __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* __restrict__ q,
                                                                  const bf16_t* __restrict__ k,
                                                                  const f16_t* __restrict__ vt,
-                                                                 bf16_t* __restrict__ out, int L, int Hq, int Hkv) {
+                                                                 bf16_t* __restrict__ out, int Lq, int L, int Hq, int Hkv) {
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int S = 3, PER_STAGE = 32 / NW;  // 16 K + 16 V^T DMA instructions per tile
   extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -232,11 +232,11 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
   bf16x8_t qf[8];
   {
     const int qi = q0 + lq;
-    const bf16_t* qrow = q + (((size_t)b * Hq + h) * L + (qi < L ? qi : 0)) * HD;
+    const bf16_t* qrow = q + (((size_t)b * Hq + h) * Lq + (qi < Lq ? qi : 0)) * HD;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16 + half * 8);
-      if (qi >= L) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      if (qi >= Lq) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
     }
   }
 
@@ -363,8 +363,8 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
   const int qi = q0 + lq;
-  if (qi >= L) return;
-  bf16_t* orow = out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
+  if (qi >= Lq) return;
+  bf16_t* orow = out + ((size_t)b * Lq + qi) * ((size_t)Hq * HD) + (size_t)h * HD;
 #pragma unroll
   for (int ds = 0; ds < 4; ++ds)
 #pragma unroll
@@ -397,7 +397,7 @@ template <int QG>
 __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_t* __restrict__ q,
                                                                     const bf16_t* __restrict__ k,
                                                                     const f16_t* __restrict__ vt,
-                                                                    bf16_t* __restrict__ out, int L, int Hq, int Hkv) {
+                                                                    bf16_t* __restrict__ out, int Lq, int L, int Hq, int Hkv) {
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int NW = QG * KGRP, S = 2;
   extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -451,11 +451,11 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
   bf16x8_t qf[8];
   {
     const int qi = q0 + lq;
-    const bf16_t* qrow = q + (((size_t)b * Hq + h) * L + (qi < L ? qi : 0)) * HD;
+    const bf16_t* qrow = q + (((size_t)b * Hq + h) * Lq + (qi < Lq ? qi : 0)) * HD;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16 + half * 8);
-      if (qi >= L) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      if (qi >= Lq) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
     }
   }
 
@@ -611,8 +611,8 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
 #pragma unroll
   for (int it = 0; it < 8; ++it) {
     const int row = it * 4 + (lane >> 4), ch = lane & 15, qi = q0 + row;
-    if (qi < L)
-      *reinterpret_cast<uint4*>(out + ((size_t)b * L + qi) * ((size_t)Hq * HD) + (size_t)h * HD + ch * 8) =
+    if (qi < Lq)
+      *reinterpret_cast<uint4*>(out + ((size_t)b * Lq + qi) * ((size_t)Hq * HD) + (size_t)h * HD + ch * 8) =
           *reinterpret_cast<const uint4*>(stg + row * OP + ch * 16);
   }
 #endif
@@ -620,19 +620,21 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
 
 }  // namespace
 
-void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int L, int Hq, int Hkv,
-                      hipStream_t s) {
-  if (B * L == 0) return;
+void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int Lq, int L, int Hq,
+                      int Hkv, hipStream_t s) {
+  if (B * Lq == 0) return;
   if (L % 8 == 0) {
     // streaming kernel: 8 waves (256 queries) per workgroup when that still gives
     // two or more workgroups per CU over the launch, else 4 waves; when even the
-    // 4-wave grid leaves CUs without a workgroup, the key-split kernel (four
-    // waves per query over interleaved 32-key tiles)
-    const bool wide = (long)((L + 255) / 256) * Hq * B >= 512;
+    // 4-wave grid leaves CUs without a workgroup, or there is only one 32-query
+    // group per (sequence, head), the key-split kernel (four waves per query over
+    // interleaved 32-key tiles)
+    const bool wide = (long)((Lq + 255) / 256) * Hq * B >= 512;
     const size_t lds = 3 * (size_t)STAGE;
     const long cus = device_cu_count();
-    if ((long)((L + 127) / 128) * Hq * B < cus && L > KT) {
-      // 64 queries per workgroup when that still fits the CUs, else 96
+    if (Lq <= QW || ((long)((Lq + 127) / 128) * Hq * B < cus && L > KT)) {
+      // 32 queries per workgroup for a single query group, else 64 when that
+      // still fits the CUs, else 96
       auto go = [&](auto qgc) {
         constexpr int QG = decltype(qgc)::value;
         constexpr size_t ring = 2 * (size_t)STEP2, merge = (size_t)3 * QG * 17 * 64 * 16;
@@ -640,10 +642,12 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
         static const hipError_t a = hipFuncSetAttribute((const void*)attn_kv4_kernel<QG>,
                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_kv);
         hip_check(a, "hipFuncSetAttribute(attn_kv4)");
-        hipLaunchKernelGGL(attn_kv4_kernel<QG>, dim3(ceil_div(L, QW * QG), Hq, B), dim3(64 * QG * KGRP), lds_kv, s, q,
-                           k, vt, out, L, Hq, Hkv);
+        hipLaunchKernelGGL(attn_kv4_kernel<QG>, dim3(ceil_div(Lq, QW * QG), Hq, B), dim3(64 * QG * KGRP), lds_kv, s,
+                           q, k, vt, out, Lq, L, Hq, Hkv);
       };
-      if ((long)ceil_div(L, QW * 2) * Hq * B <= cus)
+      if (Lq <= QW)
+        go(std::integral_constant<int, 1>{});
+      else if ((long)ceil_div(Lq, QW * 2) * Hq * B <= cus)
         go(std::integral_constant<int, 2>{});
       else
         go(std::integral_constant<int, 3>{});
@@ -654,14 +658,14 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
       static const hipError_t a8 =
           hipFuncSetAttribute((const void*)attn_stream_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       hip_check(a8, "hipFuncSetAttribute(attn_stream<8>)");
-      hipLaunchKernelGGL(attn_stream_kernel<8>, dim3(ceil_div(L, QW * 8), Hq, B), dim3(512), lds, s, q, k, vt, out, L,
-                         Hq, Hkv);
+      hipLaunchKernelGGL(attn_stream_kernel<8>, dim3(ceil_div(Lq, QW * 8), Hq, B), dim3(512), lds, s, q, k, vt, out,
+                         Lq, L, Hq, Hkv);
     } else {
       static const hipError_t a4 =
           hipFuncSetAttribute((const void*)attn_stream_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       hip_check(a4, "hipFuncSetAttribute(attn_stream<4>)");
-      hipLaunchKernelGGL(attn_stream_kernel<4>, dim3(ceil_div(L, QW * 4), Hq, B), dim3(256), lds, s, q, k, vt, out, L,
-                         Hq, Hkv);
+      hipLaunchKernelGGL(attn_stream_kernel<4>, dim3(ceil_div(Lq, QW * 4), Hq, B), dim3(256), lds, s, q, k, vt, out,
+                         Lq, L, Hq, Hkv);
     }
     DLLM_LAUNCH_CHECK("attn_stream");
     return;
@@ -669,8 +673,8 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)attn_bf16_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * STAGE);
   hip_check(attr, "hipFuncSetAttribute(attn_bf16)");
-  hipLaunchKernelGGL(attn_bf16_kernel, dim3(ceil_div(L, QW * NW), Hq, B), dim3(256), 2 * STAGE, s, q, k, vt, out, L,
-                     Hq, Hkv);
+  hipLaunchKernelGGL(attn_bf16_kernel, dim3(ceil_div(Lq, QW * NW), Hq, B), dim3(256), 2 * STAGE, s, q, k, vt, out, Lq,
+                     L, Hq, Hkv);
   DLLM_LAUNCH_CHECK("attn_bf16");
 }
 

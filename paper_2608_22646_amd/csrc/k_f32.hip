@@ -65,40 +65,42 @@ void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int
 // raw row m = b*L + l holds [q heads | k heads | v heads], each head hd wide.
 __global__ void rope_split_f32_kernel(const float* __restrict__ raw, const float* __restrict__ cosb,
                                       const float* __restrict__ sinb, float* __restrict__ q, float* __restrict__ k,
-                                      float* __restrict__ vt, int B, int L, int Hq, int Hkv, int hd) {
+                                      float* __restrict__ vt, int B, int Lq, int L, int pos0, int Hq, int Hkv,
+                                      int hd) {
   const int half = hd / 2;
   const int H = Hq + 2 * Hkv;
-  const long total = (long)B * L * H * half;
+  const long total = (long)B * Lq * H * half;
   const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= total) return;
   const int j = (int)(i % half);
   const int head = (int)((i / half) % H);
   const long m = i / ((long)half * H);
-  const int b = (int)(m / L), l = (int)(m % L);
+  const int b = (int)(m / Lq), l = (int)(m % Lq), pos = pos0 + l;
   const float* src = raw + m * (long)H * hd + (long)head * hd;
   const float x1 = src[j], x2 = src[j + half];
   if (head < Hq + Hkv) {
-    const float c = cosb[(size_t)l * half + j], sn = sinb[(size_t)l * half + j];
+    const float c = cosb[(size_t)pos * half + j], sn = sinb[(size_t)pos * half + j];
     const float y1 = x1 * c - x2 * sn;
     const float y2 = x2 * c + x1 * sn;
-    float* dst = head < Hq ? q + (((size_t)b * Hq + head) * L + l) * hd
-                           : k + (((size_t)b * Hkv + (head - Hq)) * L + l) * hd;
+    float* dst = head < Hq ? q + (((size_t)b * Hq + head) * Lq + l) * hd
+                           : k + (((size_t)b * Hkv + (head - Hq)) * L + pos) * hd;
     dst[j] = y1;
     dst[j + half] = y2;
   } else {
     const int hv = head - Hq - Hkv;
     float* dst = vt + ((size_t)b * Hkv + hv) * hd * L;
-    dst[(size_t)j * L + l] = x1;
-    dst[(size_t)(j + half) * L + l] = x2;
+    dst[(size_t)j * L + pos] = x1;
+    dst[(size_t)(j + half) * L + pos] = x2;
   }
 }
 
 void launch_rope_split_f32(const float* raw, const float* cosb, const float* sinb, float* q, float* k, float* vt,
-                           int B, int L, int Hq, int Hkv, int hd, hipStream_t s) {
-  const long total = (long)B * L * (Hq + 2 * Hkv) * (hd / 2);
+                           int B, int Lq, int L, int pos0, int Hq, int Hkv, int hd, hipStream_t s) {
+  const long total = (long)B * Lq * (Hq + 2 * Hkv) * (hd / 2);
   if (total == 0) return;
+  if (pos0 < 0 || pos0 + Lq > L) throw HipError("rope_split_f32: rows outside the sequence");
   hipLaunchKernelGGL(rope_split_f32_kernel, dim3(ceil_div(total, 256)), dim3(256), 0, s, raw, cosb, sinb, q, k, vt,
-                     B, L, Hq, Hkv, hd);
+                     B, Lq, L, pos0, Hq, Hkv, hd);
   DLLM_LAUNCH_CHECK("rope_split_f32");
 }
 
@@ -134,18 +136,18 @@ __device__ double block_sum128(double v, double* red) {
   return r;
 }
 
-// One 128-thread block per (query position, query head, sequence).  Scores for
-// every key are kept in LDS (dynamic, L doubles).
+// One 128-thread block per (query, query head, sequence).  Scores for every
+// key are kept in LDS (dynamic, L doubles).
 __global__ void __launch_bounds__(128) attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
-                                                       const float* __restrict__ vt, float* __restrict__ out, int L,
-                                                       int Hq, int Hkv, int hd, double scale) {
+                                                       const float* __restrict__ vt, float* __restrict__ out, int Lq,
+                                                       int L, int Hq, int Hkv, int hd, double scale) {
   extern __shared__ double smem[];
   double* qs = smem;          // [hd]
   double* sc = smem + 128;    // [L]
   __shared__ double red[2];
   const int l = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int kvh = h / (Hq / Hkv);
-  const float* qrow = q + (((size_t)b * Hq + h) * L + l) * hd;
+  const float* qrow = q + (((size_t)b * Hq + h) * Lq + l) * hd;
   const float* kh = k + ((size_t)b * Hkv + kvh) * L * hd;
   const float* vh = vt + ((size_t)b * Hkv + kvh) * hd * L;
   for (int d = threadIdx.x; d < hd; d += 128) qs[d] = qrow[d];
@@ -171,15 +173,15 @@ __global__ void __launch_bounds__(128) attn_f32_kernel(const float* __restrict__
     const float* vr = vh + (size_t)d * L;
     double o = 0.0;
     for (int j = 0; j < L; ++j) o = fma(sc[j], (double)vr[j], o);
-    out[((size_t)b * L + l) * Hq * hd + (size_t)h * hd + d] = (float)(o / sum);
+    out[((size_t)b * Lq + l) * Hq * hd + (size_t)h * hd + d] = (float)(o / sum);
   }
 }
 
-void launch_attn_f32(const float* q, const float* k, const float* vt, float* out, int B, int L, int Hq, int Hkv,
-                     int hd, hipStream_t s) {
-  if (B * L == 0) return;
+void launch_attn_f32(const float* q, const float* k, const float* vt, float* out, int B, int Lq, int L, int Hq,
+                     int Hkv, int hd, hipStream_t s) {
+  if (B * Lq == 0) return;
   const size_t lds = (128 + (size_t)L) * sizeof(double);
-  hipLaunchKernelGGL(attn_f32_kernel, dim3(L, Hq, B), dim3(128), lds, s, q, k, vt, out, L, Hq, Hkv, hd,
+  hipLaunchKernelGGL(attn_f32_kernel, dim3(Lq, Hq, B), dim3(128), lds, s, q, k, vt, out, Lq, L, Hq, Hkv, hd,
                      1.0 / sqrt((double)hd));
   DLLM_LAUNCH_CHECK("attn_f32");
 }

@@ -367,7 +367,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
   wait_vm_lds<0>();
   barrier_nofence();  // every wave is done reading the ring
 
-  const float inv_l = 1.0f / (float)g.L;
+  const float inv_l = 1.0f / (float)g.Lq;  // rows per sequence
   // with two k-groups only the first holds the finished tile; the second
   // joins the barriers and the stores
   if (wave < TL::NWT) {
@@ -385,7 +385,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
         for (int k = 0; k < 2; ++k) {
           // rows past M are staged but never stored
           const int m = min(m0 + wm * TL::WM + i * 32 + 8 * c + 4 * lhalf + e0 + k, g.M - 1);
-          pos[c][k] = seq_pos(m, g.L, inv_l).y;
+          pos[c][k] = g.pos0 + seq_pos(m, g.Lq, inv_l).y;
         }
 #pragma unroll
       for (int j = 0; j < TL::TJ; ++j) {
@@ -477,15 +477,16 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
       const bool isq = vb < nq;
       const int rel = isq ? vb : vb - nq;
       const int head = rel / HD, d0 = 16 * ((rel % HD) >> 5);
-      const int H = isq ? g.Hq : g.Hkv;
+      // q [B, Hq, Lq, hd] at row i; k [B, Hkv, L, hd] at position pos0 + i
+      const int H = isq ? g.Hq : g.Hkv, LL = isq ? g.Lq : g.L, p0 = isq ? 0 : g.pos0;
       bf16_t* dst = isq ? g.q : g.k;
       for (int it = tid; it < TL::BM * 4; it += TL::NTH) {
         const int r = it >> 2, q = it & 3, m = m0 + r;
         if (m >= g.M) continue;
-        const int2 bp = seq_pos(m, g.L, inv_l);
-        const int b = bp.x, pos = bp.y;
+        const int2 bp = seq_pos(m, g.Lq, inv_l);
+        const int b = bp.x, pos = p0 + bp.y;
         const int dim = (q < 2 ? d0 : HALF + d0) + 8 * (q & 1);
-        *reinterpret_cast<uint4*>(dst + (((size_t)b * H + head) * g.L + pos) * HD + dim) =
+        *reinterpret_cast<uint4*>(dst + (((size_t)b * H + head) * LL + pos) * HD + dim) =
             *reinterpret_cast<const uint4*>(blk + r * 64 + 16 * q);
       }
     } else {
@@ -496,10 +497,11 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
         const int c = it / RC, t = it - c * RC, m = m0 + 8 * t;
         if (m >= g.M) continue;
         const uint4 val = *reinterpret_cast<const uint4*>(blk + c * St::VROW + 16 * t);
-        if ((g.L & 7) == 0 && m + 7 < g.M) {
-          // eight positions of one sequence, 16-byte aligned (L % 8 == 0, m % 8 == 0)
-          const int2 bp = seq_pos(m, g.L, inv_l);
-          const int b = bp.x, pos = bp.y;
+        if (((g.L | g.Lq | g.pos0) & 7) == 0 && m + 7 < g.M) {
+          // eight positions of one sequence, 16-byte aligned (L, Lq, pos0 and m
+          // multiples of 8)
+          const int2 bp = seq_pos(m, g.Lq, inv_l);
+          const int b = bp.x, pos = g.pos0 + bp.y;
           *reinterpret_cast<uint4*>(g.vt + (((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos) = val;
         } else {
           const uint32_t wd[4] = {val.x, val.y, val.z, val.w};
@@ -507,8 +509,8 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
           for (int e = 0; e < 8; ++e) {
             const int mm = m + e;
             if (mm >= g.M) break;
-            const int2 bp = seq_pos(mm, g.L, inv_l);
-            const int b = bp.x, pos = bp.y;
+            const int2 bp = seq_pos(mm, g.Lq, inv_l);
+            const int b = bp.x, pos = g.pos0 + bp.y;
             g.vt[(((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos] = (f16_t)(wd[e >> 1] >> (16 * (e & 1)));
           }
         }
@@ -629,14 +631,15 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
 #endif
 }
 
-// resid[m, n] += sum_z part[z, m, n], z in order.
+// resid[m, n] += sum_z part[z, m, n], z in order (S = 0: the count ns is
+// only known at run time).
 template <int S>
-__global__ void splitk_resid_kernel(const float* __restrict__ part, float* __restrict__ resid, long MN) {
+__global__ void splitk_resid_kernel(const float* __restrict__ part, float* __restrict__ resid, long MN, int ns) {
   const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= MN) return;
   float4 acc = *reinterpret_cast<const float4*>(part + i);
 #pragma unroll
-  for (int z = 1; z < S; ++z) {
+  for (int z = 1; z < (S ? S : ns); ++z) {
     const float4 v = *reinterpret_cast<const float4*>(part + (size_t)z * MN + i);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
@@ -645,18 +648,71 @@ __global__ void splitk_resid_kernel(const float* __restrict__ part, float* __res
   *reinterpret_cast<float4*>(resid + i) = h;
 }
 
+// Split-K epilogues of the SwiGLU and q/k/v GEMMs (launches with few rows):
+// the float32 partial tiles [S, M, N] are summed in slice order, then the fused
+// epilogues' arithmetic is applied.  One thread per output (SwiGLU) or per
+// q/k rotate-half pair / v element.
+__global__ void splitk_swiglu_kernel(const float* __restrict__ part, int S, int M, int F,
+                                     bf16_t* __restrict__ out) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long)M * F) return;
+  const int m = (int)(i / F), f = (int)(i - (long)m * F);
+  const long N = 2L * F, MN = (long)M * N;
+  const long n = (long)m * N + 32 * (f >> 4) + (f & 15);  // gate column; up = n + 16
+  float gt = part[n], up = part[n + 16];
+  for (int z = 1; z < S; ++z) {
+    gt += part[z * MN + n];
+    up += part[z * MN + n + 16];
+  }
+  out[(size_t)m * F + f] = f2bf(__fdividef(gt, 1.0f + __expf(-gt)) * up);
+}
+
+__global__ void splitk_qkv_kernel(const float* __restrict__ part, int S, GemmArgs g) {
+  constexpr int HD = 128, HALF = 64;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long)g.M * g.N) return;
+  const int m = (int)(i / g.N), n = (int)(i - (long)m * g.N);
+  const int nq = g.Hq * HD, nkv = g.Hkv * HD;
+  const long MN = (long)g.M * g.N;
+  const int b = m / g.Lq, r = m - b * g.Lq, pos = g.pos0 + r;
+  auto sum = [&](int col) {
+    float a = part[(long)m * g.N + col];
+    for (int z = 1; z < S; ++z) a += part[z * MN + (long)m * g.N + col];
+    return a;
+  };
+  if (n < nq + nkv) {
+    // virtual column n (lower half of its 32-column block) holds dimension d,
+    // column n + 16 dimension d + 64 of the same head
+    const int w = n & 31;
+    if (w >= 16) return;
+    const bool isq = n < nq;
+    const int rel = isq ? n : n - nq, head = rel / HD, d = 16 * ((rel % HD) >> 5) + w;
+    const float x1 = sum(n), x2 = sum(n + 16);
+    const float c_ = g.cosb[(size_t)pos * HALF + d], s_ = g.sinb[(size_t)pos * HALF + d];
+    bf16_t* dst = isq ? g.q + (((size_t)b * g.Hq + head) * g.Lq + r) * HD : g.k + (((size_t)b * g.Hkv + head) * g.L + pos) * HD;
+    dst[d] = f2bf(x1 * c_ - x2 * s_);
+    dst[d + HALF] = f2bf(x2 * c_ + x1 * s_);
+  } else {
+    const int rel = n - nq - nkv, head = rel / HD, cj = rel % HD;
+    g.vt[(((size_t)b * g.Hkv + head) * HD + cj) * g.L + pos] = f2h(bf2f(f2bf(sum(n))));
+  }
+}
+
 struct Plan {
   int bm, bn, kg, split;
 };
 
-// Pick the tile and, for the residual GEMMs, a K split (any count up to 8; the
-// k-steps are spread as evenly as they divide), by a time model:
+// Pick the tile and a K split (any count up to 8, or 16 for launches of at most
+// 128 rows; the k-steps are spread as evenly as they divide), by a time model:
 // rounds of workgroups over the 256 compute units x k-steps per workgroup x
 // the tile's k-step time (measured on random bf16 data at M = 512: larger
 // tiles move fewer LDS bytes per flop and run two waves per SIMD), plus, for
 // the residual GEMMs, the memory time of the float32 partials (written here,
 // read back by the reduction) or of the residual's read-modify-write, at the
-// ~8 TB/s they move at (measured: much of it stays in the last-level cache).  The 192-wide
+// ~8 TB/s they move at (measured: much of it stays in the last-level cache).
+// Only residual GEMMs split at more than 128 rows; at most 128 rows (the block
+// rows of a cached step) the q/k/v and SwiGLU GEMMs split too, their epilogues
+// then running on the summed partials.  The 192-wide
 // tiles exist for the widths where 256-wide tiles leave CUs idle (batch-1
 // q/k/v and gate/up).
 Plan plan(int M, int N, int K, int epi) {
@@ -673,11 +729,12 @@ Plan plan(int M, int N, int K, int epi) {
   for (const Cand& c : cands) {
     if (N % c.bn != 0) continue;
     const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
-    for (int split = 1; split <= 8; ++split) {
-      if (split > 1 && (epi != EPI_RESID || ksteps / split < 4)) break;
+    const int max_split = M <= 128 ? 16 : 8;
+    for (int split = 1; split <= max_split; ++split) {
+      if (split > 1 && ((epi != EPI_RESID && M > 128) || ksteps / split < 4)) break;
       const long rounds = (tiles * split + 255) / 256;
       double t = (double)rounds * ((ksteps + split - 1) / split) * c.t_kstep_us;
-      if (epi == EPI_RESID) t += 8.0 * split * (double)M * N / BYTES_PER_US;
+      if (epi == EPI_RESID || split > 1) t += 8.0 * split * (double)M * N / BYTES_PER_US;
       if (t < best_t - 1e-9) {
         best_t = t;
         best = Plan{c.bm, c.bn, c.kg, split};
@@ -725,6 +782,8 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
     throw HipError("gemm_bf16: q and k/v regions must be whole 128-row heads");
   if (a.epi == EPI_QKV_ROPE && (a.M >= (1 << 24) || a.B >= (1 << 16)))
     throw HipError("gemm_bf16: q/k/v epilogue needs B * L < 2^24 and B < 2^16");
+  if (a.epi == EPI_QKV_ROPE && (a.Lq < 1 || a.pos0 < 0 || a.pos0 + a.Lq > a.L || a.M % a.Lq != 0))
+    throw HipError("gemm_bf16: q/k/v rows must be whole windows of Lq positions inside the sequence");
   const Plan p = plan(a.M, a.N, a.K, a.epi);
   switch (a.epi) {
     case EPI_QKV_ROPE: launch_epi<EPI_QKV_ROPE>(a, p, s); break;
@@ -733,13 +792,23 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
     default: throw HipError("gemm_bf16: unknown epilogue");
   }
   DLLM_LAUNCH_CHECK("gemm_bf16");
-  if (p.split > 1 && defer) {
+  if (p.split > 1 && a.epi == EPI_SWIGLU) {
+    const long n = (long)a.M * (a.N / 2);
+    hipLaunchKernelGGL(splitk_swiglu_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, a.splitk_buf, p.split, a.M,
+                       a.N / 2, a.out);
+    DLLM_LAUNCH_CHECK("splitk_swiglu");
+  } else if (p.split > 1 && a.epi == EPI_QKV_ROPE) {
+    const long n = (long)a.M * a.N;
+    hipLaunchKernelGGL(splitk_qkv_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, a.splitk_buf, p.split, a);
+    DLLM_LAUNCH_CHECK("splitk_qkv");
+  } else if (p.split > 1 && defer) {
     *defer = PendingResid{a.splitk_buf, p.split};
   } else if (p.split > 1) {
     const long MN = (long)a.M * a.N;
     const dim3 grid(ceil_div(MN / 4, 256));
     auto go = [&](auto sc) {
-      hipLaunchKernelGGL(splitk_resid_kernel<decltype(sc)::value>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN);
+      hipLaunchKernelGGL(splitk_resid_kernel<decltype(sc)::value>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN,
+                         p.split);
     };
     switch (p.split) {
       case 2: go(std::integral_constant<int, 2>{}); break;
@@ -749,7 +818,7 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
       case 6: go(std::integral_constant<int, 6>{}); break;
       case 7: go(std::integral_constant<int, 7>{}); break;
       case 8: go(std::integral_constant<int, 8>{}); break;
-      default: throw HipError("splitk_resid: split must be 2 .. 8");
+      default: go(std::integral_constant<int, 0>{}); break;  // 9 .. 16 (few rows): count at run time
     }
     DLLM_LAUNCH_CHECK("splitk_resid");
   }

@@ -5,8 +5,9 @@
 namespace dllm {
 
 // ---- k_misc.hip ------------------------------------------------------------
-// h[m, :] = float(E[x[m], :]) for m < M.
-void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int M, int d, hipStream_t s);
+// h[b*rows + i, :] = float(E[x[b*L + row0 + i], :]) for b < B, i < rows.
+void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int B, int rows, int L, int row0, int d,
+                  hipStream_t s);
 // cos/sin [L, hd/2] of pos * base^(-2j/hd), evaluated in float64, stored float32.
 void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, hipStream_t s);
 // out[b*rows + i, :] = act(RMSNorm(h[b*L + row0 + i, :]) * g) for b < B, i < rows.
@@ -21,14 +22,17 @@ void launch_state_init(const int32_t* prompt, int32_t* x, int32_t* commit_step, 
 // C[M, N] (+)= A[M, K] W[N, K]^T, all float32 row-major, C row stride ldc.
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc, bool accumulate,
                      hipStream_t s);
-// Split raw projections [B*L, (Hq + 2 Hkv) hd] into q/k (RoPE applied) and v^T.
+// Split raw projections [B*Lq, (Hq + 2 Hkv) hd] of the rows at positions pos0 ..
+// pos0 + Lq - 1 of each sequence into q [B, Hq, Lq, hd] and k [B, Hkv, L, hd]
+// (RoPE applied) and v^T [B, Hkv, hd, L] (k, v^T at those positions).
 void launch_rope_split_f32(const float* raw, const float* cosb, const float* sinb, float* q, float* k,
-                           float* vt, int B, int L, int Hq, int Hkv, int hd, hipStream_t s);
+                           float* vt, int B, int Lq, int L, int pos0, int Hq, int Hkv, int hd, hipStream_t s);
 // out[i] = silu(gate[i]) * up[i]
 void launch_swiglu_f32(const float* gate, const float* up, float* out, long n, hipStream_t s);
-// Non-causal attention, float32: out[b*L + l, h*hd + j].
-void launch_attn_f32(const float* q, const float* k, const float* vt, float* out, int B, int L, int Hq, int Hkv,
-                     int hd, hipStream_t s);
+// Non-causal attention, float32, of Lq queries per sequence (q [B, Hq, Lq, hd])
+// over L keys (k [B, Hkv, L, hd], v^T [B, Hkv, hd, L]): out[b*Lq + l, h*hd + j].
+void launch_attn_f32(const float* q, const float* k, const float* vt, float* out, int B, int Lq, int L, int Hq,
+                     int Hkv, int hd, hipStream_t s);
 // Per row of logits [R, V]: conf = 1 / sum exp(l - max), argmax (lowest index), mask_id excluded.
 void launch_vocab_reduce_f32(const float* logits, int R, int V, int mask_id, float* conf, int32_t* argmax,
                              hipStream_t s);
@@ -49,7 +53,10 @@ struct GemmArgs {
   bf16_t* out;              // EPI_SWIGLU: [M, N/2]; EPI_STORE: [M, N]
   bf16_t* q; bf16_t* k; f16_t* vt;   // EPI_QKV_ROPE (v^T holds the bf16 values as IEEE half)
   const float* cosb; const float* sinb;
-  int B, L, Hq, Hkv;
+  // EPI_QKV_ROPE: row m = b Lq + i holds position pos0 + i of sequence b; q is
+  // [B, Hq, Lq, hd], k [B, Hkv, L, hd] and v^T [B, Hkv, hd, L] are written at
+  // that position (a full forward: Lq = L, pos0 = 0)
+  int B, L, Hq, Hkv, Lq, pos0;
   // split-K scratch (float32 partials [split, M, N]) from the workspace
   float* splitk_buf;
 };
@@ -72,7 +79,10 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
 // Bytes of split-K scratch a launch of this shape needs (0 if it does not split).
 size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi);
 
-void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int L, int Hq,
+// Non-causal attention of Lq queries per sequence (q [B, Hq, Lq, 128]) over L
+// keys (k [B, Hkv, L, 128], v^T [B, Hkv, 128, L] as IEEE half):
+// out[b*Lq + l, h*128 + j] (bf16).
+void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int Lq, int L, int Hq,
                       int Hkv, hipStream_t s);
 
 // The bf16 LM head is read from a tiled copy: vocabulary tiles of HEAD_TILE rows,

@@ -150,3 +150,91 @@ def check_head(model, cfg, wnp, ws, B, L, row0, rows, sample=None):
     assert np.abs(cg - conf_self).max() <= 1e-5
     assert np.array_equal(ag, arg_self)
     return dict(hb_flips=fa, logit_err=float(err.max()), conf_err=float(cerr), argmax_diff=int(diff.sum()))
+
+
+def kv_views(model, kv, B, L, l):
+    """Layer l's cache entries: keys [B, Hkv, L, hd] and values^T [B, Hkv, hd, L]
+    (bf16 keys, IEEE-half values for a bf16 model; float32 for fp32)."""
+    cfg = model.cfg
+    es = 2 if cfg.dtype == "bf16" else 4
+    n = B * cfg.n_kv_heads * L * cfg.head_dim
+    S = (n * es + 255) // 256 * 256
+    kd, vd = (torch.bfloat16, torch.float16) if cfg.dtype == "bf16" else (torch.float32, torch.float32)
+    base = l * 2 * S
+    K = kv[base:base + n * es].view(kd).view(B, cfg.n_kv_heads, L, cfg.head_dim)
+    V = kv[base + S:base + S + n * es].view(vd).view(B, cfg.n_kv_heads, cfg.head_dim, L)
+    return K, V
+
+
+def check_layer_cached(model, cfg, wnp, ws, kv, B, L, row0, Lq, l, stats=None):
+    """Run layer l of a cached step (rows row0 .. row0 + Lq - 1 of each sequence,
+    keys/values of the other positions from the cache) on the GPU and check every
+    stage against the oracle on the GPU's own stage inputs, including that the
+    cache changes at the block positions only."""
+    lay = model.layout(B, L, Lq)
+    d, H, Hkv, hd, F = cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d_ff
+    M = B * Lq
+    an, wq, wk, wv, wo, mn, wg, wu, wd = layer_weights(wnp, l)
+    cos, sin = of.rope_tables(L, hd, cfg.rope_base)
+    pos = row0 + np.arange(Lq)
+    stats = stats if stats is not None else {}
+    Kc, Vc = kv_views(model, kv, B, L, l)
+    k_before, v_before = to_np(Kc, np.float64), to_np(Vc, np.float64)
+
+    h_in = read(ws, lay.h, torch.float32, (M, d))
+    model.layer_kv(l, 0, B, L, row0, Lq, kv, ws)
+    torch.cuda.synchronize()
+    a = read(ws, lay.a_attn, torch.bfloat16, (M, d))
+    q = read(ws, lay.q, torch.bfloat16, (B, H, Lq, hd))
+    K, V = to_np(Kc, np.float64), to_np(Vc, np.float64)
+    attn = read(ws, lay.attn, torch.bfloat16, (M, H * hd))
+    h_mid = read(ws, lay.h, torch.float32, (M, d))
+    model.layer_kv(l, 1, B, L, row0, Lq, kv, ws)
+    torch.cuda.synchronize()
+    a2 = read(ws, lay.a_mlp, torch.bfloat16, (M, d))
+    u = read(ws, lay.u, torch.bfloat16, (M, F))
+    h_out = read(ws, lay.h, torch.float32, (M, d))
+
+    stats["a_attn"] = assert_bf16_flips(a, of.norm_in(h_in, an, cfg.rms_eps, "bf16"), f"L{l} a_attn")
+    out = np.ones(L, dtype=bool)
+    out[pos] = False
+    assert np.array_equal(K[:, :, out], k_before[:, :, out]), f"L{l}: cached keys outside the block changed"
+    assert np.array_equal(V[:, :, :, out], v_before[:, :, :, out]), f"L{l}: cached values outside the block changed"
+    qr, kr, vr = [], [], []
+    for b in range(B):
+        q_ref, k_ref, v_ref = of.qkv_rope(cfg, a[b * Lq:(b + 1) * Lq], wq, wk, wv, cos[pos], sin[pos], "bf16")
+        qr.append((q[b], q_ref))
+        kr.append((K[b][:, pos], k_ref))
+        vr.append((V[b][:, :, pos].transpose(0, 2, 1), v_ref))
+    for name, pairs in (("q", qr), ("k", kr), ("v", vr)):
+        stats[name] = assert_bf16_flips(np.concatenate([g for g, _ in pairs], 1),
+                                        np.concatenate([r for _, r in pairs], 1), f"L{l} {name}")
+    # attention of the block queries over every cached position (bound as in check_layer)
+    o_ref = np.empty_like(attn)
+    bound = np.empty_like(attn)
+    scale = 1.0 / np.sqrt(hd)
+    grp = H // Hkv
+    for b in range(B):
+        vf = V[b].transpose(0, 2, 1)
+        sel = slice(b * Lq, (b + 1) * Lq)
+        o_ref[sel] = of.attn_out(q[b], K[b], vf, "bf16")
+        for hh in range(H):
+            p = of.softmax(q[b][hh] @ K[b][hh // grp].T * scale)
+            bound[sel, hh * hd:(hh + 1) * hd] = 2.0 ** -11 * (p @ np.abs(vf[hh // grp]))
+    d_att = np.abs(attn - o_ref)
+    lim = bound + 1.0001 * np.maximum(bf16_ulp(o_ref), bf16_ulp(attn)) + 1e-6
+    assert np.all(d_att <= lim), f"L{l} attn: {int((d_att > lim).sum())} beyond the bound; max {d_att.max():.3g}"
+    stats["attn"] = float(np.mean(d_att > 0))
+    for name, got, ref in (("h_mid", h_mid, of.residual(h_in, attn, wo, "bf16")),):
+        sc = np.abs(ref).max() + 1.0
+        err = np.abs(got - ref).max()
+        assert err <= 2e-5 * sc, f"L{l} {name} err {err:.3g} (scale {sc:.3g})"
+        stats[name] = err / sc
+    stats["a_mlp"] = assert_bf16_flips(a2, of.norm_in(h_mid, mn, cfg.rms_eps, "bf16"), f"L{l} a_mlp")
+    stats["u"] = assert_bf16_flips(u, of.swiglu(a2, wg, wu, "bf16"), f"L{l} u")
+    ho_ref = of.residual(h_mid, u, wd, "bf16")
+    sc = np.abs(ho_ref).max() + 1.0
+    err = np.abs(h_out - ho_ref).max()
+    assert err <= 2e-5 * sc, f"L{l} h_out err {err:.3g} (scale {sc:.3g})"
+    stats["h_out"] = err / sc
+    return stats
