@@ -218,6 +218,79 @@ def sweep_gen(args):
                       "lengths": rows}), flush=True)
 
 
+# update frequency of the KV cache in the paper's runs (Section 5): 16 for LLaDA, 8 for Dream
+KV_REFRESH = {"llada": 16, "dream": 8}
+
+
+def kv_reuse(args):
+    """Decode throughput with cross-step key/value reuse (the cache refreshed at
+    local steps t % R == 0, block-row forwards otherwise), and the time of one
+    refresh forward and one cached forward.  A cached forward streams every
+    weight once (plus the cache), so its roofline is HBM bandwidth."""
+    import torch
+    from paper_2608_22646_amd import binding as Bd
+    from paper_2608_22646_amd import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    cfg = wl.model
+    B, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
+    L = P + G
+    R = args.kv_reuse or KV_REFRESH["dream" if cfg.name.startswith("dream") else "llada"]
+    log(f"kv reuse: workload {wl.name}, refresh every {R} steps")
+    weights = synth.make_weights(cfg, "cuda")
+    model = Bd.Model(cfg, weights)
+    prompts = synth.make_prompts(wl, "cuda")
+    ctl = Bd.Controller.gating(wl.gating, block_len=bl)
+    ws = model.workspace(B, L, bl)
+    kv = model.kv_cache(B, L)
+    st = Bd.DecodeState(B, P, G, "cuda")
+    for i in range(args.warmup):
+        res = model.generate_kv(ctl, prompts, G, R, ws=ws, st=st, kv=kv)
+        log(f"warmup {i}: forwards {res.total_forwards} {res.forwards}")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    total_fwd = 0
+    for _ in range(args.steps):
+        res = model.generate_kv(ctl, prompts, G, R, ws=ws, st=st, kv=kv)
+        total_fwd += res.total_forwards
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    refreshes = sum((n + R - 1) // R for n in res.forwards)
+    # one refresh and one cached forward of the decoded sequence, timed on the stream with events
+    x = st.x
+    s = torch.cuda.current_stream()
+    times = {}
+    for name, refresh in (("refresh", True), ("cached", False)):
+        model.forward_kv(x, P, bl, kv, refresh, ws=ws)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        n = 10
+        ev[0].record(s)
+        for _ in range(n):
+            model.forward_kv(x, P, bl, kv, refresh, ws=ws)
+        ev[1].record(s)
+        torch.cuda.synchronize()
+        times[name] = ev[0].elapsed_time(ev[1]) / n
+    es = 2 if cfg.dtype == "bf16" else 4
+    weight_bytes = sum(w.numel() * w.element_size() for w in weights[1:])        # embedding rows aside
+    cache_bytes = cfg.n_layers * 2 * B * cfg.n_kv_heads * L * cfg.head_dim * es
+    cached_bytes = weight_bytes + cache_bytes
+    gbs = cached_bytes / (times["cached"] * 1e-3) / 1e9
+    out = {
+        "metric": f"generated tokens/s with cross-step KV reuse (refresh every {R} steps)",
+        "value": B * G * args.steps / dt, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": dt / args.steps * 1e3, "higher_is_better": True,
+        "dtype": cfg.dtype, "data": "synthetic (seeded random-init weights of the model shape, uniform random prompts)",
+        "config": {"workload": f"{wl.name}: {cfg.name} random-init, batch {B}, prompt {P}, gen {G}, block {bl}, "
+                               f"gating {'on' if wl.gating else 'off'}, KV cache refreshed every {R} steps"},
+        "forwards_per_decode": total_fwd / args.steps, "refresh_forwards_per_decode": refreshes,
+        "refresh_forward_ms": times["refresh"], "cached_forward_ms": times["cached"],
+        "roofline": {"bound": "hbm", "kernel": "cached forward (every weight streamed once + the cache read)",
+                     "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                     "bytes_per_forward": cached_bytes},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -233,6 +306,9 @@ def main():
     ap.add_argument("--ablation", action="store_true",
                     help="decode the workload under each controller preset (component ablation, fixed-threshold "
                          "decoding, fixed-schedule baseline) and print one JSON line of forwards and tokens/s")
+    ap.add_argument("--kv-reuse", type=int, nargs="?", const=0, default=None, metavar="R",
+                    help="decode with cross-step key/value reuse, the cache refreshed every R steps (default: the "
+                         "paper's 16 for LLaDA, 8 for Dream) and print one JSON line of tokens/s")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -247,6 +323,9 @@ def main():
         return
     if args.sweep_gen:
         sweep_gen(args)
+        return
+    if args.kv_reuse is not None:
+        kv_reuse(args)
         return
 
     import torch

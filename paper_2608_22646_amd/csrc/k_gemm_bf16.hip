@@ -100,6 +100,10 @@ using TileM = Tile<256, 192, 4, 2, 2>;
 using TileSM = Tile<128, 192, 2, 2, 3>;
 // the same on 8 waves in two k-groups
 using TileSM2 = Tile<128, 192, 2, 2, 3, 2>;
+// 64 x 256, 8 waves of 64 x 64 in two k-groups: launches of a
+// few dozen rows (a cached step's block rows), where the weights' HBM stream
+// bounds the time and taller tiles only add MFMA and LDS work on padding rows
+using TileT = Tile<64, 256, 1, 4, 4, 2>;  // four stages: three k-steps of weights in flight
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -631,15 +635,14 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
 #endif
 }
 
-// resid[m, n] += sum_z part[z, m, n], z in order (S = 0: the count ns is
-// only known at run time).
+// resid[m, n] += sum_z part[z, m, n], z in order.
 template <int S>
-__global__ void splitk_resid_kernel(const float* __restrict__ part, float* __restrict__ resid, long MN, int ns) {
+__global__ void splitk_resid_kernel(const float* __restrict__ part, float* __restrict__ resid, long MN) {
   const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= MN) return;
   float4 acc = *reinterpret_cast<const float4*>(part + i);
 #pragma unroll
-  for (int z = 1; z < (S ? S : ns); ++z) {
+  for (int z = 1; z < S; ++z) {
     const float4 v = *reinterpret_cast<const float4*>(part + (size_t)z * MN + i);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
@@ -712,7 +715,8 @@ struct Plan {
 // ~8 TB/s they move at (measured: much of it stays in the last-level cache).
 // Only residual GEMMs split at more than 128 rows; at most 128 rows (the block
 // rows of a cached step) the q/k/v and SwiGLU GEMMs split too, their epilogues
-// then running on the summed partials.  The 192-wide
+// then running on the summed partials, and the 64-row tile is a candidate.  A
+// launch is also bounded by streaming its weights from HBM once.  The 192-wide
 // tiles exist for the widths where 256-wide tiles leave CUs idle (batch-1
 // q/k/v and gate/up).
 Plan plan(int M, int N, int K, int epi) {
@@ -721,19 +725,27 @@ Plan plan(int M, int N, int K, int epi) {
     double t_kstep_us;
   };
   const Cand cands[] = {{128, 256, 1, 1.04}, {256, 256, 1, 1.71}, {256, 192, 1, 1.37}, {128, 192, 1, 0.87},
-                        {128, 192, 2, 0.81}};
+                        {128, 192, 2, 0.81}, {64, 256, 2, 0.55}};
   constexpr double BYTES_PER_US = 8.0e6;
+  // the weights stream from HBM once per launch (tiles of one N range share
+  // them through L2) at ~6.5 TB/s when every CU has a workgroup
+  constexpr double W_BYTES_PER_US = 6.5e6;
   Plan best{0, 0, 0, 0};
   double best_t = 1e30;
   const int ksteps = K / BK;
   for (const Cand& c : cands) {
-    if (N % c.bn != 0) continue;
+    if (N % c.bn != 0 || (c.bm == 64 && M > 128)) continue;
     const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
     const int max_split = M <= 128 ? 16 : 8;
     for (int split = 1; split <= max_split; ++split) {
       if (split > 1 && ((epi != EPI_RESID && M > 128) || ksteps / split < 4)) break;
       const long rounds = (tiles * split + 255) / 256;
-      double t = (double)rounds * ((ksteps + split - 1) / split) * c.t_kstep_us;
+      const double t_mma = (double)rounds * ((ksteps + split - 1) / split) * c.t_kstep_us;
+      const double t_w = 2.0 * N * K / (W_BYTES_PER_US * std::min(1.0, (double)(tiles * split) / 256));
+      // at a few dozen rows the weight stream bounds every tile; the tile's own
+      // k-step time still shows through (only partly hidden under the stream)
+      double t = std::max(t_mma, t_w);
+      if (M <= 128) t += 0.25 * std::min(t_mma, t_w);
       if (epi == EPI_RESID || split > 1) t += 8.0 * split * (double)M * N / BYTES_PER_US;
       if (t < best_t - 1e-9) {
         best_t = t;
@@ -757,7 +769,9 @@ void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
 
 template <int EPI>
 void launch_epi(const GemmArgs& g, const Plan& p, hipStream_t s) {
-  if (p.bm == 256 && p.bn == 256)
+  if (p.bm == 64)
+    launch_tile<TileT, EPI>(g, p.split, s);
+  else if (p.bm == 256 && p.bn == 256)
     launch_tile<TileL, EPI>(g, p.split, s);
   else if (p.bm == 256)
     launch_tile<TileM, EPI>(g, p.split, s);
@@ -801,14 +815,15 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
     const long n = (long)a.M * a.N;
     hipLaunchKernelGGL(splitk_qkv_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, a.splitk_buf, p.split, a);
     DLLM_LAUNCH_CHECK("splitk_qkv");
-  } else if (p.split > 1 && defer) {
+  } else if (p.split > 1 && defer && a.M > 128) {
+    // few rows (M <= 128) are reduced right away across the whole chip: the
+    // fused reduce + norm runs one workgroup per row
     *defer = PendingResid{a.splitk_buf, p.split};
   } else if (p.split > 1) {
     const long MN = (long)a.M * a.N;
     const dim3 grid(ceil_div(MN / 4, 256));
     auto go = [&](auto sc) {
-      hipLaunchKernelGGL(splitk_resid_kernel<decltype(sc)::value>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN,
-                         p.split);
+      hipLaunchKernelGGL(splitk_resid_kernel<decltype(sc)::value>, grid, dim3(256), 0, s, a.splitk_buf, a.resid, MN);
     };
     switch (p.split) {
       case 2: go(std::integral_constant<int, 2>{}); break;
@@ -818,7 +833,15 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
       case 6: go(std::integral_constant<int, 6>{}); break;
       case 7: go(std::integral_constant<int, 7>{}); break;
       case 8: go(std::integral_constant<int, 8>{}); break;
-      default: go(std::integral_constant<int, 0>{}); break;  // 9 .. 16 (few rows): count at run time
+      case 9: go(std::integral_constant<int, 9>{}); break;
+      case 10: go(std::integral_constant<int, 10>{}); break;
+      case 11: go(std::integral_constant<int, 11>{}); break;
+      case 12: go(std::integral_constant<int, 12>{}); break;
+      case 13: go(std::integral_constant<int, 13>{}); break;
+      case 14: go(std::integral_constant<int, 14>{}); break;
+      case 15: go(std::integral_constant<int, 15>{}); break;
+      case 16: go(std::integral_constant<int, 16>{}); break;
+      default: throw HipError("splitk_resid: split must be 2 .. 16");
     }
     DLLM_LAUNCH_CHECK("splitk_resid");
   }

@@ -164,11 +164,10 @@ void launch_rmsnorm_t(const float* h, const TG* g, TO* out, int B, int rows, int
 
 // rmsnorm_vec_kernel preceded by the split-K residual update of its row: each
 // float4 of the row is h + ((p_0 + p_1) + ... + p_{S-1}), the same operations in
-// the same order as splitk_resid_kernel, written back to h and kept for the norm
-// (S = 0: the split count ns is only known at run time).
+// the same order as splitk_resid_kernel, written back to h and kept for the norm.
 template <int NV, int S>
 __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ part,
-                                                            long MN, int ns, const bf16_t* __restrict__ g,
+                                                            long MN, const bf16_t* __restrict__ g,
                                                             bf16_t* __restrict__ out, int d, float eps) {
   const int r = blockIdx.x;
   float* row = h + (size_t)r * d;
@@ -182,7 +181,7 @@ __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ 
       const size_t i = (size_t)r * d4 + c;
       float4 acc = reinterpret_cast<const float4*>(part)[i];
 #pragma unroll
-      for (int z = 1; z < (S ? S : ns); ++z) {
+      for (int z = 1; z < S; ++z) {
         const float4 p = reinterpret_cast<const float4*>(part + (size_t)z * MN)[i];
         acc.x += p.x;
         acc.y += p.y;
@@ -228,7 +227,7 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
   // the split count is a template parameter so that every partial's loads are in flight at once
   auto go = [&](auto nvc, auto sc) {
     hipLaunchKernelGGL((resid_rmsnorm_kernel<decltype(nvc)::value, decltype(sc)::value>), dim3(M), dim3(256), 0, s, h,
-                       pend.part, MN, pend.split, g, out, d, eps);
+                       pend.part, MN, g, out, d, eps);
   };
   auto by_split = [&](auto nvc) {
     switch (pend.split) {
@@ -239,10 +238,7 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
       case 6: go(nvc, std::integral_constant<int, 6>{}); break;
       case 7: go(nvc, std::integral_constant<int, 7>{}); break;
       case 8: go(nvc, std::integral_constant<int, 8>{}); break;
-      default:
-        if (pend.split < 2 || pend.split > 16) throw HipError("resid_rmsnorm: split must be 2 .. 16");
-        go(nvc, std::integral_constant<int, 0>{});  // few rows: count at run time
-        break;
+      default: throw HipError("resid_rmsnorm: split must be 2 .. 8");
     }
   };
   if (nv <= 2)

@@ -67,8 +67,9 @@ struct PendingResid {
   const float* part = nullptr;  // [split, M, N] float32
   int split = 0;
 };
-// With defer non-null, a split-K residual GEMM leaves its partials pending
-// there instead of launching the reduction (defer->split = 0 otherwise).
+// With defer non-null, a split-K residual GEMM of more than 128 rows leaves its
+// partials pending there instead of launching the reduction (defer->split = 0
+// otherwise).
 void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer = nullptr);
 // Completes a deferred residual update and normalises in one pass, for every
 // row m < M (bf16 model, d % 4 == 0, d <= 8192):
