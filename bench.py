@@ -1,11 +1,14 @@
 #!/usr/bin/env python3
 """Throughput of the CAI-dLLM decode on one MI355X.
 
-One bench step = one dllm_generate of the workload: the prompt batch is decoded
+One bench step = one dllm_generate of the workload: a prompt batch is decoded
 block by block with the confidence-aware controller, every denoising step
 running the full bidirectional forward, the fused LM-head reduction and the
-commit kernel.  Inputs (random-init weights of the model's shape, seeded
-prompts) are resident in HBM before timing starts.
+commit kernel.  Step i decodes the i-th seeded prompt set (step 0: the
+workload's own prompts), so tokens/s averages the number of denoising steps
+over prompts, as a throughput over a benchmark does.  Inputs (random-init
+weights of the model's shape, seeded prompts) are resident in HBM before
+timing starts.
 
 Prints one JSON line: generated tokens/s, the dominant kernel's roofline
 (gate/up GEMM, bf16 MFMA, timed with HIP events on its launch stream inside the
@@ -244,18 +247,19 @@ def kv_reuse(args):
     ws = model.workspace(B, L, bl)
     kv = model.kv_cache(B, L)
     st = Bd.DecodeState(B, P, G, "cuda")
+    prompt_sets = [synth.make_prompts(wl, "cuda", first=i * B) for i in range(args.steps)]
     for i in range(args.warmup):
         res = model.generate_kv(ctl, prompts, G, R, ws=ws, st=st, kv=kv)
         log(f"warmup {i}: forwards {res.total_forwards} {res.forwards}")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    total_fwd = 0
-    for _ in range(args.steps):
-        res = model.generate_kv(ctl, prompts, G, R, ws=ws, st=st, kv=kv)
+    total_fwd = refreshes = 0
+    for i in range(args.steps):
+        res = model.generate_kv(ctl, prompt_sets[i], G, R, ws=ws, st=st, kv=kv)
         total_fwd += res.total_forwards
+        refreshes += sum((n + R - 1) // R for n in res.forwards)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    refreshes = sum((n + R - 1) // R for n in res.forwards)
     # one refresh and one cached forward of the decoded sequence, timed on the stream with events
     x = st.x
     s = torch.cuda.current_stream()
@@ -282,7 +286,7 @@ def kv_reuse(args):
         "dtype": cfg.dtype, "data": "synthetic (seeded random-init weights of the model shape, uniform random prompts)",
         "config": {"workload": f"{wl.name}: {cfg.name} random-init, batch {B}, prompt {P}, gen {G}, block {bl}, "
                                f"gating {'on' if wl.gating else 'off'}, KV cache refreshed every {R} steps"},
-        "forwards_per_decode": total_fwd / args.steps, "refresh_forwards_per_decode": refreshes,
+        "forwards_per_decode": total_fwd / args.steps, "refresh_forwards_per_decode": refreshes / args.steps,
         "refresh_forward_ms": times["refresh"], "cached_forward_ms": times["cached"],
         "roofline": {"bound": "hbm", "kernel": "cached forward (every weight streamed once + the cache read)",
                      "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
@@ -294,7 +298,7 @@ def kv_reuse(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="llada_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -344,6 +348,7 @@ def main():
     log(f"weights ready ({cfg.param_count() / 1e9:.2f} B params, {time.perf_counter() - t0:.1f} s)")
     model = Bd.Model(cfg, weights)
     prompts = synth.make_prompts(wl, dev)
+    prompt_sets = [synth.make_prompts(wl, dev, first=i * B) for i in range(args.steps)]
     ctl = Bd.Controller.gating(wl.gating, block_len=bl)
     ws = model.workspace(B, L, bl)
     st = Bd.DecodeState(B, P, G, dev)
@@ -358,11 +363,14 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     total_fwd = 0
-    for _ in range(args.steps):
-        res = model.generate(ctl, prompts, G, ws=ws, st=st)
+    fwd_each = []
+    for i in range(args.steps):
+        res = model.generate(ctl, prompt_sets[i], G, ws=ws, st=st)
         total_fwd += res.total_forwards
+        fwd_each.append(res.total_forwards)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    log(f"forwards per decode of the {args.steps} prompt sets: {fwd_each}")
     gu_ms, gu_n = model.prof_read(Bd.PROF_GATEUP)
     model.prof_enable([])
 
@@ -396,6 +404,7 @@ def main():
     breakdown["gemm_qkv_o_down"]["mfma_frac"] = None
     extra = {
         "forwards_per_decode": fwd_per_gen,
+        "forwards_per_prompt_set": fwd_each,
         "denoising_steps_per_s": total_fwd / dt,
         "forward_gemm_mfma_frac": gemm_flops / gemm_s / 1e12 / BF16_PEAK_TFLOPS,
         "forward_attention_mfma_frac": attn_flops / attn_s / 1e12 / BF16_PEAK_TFLOPS,
@@ -427,7 +436,7 @@ def main():
         "config": {"workload": f"{wl.name}: {cfg.name} random-init, batch {B}, prompt {P}, gen {G}, "
                                f"block {bl}, gating {'on' if wl.gating else 'off'}",
                    "batch": B, "prompt_len": P, "gen_len": G, "block_len": bl,
-                   "parallelism": "single GPU"},
+                   "prompt_sets": args.steps, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "gate/up GEMM + SwiGLU (gemm_bf16_kernel, EPI_SWIGLU)",
                      "achieved": gu_tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": gu_tflops / BF16_PEAK_TFLOPS, "traffic": measured_traffic(),

@@ -134,12 +134,13 @@ def make_weights(cfg: ModelConfig, device="cpu"):
     return out
 
 
-def make_prompts(wl: Workload, device="cpu"):
-    """int32 [B, P]: sequence b drawn uniformly from [0, vocab-2] with seed 0 + b."""
+def make_prompts(wl: Workload, device="cpu", first=0):
+    """int32 [B, P]: sequence b drawn uniformly from [0, vocab-2] with seed first + b
+    (first = 0: the workload's prompts; other values give further prompt sets)."""
     rows = []
     for b in range(wl.batch):
         g = torch.Generator(device="cpu")
-        g.manual_seed(PROMPT_SEED_BASE + b)
+        g.manual_seed(PROMPT_SEED_BASE + first + b)
         rows.append(torch.randint(0, wl.model.vocab - 1, (wl.prompt_len,), generator=g, dtype=torch.int64))
     return torch.stack(rows).to(torch.int32).to(device)
 

@@ -178,10 +178,12 @@ def small():
     return B.Model(SMALL, [w.to("cuda") for w in w_cpu]), [w.to(torch.float32).numpy() for w in w_cpu]
 
 
-@pytest.mark.parametrize("Bn,P,G,blk", [(2, 40, 64, 1), (1, 36, 96, 0)])
+@pytest.mark.parametrize("Bn,P,G,blk", [(2, 40, 64, 1), (1, 36, 96, 0), (5, 40, 64, 1), (5, 36, 96, 2)])
 def test_bf16_refresh_cache_and_cached_layer_stages(small, Bn, P, G, blk):
-    """P = 36: block positions not a multiple of 8 (the q/k/v epilogue's
-    element-wise v^T path)."""
+    """Up to 128 block rows the q/k/v and SwiGLU GEMMs split K and run their
+    epilogues on the summed partials; B = 5 (160 rows) runs the fused
+    epilogues on the row window.  P = 36: block positions not a multiple of 8
+    (the element-wise v^T path)."""
     model, wnp = small
     L, bl = P + G, 32
     row0 = P + blk * bl
