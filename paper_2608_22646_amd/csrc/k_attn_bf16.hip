@@ -23,6 +23,13 @@ namespace dllm {
 namespace {
 
 constexpr int HD = 128, KT = 64, QW = 32, NW = 4;
+
+// 2^x by the hardware instruction alone (v_exp_f32), without libm's rescaling
+// for results below 2^-126: every argument here is a score minus a running
+// maximum (so <= 8) whose result feeds a probability held in IEEE half or a
+// sum that is at least 1, where values below 2^-126 are zero anyway.  exp2f
+// spends five more VALU instructions per element on that rescaling.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 constexpr int K_BYTES = KT * HD * 2, V_BYTES = HD * KT * 2, STAGE = K_BYTES + V_BYTES;
 
 // XOR swizzles sized for the 64 banks (256 bytes) that one 16-lane pass of
@@ -132,14 +139,14 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
       }
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
     const float m_new = fmaxf(m_run, mt);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = exp2_hw(m_run - m_new);
     m_run = m_new;
     float psum = 0.f;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[st][r] - m_new);
+        const float p = exp2_hw(s[st][r] - m_new);
         s[st][r] = p;
         psum += p;
       }
@@ -323,7 +330,7 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
     // raise the running maximum only when it grows by more than 2^8
     if (__ballot(mt > m_run + 8.0f) != 0ull) {
       const float m_new = fmaxf(m_run, mt);
-      const float alpha = exp2f(m_run - m_new);
+      const float alpha = exp2_hw(m_run - m_new);
       m_run = m_new;
       l_run *= alpha;
 #pragma unroll
@@ -336,7 +343,7 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(fmaf(s2[st][r], sc, -m_run));
+        const float p = exp2_hw(fmaf(s2[st][r], sc, -m_run));
         s2[st][r] = p;
         psum += p;
       }
@@ -503,7 +510,7 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sc;
     if (__ballot(mt > m_run + 8.0f) != 0ull) {
       const float m_new = fmaxf(m_run, mt);
-      const float alpha = exp2f(m_run - m_new);
+      const float alpha = exp2_hw(m_run - m_new);
       m_run = m_new;
       l_run *= alpha;
 #pragma unroll
@@ -514,7 +521,7 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
     float psum = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float p = exp2f(fmaf(s2[r], sc, -m_run));
+      const float p = exp2_hw(fmaf(s2[r], sc, -m_run));
       s2[r] = p;
       psum += p;
     }
@@ -566,7 +573,7 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
       m = fmaxf(m, ml.x);
     }
     // a group that saw no key (m = -inf) contributes nothing
-    const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - m);
+    const float a0 = m_run == -INFINITY ? 0.f : exp2_hw(m_run - m);
     l_run *= a0;
 #pragma unroll
     for (int ds = 0; ds < 4; ++ds)
@@ -575,7 +582,7 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
 #pragma unroll
     for (int e = 1; e < KGRP; ++e) {
       const float4* xe = x4 + (size_t)(qg + QG * (e - 1)) * (XW / 4);
-      const float ae = me[e - 1] == -INFINITY ? 0.f : exp2f(me[e - 1] - m);
+      const float ae = me[e - 1] == -INFINITY ? 0.f : exp2_hw(me[e - 1] - m);
       l_run += le[e - 1] * ae;
 #pragma unroll
       for (int ds = 0; ds < 4; ++ds)
