@@ -242,6 +242,8 @@ def kv_reuse(args):
     log(f"kv reuse: workload {wl.name}, refresh every {R} steps")
     weights = synth.make_weights(cfg, "cuda")
     model = Bd.Model(cfg, weights)
+    if cfg.dtype == "bf16":
+        model.pack_weights()        # tiled copies streamed by the block-row GEMMs
     prompts = synth.make_prompts(wl, "cuda")
     ctl = Bd.Controller.gating(wl.gating, block_len=bl)
     ws = model.workspace(B, L, bl)

@@ -166,6 +166,19 @@ int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int
 int dllm_model_destroy(dllm_model* model);
 
 /*
+ * Optional, bf16 models: make copies of every layer's q/k/v, output, gate/up
+ * and down weights in the tiled MFMA-operand order of the LM head's copy
+ * (each 256-row x 64-k block one contiguous 32 KiB run), owned by the handle
+ * and freed by dllm_model_destroy (device memory about the size of those
+ * weights: ~14 GB for the LLaDA-8B shape).  GEMMs of at most 128 rows -- the
+ * block rows of a cached step (dllm_forward_kv and friends) -- then stream
+ * these runs instead of the row-major tensors; results are bit-identical.  As
+ * with the LM head copy, later writes to the caller's weights are not seen.
+ * A second call does nothing.  Errors: DLLM_EUNSUPPORTED (fp32 model), DLLM_EHIP.
+ */
+int dllm_model_pack_weights(dllm_model* model);
+
+/*
  * Bytes of workspace needed by dllm_forward / dllm_step / dllm_generate for
  * B sequences of length L whose LM head runs on `rows` positions per sequence
  * (the block length for a step).

@@ -63,6 +63,7 @@ _SIGS = {
     "dllm_last_error": (_c.c_char_p, []),
     "dllm_model_create": (_i32, [_c.POINTER(ModelCfg), _c.POINTER(_vp), _i32, _c.POINTER(_vp)]),
     "dllm_model_destroy": (_i32, [_vp]),
+    "dllm_model_pack_weights": (_i32, [_vp]),
     "dllm_workspace_size": (_i32, [_vp, _i32, _i32, _i32, _c.POINTER(_sz)]),
     "dllm_workspace_layout": (_i32, [_vp, _i32, _i32, _i32, _c.POINTER(WsLayout)]),
     "dllm_embed": (_i32, [_vp, _vp, _i32, _i32, _vp, _sz, _vp]),
@@ -242,6 +243,11 @@ class Model:
         h = ctypes.c_void_p()
         check(L.dllm_model_create(ctypes.byref(self._c), arr, len(self.weights), ctypes.byref(h)))
         self.h = h
+
+    def pack_weights(self):
+        """dllm_model_pack_weights: tiled copies of the projection weights for the block-row GEMMs."""
+        check(lib().dllm_model_pack_weights(self.h))
+        return self
 
     def close(self):
         if getattr(self, "h", None):

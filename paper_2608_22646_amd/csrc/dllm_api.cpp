@@ -48,6 +48,10 @@ struct dllm_model {
   dllm_model_cfg cfg;
   std::vector<const void*> w;
   bf16_t* head_tiled = nullptr;  // bf16: owned tiled copy of the LM head
+  // bf16, after dllm_model_pack_weights: packed copies of every layer's q/k/v,
+  // output, gate/up and down weights (one allocation; offsets per layer)
+  bf16_t* packed = nullptr;
+  std::vector<size_t> packed_off;  // [layer * 4 + {0: qkv, 1: o, 2: gate/up, 3: down}] in elements
   int32_t* pinned_flag = nullptr;
   uint32_t prof_mask = 0;  // bit k: record launches of kind k
   std::vector<ProfEvent> events;
@@ -234,6 +238,50 @@ void norm_rows_bf16(const dllm_model* m, float* h, PendingResid* pend, const voi
   }
 }
 
+// The weight side of a layer's four GEMMs (q/k/v, output, gate/up, down).
+GemmArgs layer_gemm(const dllm_model* m, int layer, int which) {
+  const auto& c = m->cfg;
+  const int base = 1 + 9 * layer, hd = c.head_dim;
+  GemmArgs g{};
+  switch (which) {
+    case 0:
+      g.epi = EPI_QKV_ROPE;
+      g.N = (c.n_heads + 2 * c.n_kv_heads) * hd;
+      g.K = c.d_model;
+      g.W0 = Wb(m, base + 1);
+      g.W1 = Wb(m, base + 2);
+      g.W2 = Wb(m, base + 3);
+      g.n0 = c.n_heads * hd;
+      g.n1 = c.n_kv_heads * hd;
+      break;
+    case 1:
+      g.epi = EPI_RESID;
+      g.N = c.d_model;
+      g.K = c.n_heads * hd;
+      g.W0 = Wb(m, base + 4);
+      g.n0 = c.d_model;
+      break;
+    case 2:
+      g.epi = EPI_SWIGLU;
+      g.N = 2 * c.d_ff;
+      g.K = c.d_model;
+      g.W0 = Wb(m, base + 6);
+      g.W1 = Wb(m, base + 7);
+      g.n0 = c.d_ff;
+      g.n1 = c.d_ff;
+      break;
+    default:
+      g.epi = EPI_RESID;
+      g.N = c.d_model;
+      g.K = c.d_ff;
+      g.W0 = Wb(m, base + 8);
+      g.n0 = c.d_model;
+      break;
+  }
+  if (m->packed) g.Wp = m->packed + m->packed_off[(size_t)layer * 4 + which];
+  return g;
+}
+
 // One layer (part 0: attention half, 1: MLP half, 2: both) on the B * Lq rows
 // of h (rows: see LayerRows; null = the full sequence, keys/values in the
 // workspace).  carry_in holds split-K partials the previous layer's down
@@ -253,17 +301,9 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
   PendingResid mid;  // output-projection partials, consumed by the MLP norm
   if (part == 0 || part == 2) {
     norm_rows_bf16(m, h, carry_in, W(m, base + 0), at<void>(ws, lay.a_attn), B, Lq, s);
-    GemmArgs g{};
-    g.epi = EPI_QKV_ROPE;
+    GemmArgs g = layer_gemm(m, layer, 0);
     g.M = M;
-    g.N = (c.n_heads + 2 * c.n_kv_heads) * hd;
-    g.K = d;
     g.A = at<bf16_t>(ws, lay.a_attn);
-    g.W0 = Wb(m, base + 1);
-    g.W1 = Wb(m, base + 2);
-    g.W2 = Wb(m, base + 3);
-    g.n0 = c.n_heads * hd;
-    g.n1 = c.n_kv_heads * hd;
     g.q = at<bf16_t>(ws, lay.q);
     g.k = rows && rows->k ? static_cast<bf16_t*>(rows->k) : at<bf16_t>(ws, lay.k);
     g.vt = rows && rows->vt ? static_cast<f16_t*>(rows->vt) : at<f16_t>(ws, lay.vt);
@@ -280,39 +320,22 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
       ProfScope p(m, PK_ATTN, s);
       launch_attn_bf16(g.q, g.k, g.vt, at<bf16_t>(ws, lay.attn), B, Lq, L, c.n_heads, c.n_kv_heads, s);
     }
-    GemmArgs o{};
-    o.epi = EPI_RESID;
+    GemmArgs o = layer_gemm(m, layer, 1);
     o.M = M;
-    o.N = d;
-    o.K = c.n_heads * hd;
     o.A = at<bf16_t>(ws, lay.attn);
-    o.W0 = Wb(m, base + 4);
-    o.n0 = d;
     o.resid = h;
     gemm_bf16(m, o, ws, lay, s, PK_GEMM, part == 2 ? &mid : nullptr);
   }
   if (part == 1 || part == 2) {
     norm_rows_bf16(m, h, part == 1 ? carry_in : &mid, W(m, base + 5), at<void>(ws, lay.a_mlp), B, Lq, s);
-    GemmArgs g{};
-    g.epi = EPI_SWIGLU;
+    GemmArgs g = layer_gemm(m, layer, 2);
     g.M = M;
-    g.N = 2 * c.d_ff;
-    g.K = d;
     g.A = at<bf16_t>(ws, lay.a_mlp);
-    g.W0 = Wb(m, base + 6);
-    g.W1 = Wb(m, base + 7);
-    g.n0 = c.d_ff;
-    g.n1 = c.d_ff;
     g.out = at<bf16_t>(ws, lay.u);
     gemm_bf16(m, g, ws, lay, s, PK_GATEUP);
-    GemmArgs dn{};
-    dn.epi = EPI_RESID;
+    GemmArgs dn = layer_gemm(m, layer, 3);
     dn.M = M;
-    dn.N = d;
-    dn.K = c.d_ff;
     dn.A = at<bf16_t>(ws, lay.u);
-    dn.W0 = Wb(m, base + 8);
-    dn.n0 = d;
     dn.resid = h;
     gemm_bf16(m, dn, ws, lay, s, PK_GEMM, carry_out);
   }
@@ -632,7 +655,39 @@ int dllm_model_destroy(dllm_model* m) {
   }
   if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
   if (m->head_tiled) (void)hipFree(m->head_tiled);
+  if (m->packed) (void)hipFree(m->packed);
   delete m;
+  API_END
+}
+
+int dllm_model_pack_weights(dllm_model* m) {
+  API_BEGIN
+  check_model(m);
+  require(m->cfg.dtype == DLLM_BF16, DLLM_EUNSUPPORTED, "packed weights are for bf16 models");
+  if (m->packed) return DLLM_OK;
+  const int nl = m->cfg.n_layers;
+  std::vector<size_t> off((size_t)nl * 4);
+  size_t total = 0;
+  for (int l = 0; l < nl; ++l)
+    for (int w = 0; w < 4; ++w) {
+      const GemmArgs g = layer_gemm(m, l, w);
+      off[(size_t)l * 4 + w] = total / sizeof(bf16_t);
+      total += align256(gemm_packed_bytes(g.N, g.K));
+    }
+  bf16_t* buf = nullptr;
+  // the weights may still be in flight on any stream: wait, pack, wait
+  hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
+  hip_check(hipMalloc((void**)&buf, std::max<size_t>(total, 256)), "hipMalloc");
+  try {
+    for (int l = 0; l < nl; ++l)
+      for (int w = 0; w < 4; ++w) launch_pack_gemm_weights(layer_gemm(m, l, w), buf + off[(size_t)l * 4 + w], nullptr);
+    hip_check(hipStreamSynchronize(nullptr), "hipStreamSynchronize");
+  } catch (...) {
+    (void)hipFree(buf);
+    throw;
+  }
+  m->packed_off = off;
+  m->packed = buf;
   API_END
 }
 

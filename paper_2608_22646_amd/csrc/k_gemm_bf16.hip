@@ -148,9 +148,14 @@ __device__ __forceinline__ int2 tile_origin(const GemmArgs& g, int lin) {
 // acc += A[m0 : m0+BM, k] * Bv[n0 : n0+BN, k]^T over the k-steps kt0 .. kt0+nk-1
 // (64 wide), streamed through the S-stage LDS ring.  Starts with a barrier, so
 // the ring may still be in use by a previous call; leaves no load in flight.
-template <class TL, int EPI>
+// PB: Bv is read from its packed copy g.Wp (pack_gemm_weights_kernel), where
+// the tile's 256 rows x 64 k of a k-step are one contiguous 32 KiB run whose
+// 1 KiB pieces are the MFMA B operands of (32-row group, 16-k slice) in lane
+// order: the DMA streams whole runs and each fragment read is lane-linear.
+template <class TL, int EPI, bool PB = false>
 __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave, int lane, int m0, int n0, int kt0,
                                          int nk, f32x16_t (&acc)[TL::TI][TL::TJ]) {
+  static_assert(!PB || TL::BN == 256, "a packed tile is one 256-row tile of the copy");
   constexpr int BM = TL::BM, BN = TL::BN, S = TL::S, NW = TL::NW;
   const int wt = wave % TL::NWT, kg = wave / TL::NWT;
   const int wm = wt / (BN / TL::WN), wn = wt % (BN / TL::WN);
@@ -177,13 +182,19 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
   uint32_t vob[TL::IB];
 #pragma unroll
   for (int i = 0; i < TL::IB; ++i) {
-    const int2 first = vrow<EPI>(g, n0 + 8 * (NW * i + wave));  // wave-uniform
-    rbs[i] = __builtin_amdgcn_make_buffer_rsrc((void*)wsrc[first.x], 0, 0x7fffffff, 0x00020000);
-    vob[i] = (uint32_t)(((size_t)(first.y + lr) * g.K + kbeg + lc * 8) * 2);
+    if (PB) {
+      // piece NW i + w of the (n0 / 256, k-step) run; the k advance is 32 KiB per step
+      rbs[i] = __builtin_amdgcn_make_buffer_rsrc((void*)g.Wp, 0, 0x7fffffff, 0x00020000);
+      vob[i] = (uint32_t)((((size_t)(n0 >> 8) * (g.K / BK) + kt0) * 32768) + (NW * i + wave) * 1024 + lane * 16);
+    } else {
+      const int2 first = vrow<EPI>(g, n0 + 8 * (NW * i + wave));  // wave-uniform
+      rbs[i] = __builtin_amdgcn_make_buffer_rsrc((void*)wsrc[first.x], 0, 0x7fffffff, 0x00020000);
+      vob[i] = (uint32_t)(((size_t)(first.y + lr) * g.K + kbeg + lc * 8) * 2);
+    }
   }
   auto issue = [&](int kt) {
     char* base = lds + (kt % S) * TL::LDS_STAGE;
-    const int soff = kt * BK * 2;
+    const int soff = kt * BK * 2, soff_b = PB ? kt * 32768 : soff;
 #pragma unroll
     for (int i = 0; i < TL::IA; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + 8 * (NW * i + wave) * 128), 16, voa[i], soff,
@@ -191,7 +202,7 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
 #pragma unroll
     for (int i = 0; i < TL::IB; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rbs[i], (lds_ptr_t)(base + BM * 128 + 8 * (NW * i + wave) * 128), 16,
-                                               vob[i], soff, 0, 0);
+                                               vob[i], soff_b, 0, 0);
   };
 
   constexpr int PER_STAGE = TL::IA + TL::IB;  // DMA instructions per wave per stage
@@ -215,7 +226,9 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
       af[set][i] = *reinterpret_cast<const bf16x8_t*>(base + swz(wm * TL::WM + i * 32 + lrow, ch));
 #pragma unroll
     for (int j = 0; j < TL::TJ; ++j)
-      bfr[set][j] = *reinterpret_cast<const bf16x8_t*>(base + BM * 128 + swz(wn * TL::WN + j * 32 + lrow, ch));
+      bfr[set][j] = PB ? *reinterpret_cast<const bf16x8_t*>(
+                             base + BM * 128 + ((((wn * TL::WN + j * 32) >> 5) * 4 + ks0 + kl) << 10) + lane * 16)
+                       : *reinterpret_cast<const bf16x8_t*>(base + BM * 128 + swz(wn * TL::WN + j * 32 + lrow, ch));
   };
 
   wait_vm_lds<0>();
@@ -552,7 +565,7 @@ __device__ __forceinline__ void zero_acc(f32x16_t (&acc)[TL::TI][TL::TJ]) {
 
 // One workgroup per output tile (grid.x), optionally split over K (grid.z:
 // float32 partial tiles, summed by splitk_resid_kernel).
-template <class TL, int EPI>
+template <class TL, int EPI, bool PB = false>
 __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
   // The buffer-resource builtins exist only for the device target; the host
   // pass needs just the kernel's signature for its launch stub.
@@ -572,7 +585,7 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
 
   f32x16_t acc[TL::TI][TL::TJ];
   zero_acc<TL>(acc);
-  mma_tile<TL, EPI>(g, lds, wave, lane, o.x, o.y, kt0, nk, acc);
+  mma_tile<TL, EPI, PB>(g, lds, wave, lane, o.x, o.y, kt0, nk, acc);
 
   if (TL::KG == 2) {
     // acc(group 0) += acc(group 1) through LDS (the ring is idle once every
@@ -701,6 +714,36 @@ __global__ void splitk_qkv_kernel(const float* __restrict__ part, int S, GemmArg
   }
 }
 
+// Packed copy of a GEMM's virtual weight matrix Bv [N, K] (rows in vrow order):
+// for 256-row tile t and 64-k step kb the block [256, 64] is one contiguous 32
+// KiB run, inside it the 1 KiB MFMA operand of 32-row group gr and 16-k slice
+// s in lane order (lane l: row 32 gr + l % 32, k 16 s + 8 (l / 32) .. +7) --
+// the layout of the LM head's copy.  Rows past N are zero.  One thread per
+// 16-byte vector, in destination order.
+template <int EPI>
+__global__ void pack_gemm_weights_kernel(GemmArgs g, bf16_t* __restrict__ out, size_t nvec) {
+  const int nk = g.K / 64;
+  const bf16_t* wsrc[3] = {g.W0, g.W1, g.W2};
+  for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < nvec; idx += (size_t)gridDim.x * blockDim.x) {
+    const int l = (int)(idx % 64);
+    size_t t = idx / 64;
+    const int sl = (int)(t % 4);
+    t /= 4;
+    const int gr = (int)(t % 8);
+    t /= 8;
+    const int kb = (int)(t % nk);
+    const size_t lt = t / nk;
+    const int n = (int)(lt * 256 + gr * 32 + (l & 31));
+    const int k = kb * 64 + sl * 16 + (l >> 5) * 8;
+    bf16x8_t v = {};
+    if (n < g.N) {
+      const int2 src = vrow<EPI>(g, n);
+      v = *reinterpret_cast<const bf16x8_t*>(wsrc[src.x] + (size_t)src.y * g.K + k);
+    }
+    *reinterpret_cast<bf16x8_t*>(out + idx * 8) = v;
+  }
+}
+
 struct Plan {
   int bm, bn, kg, split;
 };
@@ -757,19 +800,21 @@ Plan plan(int M, int N, int K, int epi) {
   return best;
 }
 
-template <class TL, int EPI>
+template <class TL, int EPI, bool PB = false>
 void launch_tile(const GemmArgs& g, int split, hipStream_t s) {
   const int tiles = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
   const size_t lds = lds_bytes<TL, EPI>();
-  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<TL, EPI>,
+  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_bf16_kernel<TL, EPI, PB>,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hip_check(attr, "hipFuncSetAttribute(gemm_bf16)");
-  hipLaunchKernelGGL((gemm_bf16_kernel<TL, EPI>), dim3(tiles, 1, split), dim3(TL::NTH), lds, s, g);
+  hipLaunchKernelGGL((gemm_bf16_kernel<TL, EPI, PB>), dim3(tiles, 1, split), dim3(TL::NTH), lds, s, g);
 }
 
 template <int EPI>
 void launch_epi(const GemmArgs& g, const Plan& p, hipStream_t s) {
-  if (p.bm == 64)
+  if (p.bm == 64 && g.Wp)
+    launch_tile<TileT, EPI, true>(g, p.split, s);
+  else if (p.bm == 64)
     launch_tile<TileT, EPI>(g, p.split, s);
   else if (p.bm == 256 && p.bn == 256)
     launch_tile<TileL, EPI>(g, p.split, s);
@@ -782,6 +827,21 @@ void launch_epi(const GemmArgs& g, const Plan& p, hipStream_t s) {
 }
 
 }  // namespace
+
+size_t gemm_packed_bytes(int N, int K) { return (size_t)ceil_div(N, 256) * 256 * (size_t)K * sizeof(bf16_t); }
+
+void launch_pack_gemm_weights(const GemmArgs& g, bf16_t* out, hipStream_t s) {
+  if (g.K % BK != 0) throw HipError("pack_gemm_weights: K % 64 must be 0");
+  if (gemm_packed_bytes(g.N, g.K) > 0x7fffffffu) throw HipError("pack_gemm_weights: matrix larger than 2 GiB");
+  const size_t nvec = gemm_packed_bytes(g.N, g.K) / 16;
+  const int grid = (int)std::min<size_t>(ceil_div(nvec, (size_t)256), 8192);
+  switch (g.epi) {
+    case EPI_QKV_ROPE: hipLaunchKernelGGL(pack_gemm_weights_kernel<EPI_QKV_ROPE>, dim3(grid), dim3(256), 0, s, g, out, nvec); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL(pack_gemm_weights_kernel<EPI_SWIGLU>, dim3(grid), dim3(256), 0, s, g, out, nvec); break;
+    default: hipLaunchKernelGGL(pack_gemm_weights_kernel<EPI_RESID>, dim3(grid), dim3(256), 0, s, g, out, nvec); break;
+  }
+  DLLM_LAUNCH_CHECK("pack_gemm_weights");
+}
 
 size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi) {
   const Plan p = plan(M, N, K, epi);

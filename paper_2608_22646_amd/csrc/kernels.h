@@ -59,6 +59,9 @@ struct GemmArgs {
   int B, L, Hq, Hkv, Lq, pos0;
   // split-K scratch (float32 partials [split, M, N]) from the workspace
   float* splitk_buf;
+  // optional packed copy of Bv (launch_pack_gemm_weights): launches of at most
+  // 128 rows then stream it instead of the row-major tensors
+  const bf16_t* Wp;
 };
 int device_cu_count();  // compute units of the current device (256 if it cannot be queried)
 // Split-K partial tiles of a residual GEMM whose reduction into the residual
@@ -77,6 +80,10 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer = nu
 //   out[m, :] = bf16(RMSNorm(h[m, :]) * g)
 void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, bf16_t* out, int M, int d, float eps,
                           hipStream_t s);
+// Packed copy of a GEMM's virtual weight matrix (g's W0/W1/W2, n0, n1, N, K,
+// epi) in the LM head's tiled operand order, rows padded to 256.
+size_t gemm_packed_bytes(int N, int K);
+void launch_pack_gemm_weights(const GemmArgs& g, bf16_t* out, hipStream_t s);
 // Bytes of split-K scratch a launch of this shape needs (0 if it does not split).
 size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi);
 

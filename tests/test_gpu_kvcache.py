@@ -11,9 +11,10 @@
   dllm_generate;
 * small bf16 model: the cache a refresh fills equals the keys/values of the
   plain forward bit for bit; every stage of a cached layer against the oracle
-  on the GPU's own stage inputs; decode replay;
-* full-size LLaDA-8B / Dream-7B shapes: one cached layer's stages and the
-  decode replay with the paper's update frequencies (16 and 8).
+  on the GPU's own stage inputs; decode replay; with the packed weight copies
+  (dllm_model_pack_weights) cached forwards are bit-identical;
+* full-size LLaDA-8B / Dream-7B shapes (packed weights): one cached layer's
+  stages and the decode replay with the paper's update frequencies (16 and 8).
 """
 import math
 
@@ -213,6 +214,30 @@ def test_bf16_refresh_cache_and_cached_layer_stages(small, Bn, P, G, blk):
         say(f"  layer {l}: " + ", ".join(f"{k}={v:.2e}" for k, v in st.items()))
 
 
+@pytest.mark.parametrize("Bn", [1, 2, 5])
+def test_bf16_packed_weights_bit_identical(small, Bn):
+    """The packed copies change where the block-row GEMMs read their weights,
+    not what they compute: same tiles, same k order, so the logits of a cached
+    forward are bit-identical (B = 5: 160 rows, beyond the packed path)."""
+    model, _ = small
+    packed = B.Model(SMALL, model.weights).pack_weights()
+    P, G, bl = 40, 64, 32
+    L, row0 = P + G, P + bl
+    say(f"bf16 packed weights B={Bn}")
+    x0 = synth.make_ints((Bn, L), 12, 0, SMALL.vocab - 1).cuda()
+    x1 = torch.from_numpy(_changed_block(x0.cpu().numpy(), row0, bl, 13, SMALL.vocab).astype(np.int32)).cuda()
+    out = []
+    for mdl in (model, packed):
+        kv, ws = mdl.kv_cache(Bn, L), mdl.workspace(Bn, L, bl)
+        mdl.forward_kv(x0, row0, bl, kv, refresh=True, ws=ws)
+        out.append(mdl.forward_kv(x1, row0, bl, kv, refresh=False, ws=ws, logits=True))
+    torch.cuda.synchronize()
+    (c0, a0, l0), (c1, a1, l1) = out
+    assert torch.equal(l0.view(torch.int32), l1.view(torch.int32))
+    assert torch.equal(c0.view(torch.int32), c1.view(torch.int32)) and torch.equal(a0, a1)
+    packed.close()
+
+
 def test_bf16_generate_kv_replay(small):
     model, _ = small
     ctl = B.Controller()
@@ -239,7 +264,7 @@ def test_full_size_cached_layer_and_decode(name):
     L = P + G
     say(f"full-size kv {name}")
     weights = synth.make_weights(cfg, "cuda")
-    model = B.Model(cfg, weights)
+    model = B.Model(cfg, weights).pack_weights()
     # one cached layer (layer 1: its cache was filled from a refresh of layer-0
     # output) on the second block with changed tokens
     lw = [w.to(torch.float32).cpu().numpy() for w in weights[:1 + 9 * 2]] + [None, None]
