@@ -172,8 +172,11 @@ int dllm_model_destroy(dllm_model* model);
  * and freed by dllm_model_destroy (device memory about the size of those
  * weights: ~14 GB for the LLaDA-8B shape).  GEMMs of at most 128 rows -- the
  * block rows of a cached step (dllm_forward_kv and friends) -- then stream
- * these runs instead of the row-major tensors; results are bit-identical.  As
- * with the LM head copy, later writes to the caller's weights are not seen.
+ * these runs instead of the row-major tensors: up to 64 rows through a
+ * register-direct kernel (k summed in another order: results agree to
+ * rounding, not bit for bit), 65 .. 128 rows through the tiled kernel
+ * (bit-identical).  As with the LM head copy, later writes to the caller's
+ * weights are not seen.
  * A second call does nothing.  Errors: DLLM_EUNSUPPORTED (fp32 model), DLLM_EHIP.
  */
 int dllm_model_pack_weights(dllm_model* model);

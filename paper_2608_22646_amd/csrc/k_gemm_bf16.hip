@@ -744,6 +744,148 @@ __global__ void pack_gemm_weights_kernel(GemmArgs g, bf16_t* __restrict__ out, s
   }
 }
 
+// GEMM of at most 64 rows from the packed copy, register-direct (the LM head's
+// streaming design): wave w of the grid owns GW 32-row groups of Bv (group
+// block w % ngb) and the k-slices [z KS / S, (z + 1) KS / S) of split z =
+// w / ngb; per 16-k slice it loads its GW 1 KiB W operands (contiguous runs of
+// the copy, non-temporal) and MB X operands (rows 32 mb + l % 32 of A, zero
+// past M) into a P-deep register ring -- no LDS, no barrier -- and runs GW x MB
+// MFMAs with W as the A operand (a lane ends with 16 columns n of one row m).
+// It writes float32 partials part[z, m, n]; the split-K epilogues finish them.
+// Loads complete in issue order, so before slice u only the (GW + MB) (P - 1)
+// loads of the slices after it may be outstanding.
+struct RowsArgs {
+  const bf16_t* A;   // [M, K]
+  const bf16_t* Wp;  // packed Bv
+  float* part;       // [S, M, N]
+  int M, N, K, S, ngb;
+};
+
+template <int GW, int MB, int P>
+__global__ void __launch_bounds__(256, 2) gemm_rows_kernel(RowsArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  static_assert((GW + MB) * (P - 1) < 64, "vmcnt range");
+  const int lane = threadIdx.x & 63;
+  const int wg = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (wg >= a.ngb * a.S) return;
+  const int gb = wg % a.ngb, z = wg / a.ngb;
+  const int KS = a.K / 16, nk = a.K / 64;
+  const int u0 = (int)((long)z * KS / a.S), n = (int)((long)(z + 1) * KS / a.S) - u0;
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)a.Wp, 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, 0, 0x7fffffff, 0x00020000);
+  const int lr = lane & 31, half = lane >> 5;
+  // group G = gb GW + j lies in 256-row tile G / 8 at position G % 8
+  uint32_t wbase[GW];
+#pragma unroll
+  for (int j = 0; j < GW; ++j) {
+    const int G = gb * GW + j;
+    wbase[j] = (uint32_t)(((size_t)(G >> 3) * nk * 8 + (G & 7)) * 4 * 1024 + lane * 16);
+  }
+  uint32_t xoff[MB];
+  bool xok[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = 32 * mb + lr;
+    xok[mb] = m < a.M;
+    xoff[mb] = (uint32_t)(((size_t)min(m, a.M - 1) * a.K + half * 8) * 2);
+  }
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  u32x4_t wbuf[P][GW], xbuf[P][MB];
+  auto load = [&](int u, int slot) {
+    const int us = u0 + u, kb = us >> 2, sl = us & 3;
+#pragma unroll
+    for (int j = 0; j < GW; ++j)
+      wbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rw, wbase[j] + (uint32_t)(kb * 32768 + sl * 1024), 0, 2);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+      xbuf[slot][mb] = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[mb] + (uint32_t)(us * 32), 0, 0);
+  };
+  f32x16_t acc[GW][MB];
+#pragma unroll
+  for (int j = 0; j < GW; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[j][mb][r] = 0.f;
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (p < n) load(p, p);
+  for (int b0 = 0; b0 < n; b0 += P) {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int u = b0 + p;
+      if (u < n) {
+        if (u + P - 1 < n)
+          __builtin_amdgcn_s_waitcnt((((GW + MB) * (P - 1)) & 15) | (7 << 4) | (15 << 8) |
+                                     ((((GW + MB) * (P - 1)) >> 4) << 14));
+        else
+          __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8));  // the last slices: fewer later loads issued
+        bf16x8_t xf[MB];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          xf[mb] = __builtin_bit_cast(bf16x8_t, xbuf[p][mb]);
+          if (!xok[mb]) xf[mb] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < GW; ++j)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+            acc[j][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wbuf[p][j]), xf[mb],
+                                                                acc[j][mb], 0, 0, 0);
+        if (u + P < n) load(u + P, p);
+      }
+    }
+  }
+  // partials: lane holds columns n = 32 G + 8 (r / 4) + 4 half + r % 4 of row m = 32 mb + l % 32
+  float* part = a.part + (size_t)z * a.M * a.N;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = 32 * mb + lr;
+    if (m >= a.M) continue;
+#pragma unroll
+    for (int j = 0; j < GW; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int nn = (gb * GW + j) * 32 + 8 * q + 4 * half;
+        *reinterpret_cast<float4*>(part + (size_t)m * a.N + nn) =
+            make_float4(acc[j][mb][4 * q], acc[j][mb][4 * q + 1], acc[j][mb][4 * q + 2], acc[j][mb][4 * q + 3]);
+      }
+  }
+#endif
+}
+
+// Groups per wave and K split of a register-direct launch, by a time model
+// measured at 32 rows on the LLaDA-8B shapes: the bytes a compute unit pulls
+// bound it (~28 GB/s per CU, 7 per wave), so a launch takes the slices of its
+// longest wave x (GW W loads + MB / 4 for the X loads, one costing a quarter
+// of a W load) x 0.146 us per KiB, times the workgroups per CU; plus the
+// float32 partials written and read back (~8 TB/s).  Fewer splits, then more
+// groups per wave, on ties.  Gate/up at 32 rows: 4 groups, split 5 (240
+// workgroups: 36 us); with split 6 a second workgroup on 32 of the CUs took 52.
+struct RowsPlan {
+  int gw, split;
+};
+RowsPlan rows_plan(int M, int N, int K) {
+  const int ng = N / 32, ks = K / 16, mb = M > 32 ? 2 : 1;
+  const long cus = device_cu_count();
+  RowsPlan best{1, 1};
+  double best_t = 1e30;
+  for (int gw : {4, 2, 1}) {
+    if (ng % gw != 0) continue;
+    const long ngb = ng / gw;
+    for (int split = 1; split <= std::min(16, ks); ++split) {
+      const long wgs = (ngb * split + 3) / 4, rounds = (wgs + cus - 1) / cus;
+      const double t = 0.146 * rounds * (gw + 0.25 * mb) * ((ks + split - 1) / split) +
+                       2.0 * split * M * (double)N * 4 / 8e6;
+      if (t < best_t - 1e-9) {
+        best_t = t;
+        best = RowsPlan{gw, split};
+      }
+    }
+  }
+  return best;
+}
+
 struct Plan {
   int bm, bn, kg, split;
 };
@@ -843,9 +985,60 @@ void launch_pack_gemm_weights(const GemmArgs& g, bf16_t* out, hipStream_t s) {
   DLLM_LAUNCH_CHECK("pack_gemm_weights");
 }
 
+// launches the register-direct kernel can take (given the packed copy)
+bool rows_path(int M, int N, int K) { return M >= 1 && M <= 64 && N % 32 == 0 && K % 64 == 0; }
+
 size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi) {
   const Plan p = plan(M, N, K, epi);
-  return p.split > 1 ? (size_t)p.split * M * N * sizeof(float) : 0;
+  size_t b = p.split > 1 ? (size_t)p.split * M * N * sizeof(float) : 0;
+  if (rows_path(M, N, K)) b = std::max(b, (size_t)rows_plan(M, N, K).split * M * N * sizeof(float));
+  return b;
+}
+
+template <int S>
+void launch_splitk_resid(const float* part, float* resid, long MN, hipStream_t s) {
+  hipLaunchKernelGGL(splitk_resid_kernel<S>, dim3(ceil_div(MN / 4, 256)), dim3(256), 0, s, part, resid, MN);
+}
+
+// The register-direct path: partials from gemm_rows_kernel, then the epilogue.
+void launch_gemm_rows(const GemmArgs& a, hipStream_t s) {
+  const RowsPlan rp = rows_plan(a.M, a.N, a.K);
+  RowsArgs r{a.A, a.Wp, a.splitk_buf, a.M, a.N, a.K, rp.split, a.N / 32 / rp.gw};
+  const dim3 grid(ceil_div(r.ngb * r.S, 4)), blk(256);
+  const bool two = a.M > 32;
+  auto go = [&](auto gwc) {
+    constexpr int GW = decltype(gwc)::value;
+    if (two)
+      hipLaunchKernelGGL((gemm_rows_kernel<GW, 2, 4>), grid, blk, 0, s, r);
+    else
+      hipLaunchKernelGGL((gemm_rows_kernel<GW, 1, 8>), grid, blk, 0, s, r);
+  };
+  if (rp.gw == 4)
+    go(std::integral_constant<int, 4>{});
+  else if (rp.gw == 2)
+    go(std::integral_constant<int, 2>{});
+  else
+    go(std::integral_constant<int, 1>{});
+  DLLM_LAUNCH_CHECK("gemm_rows");
+  if (a.epi == EPI_SWIGLU) {
+    const long n = (long)a.M * (a.N / 2);
+    hipLaunchKernelGGL(splitk_swiglu_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, a.splitk_buf, rp.split, a.M,
+                       a.N / 2, a.out);
+  } else if (a.epi == EPI_QKV_ROPE) {
+    const long n = (long)a.M * a.N;
+    hipLaunchKernelGGL(splitk_qkv_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, a.splitk_buf, rp.split, a);
+  } else {
+    const long MN = (long)a.M * a.N;
+    switch (rp.split) {
+#define DLLM_CASE(S_) \
+  case S_: launch_splitk_resid<S_>(a.splitk_buf, a.resid, MN, s); break;
+      DLLM_CASE(1) DLLM_CASE(2) DLLM_CASE(3) DLLM_CASE(4) DLLM_CASE(5) DLLM_CASE(6) DLLM_CASE(7) DLLM_CASE(8)
+      DLLM_CASE(9) DLLM_CASE(10) DLLM_CASE(11) DLLM_CASE(12) DLLM_CASE(13) DLLM_CASE(14) DLLM_CASE(15) DLLM_CASE(16)
+#undef DLLM_CASE
+      default: throw HipError("gemm_rows: split must be 1 .. 16");
+    }
+  }
+  DLLM_LAUNCH_CHECK("gemm_rows epilogue");
 }
 
 void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
@@ -858,6 +1051,10 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
     throw HipError("gemm_bf16: q/k/v epilogue needs B * L < 2^24 and B < 2^16");
   if (a.epi == EPI_QKV_ROPE && (a.Lq < 1 || a.pos0 < 0 || a.pos0 + a.Lq > a.L || a.M % a.Lq != 0))
     throw HipError("gemm_bf16: q/k/v rows must be whole windows of Lq positions inside the sequence");
+  if (a.Wp && rows_path(a.M, a.N, a.K)) {  // few rows from the packed copy: register-direct
+    launch_gemm_rows(a, s);
+    return;
+  }
   const Plan p = plan(a.M, a.N, a.K, a.epi);
   switch (a.epi) {
     case EPI_QKV_ROPE: launch_epi<EPI_QKV_ROPE>(a, p, s); break;

@@ -11,8 +11,10 @@
   dllm_generate;
 * small bf16 model: the cache a refresh fills equals the keys/values of the
   plain forward bit for bit; every stage of a cached layer against the oracle
-  on the GPU's own stage inputs; decode replay; with the packed weight copies
-  (dllm_model_pack_weights) cached forwards are bit-identical;
+  on the GPU's own stage inputs, also with the packed weight copies
+  (dllm_model_pack_weights: at most 64 block rows run the register-direct
+  GEMM); decode replay; packed and plain cached forwards bit-identical where
+  both run the same tiles (more than 64 rows), close otherwise;
 * full-size LLaDA-8B / Dream-7B shapes (packed weights): one cached layer's
   stages and the decode replay with the paper's update frequencies (16 and 8).
 """
@@ -179,18 +181,49 @@ def small():
     return B.Model(SMALL, [w.to("cuda") for w in w_cpu]), [w.to(torch.float32).numpy() for w in w_cpu]
 
 
-@pytest.mark.parametrize("Bn,P,G,blk", [(2, 40, 64, 1), (1, 36, 96, 0), (5, 40, 64, 1), (5, 36, 96, 2)])
-def test_bf16_refresh_cache_and_cached_layer_stages(small, Bn, P, G, blk):
+@pytest.fixture(scope="module")
+def small_packed(small):
+    model, wnp = small
+    packed = B.Model(SMALL, model.weights).pack_weights()
+    yield packed, wnp
+    packed.close()
+
+
+# one layer of the LLaDA-8B widths with GQA: the register-direct GEMM runs
+# 4-group waves (gate/up), 2-group (down) and 1-group (q/k/v, o), with one
+# (32 rows) or two (64 rows) row operands
+WIDE = synth.ModelConfig("wide-bf16", n_layers=1, d_model=4096, n_heads=32, n_kv_heads=8, head_dim=128,
+                         d_ff=12288, vocab=4000, rope_base=500000.0, dtype="bf16", lm_head_std=5 / math.sqrt(4096),
+                         norm_gain_std=0.1)
+
+
+@pytest.fixture(scope="module")
+def wide_packed():
+    w_cpu = synth.make_weights(WIDE, "cpu")
+    model = B.Model(WIDE, [w.to("cuda") for w in w_cpu]).pack_weights()
+    yield model, [w.to(torch.float32).numpy() for w in w_cpu]
+    model.close()
+
+
+@pytest.mark.parametrize("which,Bn,P,G,blk", [("small", 2, 40, 64, 1), ("small", 1, 36, 96, 0),
+                                              ("small", 5, 40, 64, 1), ("small", 5, 36, 96, 2),
+                                              ("small_packed", 2, 40, 64, 1), ("small_packed", 1, 36, 96, 2),
+                                              ("small_packed", 3, 40, 64, 0), ("wide_packed", 1, 40, 64, 1),
+                                              ("wide_packed", 2, 36, 96, 2)])
+def test_bf16_refresh_cache_and_cached_layer_stages(request, which, Bn, P, G, blk):
     """Up to 128 block rows the q/k/v and SwiGLU GEMMs split K and run their
     epilogues on the summed partials; B = 5 (160 rows) runs the fused
     epilogues on the row window.  P = 36: block positions not a multiple of 8
-    (the element-wise v^T path)."""
-    model, wnp = small
+    (the element-wise v^T path).  Packed weights: at most 64 rows (B <= 2) run
+    the register-direct GEMM (32 rows: one row operand, 64: two), 96 rows
+    (B = 3) the tiled path."""
+    model, wnp = request.getfixturevalue(which)
+    cfg = model.cfg
     L, bl = P + G, 32
     row0 = P + blk * bl
-    say(f"bf16 kv stages B={Bn} L={L} row0={row0}")
-    x0 = synth.make_ints((Bn, L), 6, 0, SMALL.vocab - 1)
-    x1 = torch.from_numpy(_changed_block(x0.numpy(), row0, bl, 7, SMALL.vocab).astype(np.int32))
+    say(f"bf16 kv stages {which} B={Bn} L={L} row0={row0}")
+    x0 = synth.make_ints((Bn, L), 6, 0, cfg.vocab - 1)
+    x1 = torch.from_numpy(_changed_block(x0.numpy(), row0, bl, 7, cfg.vocab).astype(np.int32))
     kv = model.kv_cache(Bn, L)
     ws = model.workspace(Bn, L, bl)
     ws2 = model.workspace(Bn, L, bl)
@@ -198,7 +231,7 @@ def test_bf16_refresh_cache_and_cached_layer_stages(small, Bn, P, G, blk):
     model.embed(x0.cuda(), ws)
     model.embed(x0.cuda(), ws2)
     lay0 = model.layout(Bn, L, 0)
-    for l in range(SMALL.n_layers):
+    for l in range(cfg.n_layers):
         model.layer_kv(l, 2, Bn, L, 0, L, kv, ws)
         model.layer(l, 2, Bn, L, ws2)
         torch.cuda.synchronize()
@@ -209,18 +242,21 @@ def test_bf16_refresh_cache_and_cached_layer_stages(small, Bn, P, G, blk):
         assert torch.equal(V.view(torch.int16), v2.view(torch.int16)), f"layer {l} values"
     # a cached step on changed block tokens, stage by stage
     model.embed_rows(x1.cuda(), row0, bl, ws)
-    for l in range(SMALL.n_layers):
-        st = check_layer_cached(model, SMALL, wnp, ws, kv, Bn, L, row0, bl, l)
+    for l in range(cfg.n_layers):
+        st = check_layer_cached(model, cfg, wnp, ws, kv, Bn, L, row0, bl, l)
         say(f"  layer {l}: " + ", ".join(f"{k}={v:.2e}" for k, v in st.items()))
 
 
-@pytest.mark.parametrize("Bn", [1, 2, 5])
-def test_bf16_packed_weights_bit_identical(small, Bn):
-    """The packed copies change where the block-row GEMMs read their weights,
-    not what they compute: same tiles, same k order, so the logits of a cached
-    forward are bit-identical (B = 5: 160 rows, beyond the packed path)."""
+@pytest.mark.parametrize("Bn", [1, 2, 3, 5])
+def test_bf16_packed_weights(small, small_packed, Bn):
+    """Above 64 block rows the packed copies change where the block-row GEMMs
+    read their weights, not what they compute (same tiles, same k order): the
+    logits of a cached forward are bit-identical (B = 3: 96 rows; B = 5: 160
+    rows).  At most 64 rows (B <= 2) the
+    register-direct GEMM sums k in another order: logits agree to bf16
+    rounding of the hidden states (its own parity is the stage test)."""
     model, _ = small
-    packed = B.Model(SMALL, model.weights).pack_weights()
+    packed, _ = small_packed
     P, G, bl = 40, 64, 32
     L, row0 = P + G, P + bl
     say(f"bf16 packed weights B={Bn}")
@@ -233,9 +269,14 @@ def test_bf16_packed_weights_bit_identical(small, Bn):
         out.append(mdl.forward_kv(x1, row0, bl, kv, refresh=False, ws=ws, logits=True))
     torch.cuda.synchronize()
     (c0, a0, l0), (c1, a1, l1) = out
-    assert torch.equal(l0.view(torch.int32), l1.view(torch.int32))
-    assert torch.equal(c0.view(torch.int32), c1.view(torch.int32)) and torch.equal(a0, a1)
-    packed.close()
+    if Bn > 2:
+        assert torch.equal(l0.view(torch.int32), l1.view(torch.int32))
+        assert torch.equal(c0.view(torch.int32), c1.view(torch.int32)) and torch.equal(a0, a1)
+    else:
+        err = (l1 - l0).abs()
+        say(f"  logits max |diff| {err.max().item():.3e} mean {err.mean().item():.3e} "
+            f"(max |logit| {l0.abs().max().item():.2f})")
+        assert err.max().item() < 2e-2 * l0.abs().max().item() and err.mean().item() < 1e-2
 
 
 def test_bf16_generate_kv_replay(small):
