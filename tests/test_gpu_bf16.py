@@ -45,12 +45,14 @@ def small192():
     return _load(SMALL192)
 
 
-@pytest.mark.parametrize("Bn,P,G", [(2, 40, 64), (1, 9, 32), (2, 1036, 64), (2, 2936, 64)])
+@pytest.mark.parametrize("Bn,P,G", [(2, 40, 64), (1, 9, 32), (2, 1036, 64), (2, 2936, 64), (2, 16136, 64)])
 def test_forward_stages(small, Bn, P, G):
     """Ragged sizes: M = 208 (128-row tiles, ragged), 41 (single partial tile) and
     2200 (256-row tiles, ragged); L not a multiple of the 32- or 64-key attention
     tiles.  L = 3000 runs the key-split attention with 96 queries per workgroup
-    (the others with 64) and a partial last query block."""
+    (the others with 64) and a partial last query block; L = 16200 the
+    8-wave streaming attention (a partial last 64-key tile and a partial
+    last 256-query block)."""
     model, wnp = small
     L = P + G
     say(f"bf16 stages B={Bn} L={L}")
