@@ -169,43 +169,61 @@ __device__ __forceinline__ void mma_tile(const GemmArgs& g, char* lds, int wave,
   // A rows past M are clamped to M-1 (their results are never stored).
   const int lr = lane >> 3, lc = (lane & 7) ^ (((wave & 1) << 2) | (lr >> 1));
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, 0x7fffffff, 0x00020000);
-  uint32_t voa[TL::IA];
+  // In 8-wave tiles only waves 0..3 (one per SIMD) issue the DMA, each for its
+  // own rows and those of wave + 4: an LDS-DMA burst stalls the issuing wave,
+  // and the other wave of its SIMD keeps the MFMA pipe busy meanwhile (gate/up
+  // at M = 8192: 1496 -> 1415 us; 1-4% at M = 512).  wave + 4 has the same
+  // parity, so the same chunk swizzle.
+  constexpr int HW = NW == 8 ? 2 : 1;  // waves whose DMA one issuing wave covers
+  const bool issuer = HW == 1 || wave < NW / 2;
+  uint32_t voa[HW][TL::IA];
 #pragma unroll
-  for (int i = 0; i < TL::IA; ++i) {
-    const int row = min(m0 + 8 * (NW * i + wave) + lr, g.M - 1);
-    voa[i] = (uint32_t)(((size_t)row * g.K + kbeg + lc * 8) * 2);
-  }
+  for (int hw = 0; hw < HW; ++hw)
+#pragma unroll
+    for (int i = 0; i < TL::IA; ++i) {
+      const int wv = wave + hw * (NW / 2);
+      const int row = min(m0 + 8 * (NW * i + wv) + lr, g.M - 1);
+      voa[hw][i] = (uint32_t)(((size_t)row * g.K + kbeg + lc * 8) * 2);
+    }
   // Bv rows: each 8-row DMA group lies in one tensor (the tile's q/k/v tensor,
   // or gate / up by 32-row parity for SwiGLU).
   const bf16_t* wsrc[3] = {g.W0, g.W1, g.W2};
-  __amdgpu_buffer_rsrc_t rbs[TL::IB];
-  uint32_t vob[TL::IB];
+  __amdgpu_buffer_rsrc_t rbs[HW][TL::IB];
+  uint32_t vob[HW][TL::IB];
 #pragma unroll
-  for (int i = 0; i < TL::IB; ++i) {
-    if (PB) {
-      // piece NW i + w of the (n0 / 256, k-step) run; the k advance is 32 KiB per step
-      rbs[i] = __builtin_amdgcn_make_buffer_rsrc((void*)g.Wp, 0, 0x7fffffff, 0x00020000);
-      vob[i] = (uint32_t)((((size_t)(n0 >> 8) * (g.K / BK) + kt0) * 32768) + (NW * i + wave) * 1024 + lane * 16);
-    } else {
-      const int2 first = vrow<EPI>(g, n0 + 8 * (NW * i + wave));  // wave-uniform
-      rbs[i] = __builtin_amdgcn_make_buffer_rsrc((void*)wsrc[first.x], 0, 0x7fffffff, 0x00020000);
-      vob[i] = (uint32_t)(((size_t)(first.y + lr) * g.K + kbeg + lc * 8) * 2);
+  for (int hw = 0; hw < HW; ++hw)
+#pragma unroll
+    for (int i = 0; i < TL::IB; ++i) {
+      const int wv = wave + hw * (NW / 2);
+      if (PB) {
+        // piece NW i + w of the (n0 / 256, k-step) run; the k advance is 32 KiB per step
+        rbs[hw][i] = __builtin_amdgcn_make_buffer_rsrc((void*)g.Wp, 0, 0x7fffffff, 0x00020000);
+        vob[hw][i] = (uint32_t)((((size_t)(n0 >> 8) * (g.K / BK) + kt0) * 32768) + (NW * i + wv) * 1024 + lane * 16);
+      } else {
+        const int2 first = vrow<EPI>(g, n0 + 8 * (NW * i + wv));  // wave-uniform
+        rbs[hw][i] = __builtin_amdgcn_make_buffer_rsrc((void*)wsrc[first.x], 0, 0x7fffffff, 0x00020000);
+        vob[hw][i] = (uint32_t)(((size_t)(first.y + lr) * g.K + kbeg + lc * 8) * 2);
+      }
     }
-  }
   auto issue = [&](int kt) {
+    if (!issuer) return;
     char* base = lds + (kt % S) * TL::LDS_STAGE;
     const int soff = kt * BK * 2, soff_b = PB ? kt * 32768 : soff;
 #pragma unroll
-    for (int i = 0; i < TL::IA; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + 8 * (NW * i + wave) * 128), 16, voa[i], soff,
-                                               0, 0);
+    for (int hw = 0; hw < HW; ++hw) {
+      const int wv = wave + hw * (NW / 2);
 #pragma unroll
-    for (int i = 0; i < TL::IB; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rbs[i], (lds_ptr_t)(base + BM * 128 + 8 * (NW * i + wave) * 128), 16,
-                                               vob[i], soff_b, 0, 0);
+      for (int i = 0; i < TL::IA; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + 8 * (NW * i + wv) * 128), 16, voa[hw][i],
+                                                 soff, 0, 0);
+#pragma unroll
+      for (int i = 0; i < TL::IB; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rbs[hw][i], (lds_ptr_t)(base + BM * 128 + 8 * (NW * i + wv) * 128),
+                                                 16, vob[hw][i], soff_b, 0, 0);
+    }
   };
 
-  constexpr int PER_STAGE = TL::IA + TL::IB;  // DMA instructions per wave per stage
+  constexpr int PER_STAGE = HW * (TL::IA + TL::IB);  // DMA instructions per issuing wave per stage
   constexpr int NS = BK / 16, NF = TL::TI + TL::TJ, NM = TL::TI * TL::TJ;
   constexpr int NSW = NS / TL::KG;  // k-slices of a step that this wave's group computes
   static_assert(NM >= NF && NSW % 2 == 0, "pipeline needs at least as many MFMAs as fragment reads per slice");
