@@ -13,9 +13,9 @@
 //   O^T (128 x 32) += V^T . P^T               (16 MFMAs)
 // in IEEE half: P in [0, 1] rounded to half (11-bit significand, 8x finer than
 // bf16) and V^T holding the bf16 values of v, which half represents exactly in
-// its range.  The key order inside each 16-key MFMA slice is permuted to match
-// where the scores already sit in the S^T registers; V^T is read with the same
-// permutation.
+// its range.  The K rows of the S^T product are fed in a permuted order inside
+// each 16-key group (kperm), so the scores a lane holds for one P.V slice are
+// 8 consecutive keys and its V^T operand is a single 16-byte LDS read.
 #include "kernels.h"
 
 namespace dllm {
@@ -42,6 +42,13 @@ __device__ __forceinline__ int k_off(int key, int chunk) {  // rows of 256 B, 16
 __device__ __forceinline__ int v_off(int d, int chunk) {  // rows of 128 B, 8 chunks
   return K_BYTES + d * 128 + ((chunk ^ ((d >> 1) & 7)) << 4);
 }
+// Key order of the S^T MFMA rows inside each 16-key group: row i takes key
+// kperm(i) (bits 2 and 3 swapped).  A lane's scores then come out as 8
+// consecutive keys per P.V slice (register 4b + c of lane half h holds key
+// 8h + 4b + c of the group), so its V^T operand is one 16-byte chunk -- one
+// conflict-free ds_read_b128 instead of two 8-byte reads that two lanes of a
+// pass share banks with.
+__device__ __forceinline__ int kperm(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
 
 __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                                                            const f16_t* __restrict__ vt, bf16_t* __restrict__ out,
@@ -121,7 +128,7 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
       for (int r = 0; r < 16; ++r) s[st][r] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + lq, ks * 2 + half));
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
         s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[st], 0, 0, 0);
       }
     }
@@ -132,7 +139,7 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = t0 + st * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const int key = t0 + st * 32 + kperm(8 * (r >> 2) + 4 * half + (r & 3));
         const float x = key < L ? s[st][r] * sc : -INFINITY;
         s[st][r] = x;
         mt = fmaxf(mt, x);
@@ -163,14 +170,11 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
       const int st = jk >> 1, r0 = (jk & 1) * 8;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s[st][r0 + e];
-      // slots 0-3: keys 16jk + 4*half + [0,4); slots 4-7: keys 16jk + 8 + 4*half + [0,4)
-      const int kA = jk * 16 + 4 * half, kB = kA + 8;
+      // slot e: key 16jk + 8*half + e (kperm), one 16-byte V^T chunk
 #pragma unroll
       for (int ds = 0; ds < 4; ++ds) {
         const int d = ds * 32 + lq;
-        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kA >> 3) + (kA & 7) * 2);
-        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kB >> 3) + (kB & 7) * 2);
-        const f16x8_t vf = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
+        const f16x8_t vf = *reinterpret_cast<const f16x8_t*>(base + v_off(d, 2 * jk + half));
         o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
       }
     }
@@ -227,7 +231,8 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
                                                                  const f16_t* __restrict__ vt,
                                                                  bf16_t* __restrict__ out, int Lq, int L, int Hq, int Hkv) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int S = 3, PER_STAGE = 32 / NW;  // 16 K + 16 V^T DMA instructions per tile
+  // D tiles in flight ahead of the one in use
+  constexpr int D = 2, S = D + 1, PER_STAGE = 32 / NW;  // 16 K + 16 V^T DMA instructions per tile
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
@@ -285,17 +290,34 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
   float m_run = -INFINITY, l_run = 0.f;
   const float sc = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
 
+  // O^T += V^T P^T for one 16-key slice jk of a tile; P (half) slot e holds
+  // key 16 jk + 8 half + e (kperm), so the V^T operand is one 16-byte chunk
+  auto pv_slice = [&](const char* b_, int jk, const f16x8_t& pf) {
+#pragma unroll
+    for (int ds = 0; ds < 4; ++ds) {
+      const int d = ds * 32 + lq;
+      const f16x8_t vf = *reinterpret_cast<const f16x8_t*>(b_ + v_off(d, 2 * jk + half));
+      o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
+    }
+  };
+  auto to_half = [&](const f32x16_t (&p2)[2], int jk) {
+    f16x8_t pf;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pf[e] = (_Float16)p2[jk >> 1][(jk & 1) * 8 + e];
+    return pf;
+  };
+
   const int ntiles = (L + KT - 1) / KT;
 #pragma unroll
-  for (int s = 0; s < S - 1; ++s)
+  for (int s = 0; s < D; ++s)
     if (s < ntiles) issue(s);
   for (int t = 0; t < ntiles; ++t) {
     if (t + 1 < ntiles)
-      wait_vmcnt_a<PER_STAGE * (S - 2)>();
+      wait_vmcnt_a<PER_STAGE * (D - 1)>();
     else
       wait_vmcnt_a<0>();
-    barrier_nofence_a();
-    if (t + S - 1 < ntiles) issue(t + S - 1);
+    barrier_nofence_a();  // tile t visible; every wave is done with the slot refilled next
+    if (t + D < ntiles) issue(t + D);
     const char* base = lds + (t % S) * STAGE;
 
     f32x16_t s2[2];
@@ -305,7 +327,7 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
       for (int r = 0; r < 16; ++r) s2[st][r] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + lq, ks * 2 + half));
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
         s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s2[st], 0, 0, 0);
       }
     }
@@ -321,7 +343,7 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = t0 + st * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          const int key = t0 + st * 32 + kperm(8 * (r >> 2) + 4 * half + (r & 3));
           if (key >= L) s2[st][r] = -INFINITY;
           mt = fmaxf(mt, s2[st][r]);
         }
@@ -348,23 +370,8 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
         psum += p;
       }
     l_run += psum;
-
 #pragma unroll
-    for (int jk = 0; jk < 4; ++jk) {
-      f16x8_t pf;
-      const int st = jk >> 1, r0 = (jk & 1) * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[st][r0 + e];
-      const int kA = jk * 16 + 4 * half, kB = kA + 8;
-#pragma unroll
-      for (int ds = 0; ds < 4; ++ds) {
-        const int d = ds * 32 + lq;
-        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kA >> 3) + (kA & 7) * 2);
-        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v_off(d, kB >> 3) + (kB & 7) * 2);
-        const f16x8_t vf = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
-        o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
-      }
-    }
+    for (int jk = 0; jk < 4; ++jk) pv_slice(base, jk, to_half(s2, jk));
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -488,8 +495,8 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
     for (int r = 0; r < 16; ++r) s2[r] = s2b[r] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 8; ks += 2) {
-      const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(base + k_off(lq, ks * 2 + half));
-      const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(base + k_off(lq, ks * 2 + 2 + half));
+      const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(base + k_off(kperm(lq), ks * 2 + half));
+      const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(base + k_off(kperm(lq), ks * 2 + 2 + half));
       s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s2, 0, 0, 0);
       s2b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks + 1], s2b, 0, 0, 0);
     }
@@ -502,7 +509,7 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
     } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = t0 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const int key = t0 + kperm(8 * (r >> 2) + 4 * half + (r & 3));
         if (key >= L) s2[r] = -INFINITY;
         mt = fmaxf(mt, s2[r]);
       }
@@ -532,14 +539,11 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
       f16x8_t pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[jk * 8 + e];
-      // slots 0-3: keys 16jk + 4*half + [0,4); slots 4-7: keys 16jk + 8 + 4*half + [0,4)
-      const int kA = jk * 16 + 4 * half, kB = kA + 8;
+      // slot e: key 16jk + 8*half + e (kperm), one 16-byte V^T chunk
 #pragma unroll
       for (int ds = 0; ds < 4; ++ds) {
         const int d = ds * 32 + lq;
-        const f16x4_t va = *reinterpret_cast<const f16x4_t*>(base + v2_off(d, kA >> 3) + (kA & 7) * 2);
-        const f16x4_t vb = *reinterpret_cast<const f16x4_t*>(base + v2_off(d, kB >> 3) + (kB & 7) * 2);
-        const f16x8_t vf = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
+        const f16x8_t vf = *reinterpret_cast<const f16x8_t*>(base + v2_off(d, 2 * jk + half));
         o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
       }
     }
