@@ -120,18 +120,28 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
     if (t + 1 < ntiles) gload((t + 1) * KT);
     const char* base = lds + buf * STAGE;
 
-    // S^T = K . Q^T for keys 32*st + (rows), queries = lanes
+    // S^T = K . Q^T for keys 32*st + (rows), queries = lanes; the K fragments
+    // are read ahead of their MFMAs
     f32x16_t s[2];
+    bf16x8_t kf[2][8];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+        kf[st][ks] = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[st][r] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
-        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[st], 0, 0, 0);
-      }
+      for (int ks = 0; ks < 8; ++ks) s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][ks], qf[ks], s[st], 0, 0, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    for (int x = 0; x < 8; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     // scale into the log2 domain, mask keys past L, tile max
     const int t0 = t * KT;
     float mt = -INFINITY;
@@ -290,16 +300,8 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
   float m_run = -INFINITY, l_run = 0.f;
   const float sc = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
 
-  // O^T += V^T P^T for one 16-key slice jk of a tile; P (half) slot e holds
-  // key 16 jk + 8 half + e (kperm), so the V^T operand is one 16-byte chunk
-  auto pv_slice = [&](const char* b_, int jk, const f16x8_t& pf) {
-#pragma unroll
-    for (int ds = 0; ds < 4; ++ds) {
-      const int d = ds * 32 + lq;
-      const f16x8_t vf = *reinterpret_cast<const f16x8_t*>(b_ + v_off(d, 2 * jk + half));
-      o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
-    }
-  };
+  // P (half) slot e of slice jk holds key 16 jk + 8 half + e (kperm), so a
+  // lane's V^T operand of the slice is the 16-byte chunk 2 jk + half of row d
   auto to_half = [&](const f32x16_t (&p2)[2], int jk) {
     f16x8_t pf;
 #pragma unroll
@@ -320,17 +322,29 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
     if (t + D < ntiles) issue(t + D);
     const char* base = lds + (t % S) * STAGE;
 
+    // S^T: all 16 K fragments are read before the MFMAs that use them, the
+    // second 32-key half's reads under the first half's MFMAs (read one,
+    // multiply one, each read waiting for its LDS round trip, runs ~2x slower)
     f32x16_t s2[2];
+    bf16x8_t kf[2][8];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+        kf[st][ks] = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) s2[st][r] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
-        s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s2[st], 0, 0, 0);
-      }
+      for (int ks = 0; ks < 8; ++ks) s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][ks], qf[ks], s2[st], 0, 0, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // the first half's K reads
+    for (int x = 0; x < 8; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA of the first half
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one K read of the second half
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     const int t0 = t * KT;
     float mt = -INFINITY;
     if (t0 + KT <= L) {
@@ -370,8 +384,28 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
         psum += p;
       }
     l_run += psum;
+    // O^T += V^T P^T: each slice's four V^T reads are issued under the
+    // previous slice's MFMAs
+    f16x8_t vf[2][4];
 #pragma unroll
-    for (int jk = 0; jk < 4; ++jk) pv_slice(base, jk, to_half(s2, jk));
+    for (int ds = 0; ds < 4; ++ds) vf[0][ds] = *reinterpret_cast<const f16x8_t*>(base + v_off(ds * 32 + lq, half));
+#pragma unroll
+    for (int jk = 0; jk < 4; ++jk) {
+      if (jk < 3) {
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds)
+          vf[(jk + 1) & 1][ds] = *reinterpret_cast<const f16x8_t*>(base + v_off(ds * 32 + lq, 2 * (jk + 1) + half));
+      }
+      const f16x8_t pf = to_half(s2, jk);
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[jk & 1][ds], pf, o[ds], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // slice 0's V^T reads
+    for (int x = 0; x < 12; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one V^T read of the next slice
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -489,16 +523,26 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
     if (t0 >= L) continue;  // this group has no keys left in the last step
     const char* base = lds + (u % S) * STEP2 + kg * TB2;
 
-    // two independent accumulation chains (even and odd 16-dim slices)
+    // two independent accumulation chains (even and odd 16-dim slices); the K
+    // fragments are read in batches of KPF ahead of the MFMAs that use them
+    // (two at three waves per SIMD, where eight would not fit the registers)
+    constexpr int KPF = QG == 3 ? 2 : 8;
     f32x16_t s2, s2b;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s2[r] = s2b[r] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < 8; ks += 2) {
-      const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(base + k_off(kperm(lq), ks * 2 + half));
-      const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(base + k_off(kperm(lq), ks * 2 + 2 + half));
-      s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s2, 0, 0, 0);
-      s2b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks + 1], s2b, 0, 0, 0);
+    for (int k0 = 0; k0 < 8; k0 += KPF) {
+      bf16x8_t kf[KPF];
+#pragma unroll
+      for (int i = 0; i < KPF; ++i)
+        kf[i] = *reinterpret_cast<const bf16x8_t*>(base + k_off(kperm(lq), (k0 + i) * 2 + half));
+#pragma unroll
+      for (int i = 0; i < KPF; i += 2) {
+        s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i], qf[k0 + i], s2, 0, 0, 0);
+        s2b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i + 1], qf[k0 + i + 1], s2b, 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, KPF, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, KPF, 0);
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) s2[r] += s2b[r];
@@ -534,17 +578,23 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
     }
     l_run += psum;
 
+    // slot e of slice jk: key 16jk + 8*half + e (kperm), one 16-byte V^T
+    // chunk; a slice's four V^T fragments are read before its MFMAs (left to
+    // the compiler at three waves per SIMD, short of registers)
 #pragma unroll
     for (int jk = 0; jk < 2; ++jk) {
+      f16x8_t vf[4];
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+        vf[ds] = *reinterpret_cast<const f16x8_t*>(base + v2_off(ds * 32 + lq, 2 * jk + half));
       f16x8_t pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[jk * 8 + e];
-      // slot e: key 16jk + 8*half + e (kperm), one 16-byte V^T chunk
 #pragma unroll
-      for (int ds = 0; ds < 4; ++ds) {
-        const int d = ds * 32 + lq;
-        const f16x8_t vf = *reinterpret_cast<const f16x8_t*>(base + v2_off(d, 2 * jk + half));
-        o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[ds], 0, 0, 0);
+      for (int ds = 0; ds < 4; ++ds) o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[ds], pf, o[ds], 0, 0, 0);
+      if (QG < 3) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
       }
     }
   }
