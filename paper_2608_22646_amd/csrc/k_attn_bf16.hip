@@ -49,6 +49,18 @@ __device__ __forceinline__ int v_off(int d, int chunk) {  // rows of 128 B, 8 ch
 // conflict-free ds_read_b128 instead of two 8-byte reads that two lanes of a
 // pass share banks with.
 __device__ __forceinline__ int kperm(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
+// max / sum of x over lanes l and l ^ 32 (the two halves holding one query's
+// scores): v_permlane32_swap with both operands x yields, at every lane, the
+// values of the lower and the upper half at that position -- a VALU exchange
+// instead of an LDS round trip (ds_bpermute)
+__device__ __forceinline__ float max_pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                                                            const f16_t* __restrict__ vt, bf16_t* __restrict__ out,
@@ -154,7 +166,7 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
         s[st][r] = x;
         mt = fmaxf(mt, x);
       }
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    mt = max_pair32(mt);
     const float m_new = fmaxf(m_run, mt);
     const float alpha = exp2_hw(m_run - m_new);
     m_run = m_new;
@@ -192,7 +204,7 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
     __syncthreads();
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = sum_pair32(l_run);
   const float inv = 1.0f / l_tot;
   const int qi = q0 + lq;
   if (qi >= Lq) return;
@@ -326,25 +338,27 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
     // second 32-key half's reads under the first half's MFMAs (read one,
     // multiply one, each read waiting for its LDS round trip, runs ~2x slower)
     f32x16_t s2[2];
-    bf16x8_t kf[2][8];
+    bf16x8_t kf[8][2];
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+        kf[ks][st] = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-        kf[st][ks] = *reinterpret_cast<const bf16x8_t*>(base + k_off(st * 32 + kperm(lq), ks * 2 + half));
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-#pragma unroll
       for (int r = 0; r < 16; ++r) s2[st][r] = 0.f;
+    // the two 32-key halves' accumulation chains alternate
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][ks], qf[ks], s2[st], 0, 0, 0);
+    for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+      for (int st = 0; st < 2; ++st) s2[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][st], qf[ks], s2[st], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);  // K reads run six ahead of their MFMAs
+    for (int x = 0; x < 10; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // the first half's K reads
-    for (int x = 0; x < 8; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA of the first half
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one K read of the second half
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
     const int t0 = t * KT;
     float mt = -INFINITY;
     if (t0 + KT <= L) {
@@ -362,7 +376,7 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
           mt = fmaxf(mt, s2[st][r]);
         }
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sc;
+    mt = max_pair32(mt) * sc;
     // raise the running maximum only when it grows by more than 2^8
     if (__ballot(mt > m_run + 8.0f) != 0ull) {
       const float m_new = fmaxf(m_run, mt);
@@ -408,7 +422,7 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = sum_pair32(l_run);
   const float inv = 1.0f / l_tot;
   const int qi = q0 + lq;
   if (qi >= Lq) return;
@@ -558,7 +572,7 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
         mt = fmaxf(mt, s2[r]);
       }
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sc;
+    mt = max_pair32(mt) * sc;
     if (__ballot(mt > m_run + 8.0f) != 0ull) {
       const float m_new = fmaxf(m_run, mt);
       const float alpha = exp2_hw(m_run - m_new);
@@ -654,7 +668,7 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
   // normalise and stage the wave's 32 output rows (bf16, 272-byte pitch) in
   // the hand-over slot of its group-1 partner, which only this wave reads,
   // then store them as whole 256-byte rows
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = sum_pair32(l_run);
   const float inv = 1.0f / l_tot;
   constexpr int OP = 272;
   char* stg = lds + (size_t)qg * XW * 4;
