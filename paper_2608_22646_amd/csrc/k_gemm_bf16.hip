@@ -1019,7 +1019,9 @@ void launch_splitk_resid(const float* part, float* resid, long MN, hipStream_t s
 }
 
 // The register-direct path: partials from gemm_rows_kernel, then the epilogue.
-void launch_gemm_rows(const GemmArgs& a, hipStream_t s) {
+// A residual GEMM's partials are left to the next norm when defer is given
+// (its 1024-thread fused kernel adds them), else reduced across the chip.
+void launch_gemm_rows(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   const RowsPlan rp = rows_plan(a.M, a.N, a.K);
   RowsArgs r{a.A, a.Wp, a.splitk_buf, a.M, a.N, a.K, rp.split, a.N / 32 / rp.gw};
   const dim3 grid(ceil_div(r.ngb * r.S, 4)), blk(256);
@@ -1045,6 +1047,8 @@ void launch_gemm_rows(const GemmArgs& a, hipStream_t s) {
   } else if (a.epi == EPI_QKV_ROPE) {
     const long n = (long)a.M * a.N;
     hipLaunchKernelGGL(splitk_qkv_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, a.splitk_buf, rp.split, a);
+  } else if (defer && a.M <= RESID_NORM_WIDE_ROWS) {
+    *defer = PendingResid{a.splitk_buf, rp.split};
   } else {
     const long MN = (long)a.M * a.N;
     switch (rp.split) {
@@ -1070,7 +1074,7 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   if (a.epi == EPI_QKV_ROPE && (a.Lq < 1 || a.pos0 < 0 || a.pos0 + a.Lq > a.L || a.M % a.Lq != 0))
     throw HipError("gemm_bf16: q/k/v rows must be whole windows of Lq positions inside the sequence");
   if (a.Wp && rows_path(a.M, a.N, a.K)) {  // few rows from the packed copy: register-direct
-    launch_gemm_rows(a, s);
+    launch_gemm_rows(a, s, defer);
     return;
   }
   const Plan p = plan(a.M, a.N, a.K, a.epi);

@@ -165,10 +165,13 @@ void launch_rmsnorm_t(const float* h, const TG* g, TO* out, int B, int rows, int
 // rmsnorm_vec_kernel preceded by the split-K residual update of its row: each
 // float4 of the row is h + ((p_0 + p_1) + ... + p_{S-1}), the same operations in
 // the same order as splitk_resid_kernel, written back to h and kept for the norm.
-template <int NV, int S>
-__global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ part,
-                                                            long MN, const bf16_t* __restrict__ g,
-                                                            bf16_t* __restrict__ out, int d, float eps) {
+// NT threads per row: 256, or 1024 for a few rows (a cached step's block
+// rows, whose register-direct GEMMs leave up to 16 partials): one workgroup per
+// row then has every partial load of the row in flight at once.
+template <int NV, int S, int NT = 256>
+__global__ void __launch_bounds__(NT) resid_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ part,
+                                                           long MN, const bf16_t* __restrict__ g,
+                                                           bf16_t* __restrict__ out, int d, float eps) {
   const int r = blockIdx.x;
   float* row = h + (size_t)r * d;
   const int d4 = d / 4;
@@ -176,7 +179,7 @@ __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ 
   double ss = 0.0;
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
-    const int c = threadIdx.x + 256 * j;
+    const int c = threadIdx.x + NT * j;
     if (c < d4) {
       const size_t i = (size_t)r * d4 + c;
       float4 acc = reinterpret_cast<const float4*>(part)[i];
@@ -200,15 +203,22 @@ __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ 
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
-  __shared__ double prt[4];
+  constexpr int NWV = NT / 64;
+  __shared__ double prt[NWV];
   if ((threadIdx.x & 63) == 0) prt[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const double tot = (prt[0] + prt[1]) + (prt[2] + prt[3]);
+  double tot = 0.0;
+  if (NWV == 4) {
+    tot = (prt[0] + prt[1]) + (prt[2] + prt[3]);
+  } else {
+#pragma unroll
+    for (int w = 0; w < NWV; ++w) tot += prt[w];
+  }
   const float rstd = (float)(1.0 / sqrt(tot / (double)d + (double)eps));
   bf16_t* dst = out + (size_t)r * d;
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
-    const int c = threadIdx.x + 256 * j;
+    const int c = threadIdx.x + NT * j;
     if (c < d4) {
       const float4 gg = Vec4<bf16_t>::load(g, c);
       Vec4<bf16_t>::store(dst, c, make_float4(v[j].x * rstd * gg.x, v[j].y * rstd * gg.y, v[j].z * rstd * gg.z,
@@ -223,8 +233,31 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
   if (d % 4 != 0 || d > 8192 || ((uintptr_t)h | (uintptr_t)pend.part | (uintptr_t)g | (uintptr_t)out) % 16 != 0)
     throw HipError("resid_rmsnorm: needs d % 4 == 0, d <= 8192 and 16-byte aligned rows");
   const long MN = (long)M * d;
-  const int nv = ceil_div(d, 1024);
   // the split count is a template parameter so that every partial's loads are in flight at once
+  if (M <= RESID_NORM_WIDE_ROWS) {
+    auto go = [&](auto nvc, auto sc) {
+      hipLaunchKernelGGL((resid_rmsnorm_kernel<decltype(nvc)::value, decltype(sc)::value, 1024>), dim3(M), dim3(1024),
+                         0, s, h, pend.part, MN, g, out, d, eps);
+    };
+    auto by_split = [&](auto nvc) {
+      switch (pend.split) {
+#define DLLM_CASE(S_) \
+  case S_: go(nvc, std::integral_constant<int, S_>{}); break;
+        DLLM_CASE(1) DLLM_CASE(2) DLLM_CASE(3) DLLM_CASE(4) DLLM_CASE(5) DLLM_CASE(6) DLLM_CASE(7) DLLM_CASE(8)
+        DLLM_CASE(9) DLLM_CASE(10) DLLM_CASE(11) DLLM_CASE(12) DLLM_CASE(13) DLLM_CASE(14) DLLM_CASE(15)
+        DLLM_CASE(16)
+#undef DLLM_CASE
+        default: throw HipError("resid_rmsnorm: split must be 1 .. 16");
+      }
+    };
+    if (d <= 4096)
+      by_split(std::integral_constant<int, 1>{});
+    else
+      by_split(std::integral_constant<int, 2>{});
+    DLLM_LAUNCH_CHECK("resid_rmsnorm");
+    return;
+  }
+  const int nv = ceil_div(d, 1024);
   auto go = [&](auto nvc, auto sc) {
     hipLaunchKernelGGL((resid_rmsnorm_kernel<decltype(nvc)::value, decltype(sc)::value>), dim3(M), dim3(256), 0, s, h,
                        pend.part, MN, g, out, d, eps);

@@ -78,6 +78,10 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer = nu
 // row m < M (bf16 model, d % 4 == 0, d <= 8192):
 //   h[m, :] += sum_z part[z, m, :]   (z in order, as the split-K reduction does)
 //   out[m, :] = bf16(RMSNorm(h[m, :]) * g)
+// Rows up to which the split-K partials of the register-direct GEMM (1 .. 16
+// of them) are left pending for the next norm, and the fused kernel runs one
+// 1024-thread workgroup per row (d <= 8192).
+constexpr int RESID_NORM_WIDE_ROWS = 64;
 void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, bf16_t* out, int M, int d, float eps,
                           hipStream_t s);
 // Packed copy of a GEMM's virtual weight matrix (g's W0/W1/W2, n0, n1, N, K,
