@@ -23,6 +23,7 @@ import sys
 import time
 
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X fp32 vector ALUs
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 
 
@@ -36,12 +37,15 @@ GEMM_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_26
                            "k_gemm_bf16.hip")
 
 
-def measured_traffic():
+def measured_traffic(workload):
     """HBM bytes per gate/up GEMM launch from the committed rocprofv3 counter
     summary (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading
-    for a plain copy of known size), or None when the summary is missing or was
-    taken on a different version of the GEMM source."""
+    for a plain copy of known size), or None when the summary is missing, was
+    taken on a different version of the GEMM source, or covers another
+    workload (the counters are taken on the LLaDA-8B batch-1 decode)."""
     import hashlib
+    if workload != "llada_b1":
+        return None
     try:
         fields = dict(l.split("=", 1) for l in open(TRAFFIC_SUMMARY).read().split("\n") if "=" in l)
         src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
@@ -450,6 +454,8 @@ def main():
         cpu = cpu_baseline(cfg, weights, prompts, wl, fwd_per_gen, args.cpu_budget)
         log(f"cpu baseline: {cpu['value']:.4f} tokens/s on {cpu['cores']} threads")
 
+    bf16 = cfg.dtype == "bf16"
+    peak = BF16_PEAK_TFLOPS if bf16 else FP32_VECTOR_PEAK_TFLOPS
     out = {
         "metric": "generated tokens/s (LLaDA-8B shape, gen 256) + forward MFMA util vs peak",
         "value": value,
@@ -467,9 +473,12 @@ def main():
                                f"block {bl}, gating {'on' if wl.gating else 'off'}",
                    "batch": B, "prompt_len": P, "gen_len": G, "block_len": bl,
                    "prompt_sets": args.steps, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "gate/up GEMM + SwiGLU (gemm_bf16_kernel, EPI_SWIGLU)",
-                     "achieved": gu_tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": gu_tflops / BF16_PEAK_TFLOPS, "traffic": measured_traffic(),
+        # the float32 model's GEMMs run on the vector ALUs (gemm_f32_kernel)
+        "roofline": {"bound": "mfma" if bf16 else "alu",
+                     "kernel": ("gate/up GEMM + SwiGLU (gemm_bf16_kernel, EPI_SWIGLU)" if bf16
+                                else "gate/up GEMM (gemm_f32_kernel)"),
+                     "achieved": gu_tflops, "peak": peak, "unit": "TFLOP/s",
+                     "frac": gu_tflops / peak, "traffic": measured_traffic(wl.name),
                      "flops_per_launch": flops["gate_up"], "avg_launch_us": gu_avg_s * 1e6,
                      "launches": gu_n},
         "cpu_baseline": cpu,
