@@ -100,6 +100,8 @@ using TileM = Tile<256, 192, 4, 2, 2>;
 using TileSM = Tile<128, 192, 2, 2, 3>;
 // the same on 8 waves in two k-groups
 using TileSM2 = Tile<128, 192, 2, 2, 3, 2>;
+// 128 x 128, 8 waves of 64 x 64 in two k-groups, four stages
+using TileQ = Tile<128, 128, 2, 2, 4, 2>;
 // 64 x 256, 8 waves of 64 x 64 in two k-groups: launches of a
 // few dozen rows (a cached step's block rows), where the weights' HBM stream
 // bounds the time and taller tiles only add MFMA and LDS work on padding rows
@@ -928,7 +930,7 @@ Plan plan(int M, int N, int K, int epi) {
     double t_kstep_us;
   };
   const Cand cands[] = {{128, 256, 1, 1.04}, {256, 256, 1, 1.71}, {256, 192, 1, 1.37}, {128, 192, 1, 0.87},
-                        {128, 192, 2, 0.81}, {64, 256, 2, 0.55}};
+                        {128, 192, 2, 0.81}, {64, 256, 2, 0.55}, {128, 128, 2, 0.46}};
   constexpr double BYTES_PER_US = 8.0e6;
   // the weights stream from HBM once per launch (tiles of one N range share
   // them through L2) at ~6.5 TB/s when every CU has a workgroup
@@ -938,6 +940,12 @@ Plan plan(int M, int N, int K, int epi) {
   const int ksteps = K / BK;
   for (const Cand& c : cands) {
     if (N % c.bn != 0 || (c.bm == 64 && M > 128)) continue;
+    // the 128 x 128 tile only where it measured faster: output projections
+    // (K <= 4096) of 160 .. 512 rows -- LLaDA-8B shape at 512 rows 29.5 + 8.8
+    // us for the GEMM and its reduction at split 2 against 33.4 + 11.3 for
+    // 128 x 256 at split 4, 23.4 against 26.2 us at 160 rows; it lost on the
+    // down projections (longer K) and at 768 rows (51.3 against 48.2 us)
+    if (c.bn == 128 && (epi != EPI_RESID || K > 4096 || M <= 128 || M > 512)) continue;
     const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
     const int max_split = M <= 128 ? 16 : 8;
     for (int split = 1; split <= max_split; ++split) {
@@ -976,6 +984,8 @@ void launch_epi(const GemmArgs& g, const Plan& p, hipStream_t s) {
     launch_tile<TileT, EPI, true>(g, p.split, s);
   else if (p.bm == 64)
     launch_tile<TileT, EPI>(g, p.split, s);
+  else if (p.bm == 128 && p.bn == 128)
+    launch_tile<TileQ, EPI>(g, p.split, s);
   else if (p.bm == 256 && p.bn == 256)
     launch_tile<TileL, EPI>(g, p.split, s);
   else if (p.bm == 256)
