@@ -11,8 +11,10 @@
  *  - Pointers documented "device" are HIP device memory owned by the caller;
  *    the library never frees them and keeps none after the call returns
  *    (except the weights borrowed by a model handle, see dllm_model_create).
- *  - The library allocates no device memory: scratch space is the caller's
- *    `workspace` of at least dllm_workspace_size() bytes, 256-byte aligned.
+ *  - Apart from the weight copies a model handle owns (the LM-head copy of
+ *    dllm_model_create, the copies of dllm_model_pack_weights), the library
+ *    allocates no device memory: scratch space is the caller's `workspace` of
+ *    at least dllm_workspace_size() bytes, 256-byte aligned.
  *  - `stream` is a hipStream_t passed as void*; NULL is the null stream.  All
  *    device work is enqueued on it in order; entry points return once the work
  *    is enqueued unless stated otherwise.
