@@ -435,6 +435,9 @@ def main():
         "forward_attention_mfma_frac": attn_flops / attn_s / 1e12 / BF16_PEAK_TFLOPS,
         "forward_mfma_frac_wall": flops["total"] * total_fwd / dt / 1e12 / BF16_PEAK_TFLOPS,
         "lm_head_hbm_frac": hbytes / head_s / 1e9 / HBM_PEAK_GBS,
+        # the commit kernel is latency-bound (~5 us for a few KB): conf, argmax,
+        # s and budget read, x and commit_step read and written, reason written
+        "commit_hbm_frac": B * bl * 33 / (breakdown["commit"]["ms_per_forward"] / 1e3) / 1e9 / HBM_PEAK_GBS,
         "kernel_ms_per_forward": {k: round(v["ms_per_forward"], 4) for k, v in breakdown.items()},
     }
     log(json.dumps(extra))
