@@ -205,21 +205,26 @@ def wide_packed():
     model.close()
 
 
-@pytest.mark.parametrize("which,Bn,P,G,blk", [("small", 2, 40, 64, 1), ("small", 1, 36, 96, 0),
-                                              ("small", 5, 40, 64, 1), ("small", 5, 36, 96, 2),
-                                              ("small_packed", 2, 40, 64, 1), ("small_packed", 1, 36, 96, 2),
-                                              ("small_packed", 3, 40, 64, 0), ("wide_packed", 1, 40, 64, 1),
-                                              ("wide_packed", 2, 36, 96, 2)])
-def test_bf16_refresh_cache_and_cached_layer_stages(request, which, Bn, P, G, blk):
+@pytest.mark.parametrize("which,Bn,P,G,blk,bl", [("small", 2, 40, 64, 1, 32), ("small", 1, 36, 96, 0, 32),
+                                                 ("small", 5, 40, 64, 1, 32), ("small", 5, 36, 96, 2, 32),
+                                                 ("small_packed", 2, 40, 64, 1, 32),
+                                                 ("small_packed", 1, 36, 96, 2, 32),
+                                                 ("small_packed", 3, 40, 64, 0, 32),
+                                                 ("small_packed", 3, 40, 64, 2, 16),
+                                                 ("wide_packed", 1, 40, 64, 1, 32),
+                                                 ("wide_packed", 2, 36, 96, 2, 32),
+                                                 ("wide_packed", 1, 40, 64, 3, 16)])
+def test_bf16_refresh_cache_and_cached_layer_stages(request, which, Bn, P, G, blk, bl):
     """Up to 128 block rows the q/k/v and SwiGLU GEMMs split K and run their
     epilogues on the summed partials; B = 5 (160 rows) runs the fused
     epilogues on the row window.  P = 36: block positions not a multiple of 8
     (the element-wise v^T path).  Packed weights: at most 64 rows (B <= 2) run
     the register-direct GEMM (32 rows: one row operand, 64: two), 96 rows
-    (B = 3) the tiled path."""
+    (B = 3) the tiled path; 16-row blocks give partial row operands (16 rows,
+    and 48 = B 3 x 16: the second operand half past the rows)."""
     model, wnp = request.getfixturevalue(which)
     cfg = model.cfg
-    L, bl = P + G, 32
+    L = P + G
     row0 = P + blk * bl
     say(f"bf16 kv stages {which} B={Bn} L={L} row0={row0}")
     x0 = synth.make_ints((Bn, L), 6, 0, cfg.vocab - 1)
