@@ -284,12 +284,16 @@ def test_bf16_packed_weights(small, small_packed, Bn):
         assert err.max().item() < 2e-2 * l0.abs().max().item() and err.mean().item() < 1e-2
 
 
-def test_bf16_generate_kv_replay(small):
-    model, _ = small
+@pytest.mark.parametrize("which,Bn", [("small", 2), ("small_packed", 2), ("small_packed", 3)])
+def test_bf16_generate_kv_replay(request, which, Bn):
+    """Cached decodes (refresh every 4 steps) replayed through the oracle
+    controller; packed weights: 64 block rows on the register-direct GEMM with
+    its partials folded into the next norm, 96 on the tiled path."""
+    model, _ = request.getfixturevalue(which)
     ctl = B.Controller()
-    Bn, P, G = 2, 24, 96
+    P, G = 24, 96
     prompts = synth.make_ints((Bn, P), 21, 0, SMALL.vocab - 1)
-    say("bf16 small generate_kv")
+    say(f"bf16 generate_kv {which} B={Bn}")
     res = model.generate_kv(ctl, prompts.cuda(), G, 4, trace=True)
     torch.cuda.synchronize()
     ref = replay(res.conf_trace.cpu().numpy(), res.argmax_trace.cpu().numpy(), prompts.numpy(), G, SMALL.mask_id,
