@@ -30,6 +30,19 @@ constexpr int HD = 128, KT = 64, QW = 32, NW = 4;
 // sum that is at least 1, where values below 2^-126 are zero anyway.  exp2f
 // spends five more VALU instructions per element on that rescaling.
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// (query block, head, sequence) of this workgroup in a 1-D grid of
+// nqb x Hq x B workgroups.  Workgroup i runs on XCD i % 8; each XCD takes a
+// contiguous run of the (sequence, head, query block) order, so the query
+// blocks of one head, which all read that head's keys and values, share one
+// XCD's L2 (in grid order they were spread over all eight).
+__device__ __forceinline__ int3 attn_block(int nqb, int Hq) {
+  const int T = (int)gridDim.x, per = T >> 3, rem = T & 7;
+  const int i = (int)blockIdx.x, x = i & 7;
+  const int lin = x * per + min(x, rem) + (i >> 3);
+  const int qb = lin % nqb, r = lin / nqb;
+  return make_int3(qb, r % Hq, r / Hq);
+}
 constexpr int K_BYTES = KT * HD * 2, V_BYTES = HD * KT * 2, STAGE = K_BYTES + V_BYTES;
 
 // XOR swizzles sized for the 64 banks (256 bytes) that one 16-lane pass of
@@ -67,8 +80,9 @@ __global__ void __launch_bounds__(256, 1) attn_bf16_kernel(const bf16_t* __restr
                                                            int Lq, int L, int Hq, int Hkv) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
-  const int q0 = blockIdx.x * (QW * NW) + wave * QW;
+  const int3 wb = attn_block((Lq + QW * NW - 1) / (QW * NW), Hq);
+  const int h = wb.y, b = wb.z, g = h / (Hq / Hkv);
+  const int q0 = wb.x * (QW * NW) + wave * QW;
   const int lq = lane & 31, half = lane >> 5;
   const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
   const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
@@ -257,8 +271,9 @@ __global__ void __launch_bounds__(64 * NW, 1) attn_stream_kernel(const bf16_t* _
   constexpr int D = 2, S = D + 1, PER_STAGE = 32 / NW;  // 16 K + 16 V^T DMA instructions per tile
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
-  const int q0 = blockIdx.x * (QW * NW) + wave * QW;
+  const int3 wb = attn_block((Lq + QW * NW - 1) / (QW * NW), Hq);
+  const int h = wb.y, b = wb.z, g = h / (Hq / Hkv);
+  const int q0 = wb.x * (QW * NW) + wave * QW;
   const int lq = lane & 31, half = lane >> 5;
   const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
   const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
@@ -465,8 +480,9 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qg = wave % QG, kg = wave / QG;
-  const int h = blockIdx.y, b = blockIdx.z, g = h / (Hq / Hkv);
-  const int q0 = blockIdx.x * (QW * QG) + qg * QW;
+  const int3 wb = attn_block((Lq + QW * QG - 1) / (QW * QG), Hq);
+  const int h = wb.y, b = wb.z, g = h / (Hq / Hkv);
+  const int q0 = wb.x * (QW * QG) + qg * QW;
   const int lq = lane & 31, half = lane >> 5;
   const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
   const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
@@ -717,7 +733,7 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
         static const hipError_t a = hipFuncSetAttribute((const void*)attn_kv4_kernel<QG>,
                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_kv);
         hip_check(a, "hipFuncSetAttribute(attn_kv4)");
-        hipLaunchKernelGGL(attn_kv4_kernel<QG>, dim3(ceil_div(Lq, QW * QG), Hq, B), dim3(64 * QG * KGRP), lds_kv, s,
+        hipLaunchKernelGGL(attn_kv4_kernel<QG>, dim3(ceil_div(Lq, QW * QG) * Hq * B), dim3(64 * QG * KGRP), lds_kv, s,
                            q, k, vt, out, Lq, L, Hq, Hkv);
       };
       if (Lq <= QW)
@@ -733,13 +749,13 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
       static const hipError_t a8 =
           hipFuncSetAttribute((const void*)attn_stream_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       hip_check(a8, "hipFuncSetAttribute(attn_stream<8>)");
-      hipLaunchKernelGGL(attn_stream_kernel<8>, dim3(ceil_div(Lq, QW * 8), Hq, B), dim3(512), lds, s, q, k, vt, out,
+      hipLaunchKernelGGL(attn_stream_kernel<8>, dim3(ceil_div(Lq, QW * 8) * Hq * B), dim3(512), lds, s, q, k, vt, out,
                          Lq, L, Hq, Hkv);
     } else {
       static const hipError_t a4 =
           hipFuncSetAttribute((const void*)attn_stream_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       hip_check(a4, "hipFuncSetAttribute(attn_stream<4>)");
-      hipLaunchKernelGGL(attn_stream_kernel<4>, dim3(ceil_div(Lq, QW * 4), Hq, B), dim3(256), lds, s, q, k, vt, out,
+      hipLaunchKernelGGL(attn_stream_kernel<4>, dim3(ceil_div(Lq, QW * 4) * Hq * B), dim3(256), lds, s, q, k, vt, out,
                          Lq, L, Hq, Hkv);
     }
     DLLM_LAUNCH_CHECK("attn_stream");
@@ -748,7 +764,7 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)attn_bf16_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * STAGE);
   hip_check(attr, "hipFuncSetAttribute(attn_bf16)");
-  hipLaunchKernelGGL(attn_bf16_kernel, dim3(ceil_div(Lq, QW * NW), Hq, B), dim3(256), 2 * STAGE, s, q, k, vt, out, Lq,
+  hipLaunchKernelGGL(attn_bf16_kernel, dim3(ceil_div(Lq, QW * NW) * Hq * B), dim3(256), 2 * STAGE, s, q, k, vt, out, Lq,
                      L, Hq, Hkv);
   DLLM_LAUNCH_CHECK("attn_bf16");
 }
