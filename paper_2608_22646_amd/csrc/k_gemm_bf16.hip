@@ -595,8 +595,14 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int tiles = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
   // workgroup i runs on XCD i % 8: give each XCD a contiguous run of the order
+  // (XCD x takes tiles / 8 of them, one more for the first tiles % 8 XCDs).
+  // With split-K the XCD of (tile, split) is that of the tile only when the
+  // tile count is a multiple of 8; otherwise the order is left as it is.
   int lin = blockIdx.x;
-  if ((tiles & 7) == 0) lin = (blockIdx.x & 7) * (tiles >> 3) + (blockIdx.x >> 3);
+  if (gridDim.z == 1 || (tiles & 7) == 0) {
+    const int x = blockIdx.x & 7;
+    lin = x * (tiles >> 3) + min(x, tiles & 7) + (blockIdx.x >> 3);
+  }
   const int2 o = tile_origin<TL>(g, lin);
   // K slice z of S: k-steps [z KS / S, (z + 1) KS / S)
   const int ks_total = g.K / BK;
