@@ -594,20 +594,17 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
   // wave index made provably uniform so per-wave buffer descriptors stay scalar
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int tiles = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
-  // workgroup i runs on XCD i % 8: give each XCD a contiguous run of the order
-  // (XCD x takes tiles / 8 of them, one more for the first tiles % 8 XCDs).
-  // With split-K the XCD of (tile, split) is that of the tile only when the
-  // tile count is a multiple of 8; otherwise the order is left as it is.
-  int lin = blockIdx.x;
-  if (gridDim.z == 1 || (tiles & 7) == 0) {
-    const int x = blockIdx.x & 7;
-    lin = x * (tiles >> 3) + min(x, tiles & 7) + (blockIdx.x >> 3);
-  }
+  // workgroup i (in x, then z order) runs on XCD i % 8: give each XCD a
+  // contiguous run of the (split, tile) order -- XCD x takes T / 8 of the
+  // T = tiles x splits workgroups, one more for the first T % 8 XCDs
+  const int T = tiles * (int)gridDim.z, i = blockIdx.x + tiles * blockIdx.z, x = i & 7;
+  const int li = x * (T >> 3) + min(x, T & 7) + (i >> 3);
+  const int lin = li % tiles, zs = li / tiles;
   const int2 o = tile_origin<TL>(g, lin);
   // K slice z of S: k-steps [z KS / S, (z + 1) KS / S)
   const int ks_total = g.K / BK;
-  const int kt0 = (int)((long)blockIdx.z * ks_total / gridDim.z);
-  const int nk = (int)((long)(blockIdx.z + 1) * ks_total / gridDim.z) - kt0;
+  const int kt0 = (int)((long)zs * ks_total / gridDim.z);
+  const int nk = (int)((long)(zs + 1) * ks_total / gridDim.z) - kt0;
 
   f32x16_t acc[TL::TI][TL::TJ];
   zero_acc<TL>(acc);
@@ -653,7 +650,7 @@ __global__ void __launch_bounds__(TL::NTH, 1) gemm_bf16_kernel(GemmArgs g) {
   if (gridDim.z > 1) {  // split-K partial tile
     const int wm = (wave % TL::NWT) / (TL::BN / TL::WN), wn = (wave % TL::NWT) % (TL::BN / TL::WN);
     const int lhalf = lane >> 5, col_in = lane & 31;
-    float* part = g.splitk_buf + (size_t)blockIdx.z * g.M * g.N;
+    float* part = g.splitk_buf + (size_t)zs * g.M * g.N;
 #pragma unroll
     for (int i = 0; i < TL::TI; ++i)
 #pragma unroll
