@@ -943,13 +943,18 @@ Plan plan(int M, int N, int K, int epi) {
   const int ksteps = K / BK;
   for (const Cand& c : cands) {
     if (N % c.bn != 0 || (c.bm == 64 && M > 128)) continue;
+    const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
     // the 128 x 128 tile only where it measured faster: output projections
     // (K <= 4096) of 160 .. 512 rows -- LLaDA-8B shape at 512 rows 29.5 + 8.8
     // us for the GEMM and its reduction at split 2 against 33.4 + 11.3 for
     // 128 x 256 at split 4, 23.4 against 26.2 us at 160 rows; it lost on the
-    // down projections (longer K) and at 768 rows (51.3 against 48.2 us)
-    if (c.bn == 128 && (epi != EPI_RESID || K > 4096 || M <= 128 || M > 512)) continue;
-    const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
+    // down projections (longer K) and at 768 rows (51.3 against 48.2 us) --
+    // and q/k/v launches whose 128 x 128 tiles fit one round on the CUs
+    // (Dream-7B shape at 768 rows: 216 tiles, 46 against 57 us for 144 tiles
+    // of 128 x 192; at 384 tiles, LLaDA-8B at 512 rows, it lost: 95 against 72)
+    if (c.bn == 128 && !(M > 128 && ((epi == EPI_RESID && K <= 4096 && M <= 512) ||
+                                     (epi == EPI_QKV_ROPE && tiles <= 256))))
+      continue;
     const int max_split = M <= 128 ? 16 : 8;
     for (int split = 1; split <= max_split; ++split) {
       if (split > 1 && ((epi != EPI_RESID && M > 128) || ksteps / split < 4)) break;
