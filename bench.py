@@ -31,25 +31,30 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-TRAFFIC_SUMMARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                               "gemm_gateup_llada_b1_traffic.txt")
-GEMM_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_22646_amd", "csrc",
-                           "k_gemm_bf16.hip")
+PROFILES = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles")
+CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_22646_amd", "csrc")
+# committed rocprofv3 counter summaries: (file, source of the counted kernel, key of its hash)
+TRAFFIC = {
+    "gate_up": ("gemm_gateup_llada_b1_traffic.txt", "k_gemm_bf16.hip", "gemm_source_sha256"),
+    "lm_head": ("head_stream_llada_b1_traffic.txt", "k_head_bf16.hip", "head_source_sha256"),
+}
 
 
-def measured_traffic(workload):
-    """HBM bytes per gate/up GEMM launch from the committed rocprofv3 counter
-    summary (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading
-    for a plain copy of known size), or None when the summary is missing, was
-    taken on a different version of the GEMM source, or covers another
-    workload (the counters are taken on the LLaDA-8B batch-1 decode)."""
+def measured_traffic(workload, kernel="gate_up"):
+    """HBM bytes per launch of the gate/up GEMM (or the LM head) from the
+    committed rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, each scaled by
+    the same counter's reading for a plain copy of known size), or None when the
+    summary is missing, was taken on a different version of the kernel's
+    source, or covers another workload (the counters are taken on the LLaDA-8B
+    batch-1 decode)."""
     import hashlib
     if workload != "llada_b1":
         return None
+    summary, source, key = TRAFFIC[kernel]
     try:
-        fields = dict(l.split("=", 1) for l in open(TRAFFIC_SUMMARY).read().split("\n") if "=" in l)
-        src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
-        if fields.get("gemm_source_sha256", "").strip() != src:
+        fields = dict(l.split("=", 1) for l in open(os.path.join(PROFILES, summary)).read().split("\n") if "=" in l)
+        src = hashlib.sha256(open(os.path.join(CSRC, source), "rb").read()).hexdigest()
+        if fields.get(key, "").strip() != src:
             return None
         return float(fields["traffic_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
@@ -435,6 +440,8 @@ def main():
         "forward_attention_mfma_frac": attn_flops / attn_s / 1e12 / BF16_PEAK_TFLOPS,
         "forward_mfma_frac_wall": flops["total"] * total_fwd / dt / 1e12 / BF16_PEAK_TFLOPS,
         "lm_head_hbm_frac": hbytes / head_s / 1e9 / HBM_PEAK_GBS,
+        # algorithmic bytes of one LM-head launch and what the HBM counters read
+        "lm_head_bytes": {"algorithmic": hbytes, "traffic": measured_traffic(wl.name, "lm_head")},
         # the commit kernel is latency-bound (~5 us for a few KB): conf, argmax,
         # s and budget read, x and commit_step read and written, reason written
         "commit_hbm_frac": B * bl * 33 / (breakdown["commit"]["ms_per_forward"] / 1e3) / 1e9 / HBM_PEAK_GBS,

@@ -49,7 +49,10 @@ def traffic(fetch, write, cfetch, cwrite, substr, copy_bytes, command):
     ff = exp_kib / copy_reading(cfetch)
     fw = exp_kib / copy_reading(cwrite)
     tb = (f_kib * ff + w_kib * fw) * 1024.0
-    src = os.path.join(HERE, "csrc", "k_gemm_bf16.hip")
+    # the source the counted kernel is built from, hashed so that a reader of
+    # the summary can tell when the kernel has changed since
+    name = "head" if "head_stream" in substr else "gemm"
+    src = os.path.join(HERE, "csrc", "k_head_bf16.hip" if name == "head" else "k_gemm_bf16.hip")
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
     print(f"# HBM traffic of one launch from rocprofv3 --pmc counters\n# command: {command}")
     print(f"# kernel: launches whose name contains '{substr}'")
@@ -61,7 +64,7 @@ def traffic(fetch, write, cfetch, cwrite, substr, copy_bytes, command):
     print(f"fetch_scale={ff:.4f}")
     print(f"write_scale={fw:.4f}")
     print(f"traffic_bytes_per_launch={tb:.0f}")
-    print(f"gemm_source_sha256={sha}")
+    print(f"{name}_source_sha256={sha}")
 
 
 if __name__ == "__main__":
