@@ -24,6 +24,12 @@ Precision modes
            bf16 (round-to-nearest-even) where they are produced -- while the
            residual stream, norm statistics, softmax and SiLU stay in float64
            and products accumulate in float32 (BLAS sgemm).
+  "bf16_f64acc" : the same rounding points as "bf16", but every matrix
+           product accumulates in float64.  Not a model of any kernel: it
+           measures how far two correct float32 accumulation orders of one
+           bf16 model can drift apart once bf16 rounding of the activations
+           turns last-bit differences into whole bf16 steps (the bar that
+           end-to-end bf16 logits are held to is set from that drift).
 
 Test infrastructure only; see the package docstring.
 """
@@ -92,7 +98,7 @@ def attention(q, k, v, mode="f64"):
     hkv = k.shape[0]
     group = hq // hkv
     scale = 1.0 / math.sqrt(hd)
-    dt = np.float64 if mode == "f64" else np.float32
+    dt = np.float32 if mode == "bf16" else np.float64
     out = np.empty((hq, L, hd), dtype=np.float64)
     for h in range(hq):
         kv = h // group
@@ -103,15 +109,15 @@ def attention(q, k, v, mode="f64"):
 
 
 def _matmul(a, w, mode):
-    """a [M, K] @ w[N, K]^T: float64 in "f64" mode, float32 BLAS in "bf16" mode."""
-    if mode == "f64":
+    """a [M, K] @ w[N, K]^T: float32 BLAS in "bf16" mode, float64 otherwise."""
+    if mode != "bf16":
         return np.asarray(a, np.float64) @ np.asarray(w, np.float64).T
     return (np.asarray(a, np.float32) @ np.asarray(w, np.float32).T).astype(np.float64)
 
 
 def _op(x, mode):
-    """Value handed to a matrix product: bf16-rounded in "bf16" mode."""
-    return round_bf16(x).astype(np.float64) if mode == "bf16" else np.asarray(x, np.float64)
+    """Value handed to a matrix product: bf16-rounded in the bf16 modes."""
+    return round_bf16(x).astype(np.float64) if mode != "f64" else np.asarray(x, np.float64)
 
 
 def norm_in(h, gain, eps, mode):

@@ -26,8 +26,12 @@ def confidence_argmax(logits, mask_id):
 
 
 def top2_gap(logits, mask_id):
-    """Gap between the largest and second-largest logit (mask excluded); used to
-    flag near-ties where two correct implementations may pick different tokens."""
+    """logits [..., V] -> float64 [...]: the largest logit over v != mask_id minus
+    the largest logit of any other index v != mask_id (0 at a tie for the top,
+    +inf when only one finite candidate exists).
+
+    Used to excuse near-ties: if two logit rows differ by at most e in every
+    entry, their argmaxes can differ only where this gap is at most 2 e."""
     l = np.array(logits, dtype=np.float64, copy=True)
     l[..., mask_id] = -np.inf
     part = np.sort(l, axis=-1)

@@ -111,27 +111,30 @@ def weight_specs(cfg: ModelConfig):
     return specs
 
 
-def make_weights(cfg: ModelConfig, device="cpu"):
-    """Seeded random weights in the fixed order, stored in ``cfg.torch_dtype``.
+def make_weight(cfg: ModelConfig, i: int, device="cpu"):
+    """Tensor i of the fixed order (seed 1234 + i), stored in ``cfg.torch_dtype``.
 
     Draws use torch's generator for ``device`` (the CPU and GPU generators give
     different streams; a parity test always hands the same tensors to both
     sides).  bf16 storage rounds the fp32 draw to nearest-even.
     """
-    out = []
-    for i, (_, shape, std) in enumerate(weight_specs(cfg)):
-        g = torch.Generator(device=device)
-        g.manual_seed(WEIGHT_SEED_BASE + i)
-        if std is None:
-            if cfg.norm_gain_std > 0:
-                w = 1.0 + cfg.norm_gain_std * torch.randn(shape, generator=g, device=device)
-            else:
-                w = torch.ones(shape, device=device)
+    _, shape, std = weight_specs(cfg)[i]
+    g = torch.Generator(device=device)
+    g.manual_seed(WEIGHT_SEED_BASE + i)
+    if std is None:
+        if cfg.norm_gain_std > 0:
+            w = 1.0 + cfg.norm_gain_std * torch.randn(shape, generator=g, device=device)
         else:
-            w = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
-            w.mul_(std)
-        out.append(w.to(cfg.torch_dtype).contiguous())
-    return out
+            w = torch.ones(shape, device=device)
+    else:
+        w = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+        w.mul_(std)
+    return w.to(cfg.torch_dtype).contiguous()
+
+
+def make_weights(cfg: ModelConfig, device="cpu"):
+    """Every tensor of the fixed order (make_weight)."""
+    return [make_weight(cfg, i, device) for i in range(cfg.n_weights)]
 
 
 def make_prompts(wl: Workload, device="cpu", first=0):

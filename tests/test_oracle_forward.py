@@ -136,6 +136,64 @@ def test_confidence_argmax():
     assert c[0] == pytest.approx(1 / (V - 1), rel=1e-13)
 
 
+def _gap_by_definition(row, mask):
+    """Largest logit minus the largest logit of any other index (mask excluded),
+    by a plain scan: the distance by which the argmax leads its runner-up."""
+    best, best_i = -math.inf, -1
+    for i, v in enumerate(row):
+        if i != mask and v > best:
+            best, best_i = v, i
+    second = -math.inf
+    for i, v in enumerate(row):
+        if i != mask and i != best_i and v > second:
+            second = v
+    return best - second
+
+
+def test_top2_gap():
+    V, mask = 12, 11
+    # hand rows with a known lead
+    row = np.array([0.5, 3.0, -1.0, 2.25, 0.0, 2.9, 1.0, -4.0, 0.0, 0.0, 0.0, 0.0])
+    assert ov.top2_gap(row, mask) == pytest.approx(0.1, abs=1e-15)
+    row2 = np.zeros(V)
+    row2[4] = 7.0
+    row2[9] = -3.5
+    assert ov.top2_gap(row2, mask) == 7.0          # runner-up is one of the zeros
+    # ties at the top: gap 0 (either index is a correct argmax)
+    row3 = row.copy()
+    row3[5] = 3.0
+    assert ov.top2_gap(row3, mask) == 0.0
+    # the mask id holding the largest logit is ignored on both places
+    row4 = row.copy()
+    row4[mask] = 50.0
+    assert ov.top2_gap(row4, mask) == pytest.approx(0.1, abs=1e-15)
+    row5 = row.copy()
+    row5[mask] = 2.95                               # between the leader and the runner-up
+    assert ov.top2_gap(row5, mask) == pytest.approx(0.1, abs=1e-15)
+    # -inf entries: a single finite candidate leads by +inf; -inf never is the runner-up
+    row6 = np.full(V, -np.inf)
+    row6[3] = 1.0
+    assert ov.top2_gap(row6, mask) == np.inf
+    row6[7] = -2.0
+    assert ov.top2_gap(row6, mask) == 3.0
+    # batched rows, brute force on random logits with planted ties and masks on top
+    l = rng.standard_normal((40, 37)) * 3
+    l[::5, 8] = l[::5, 20] = l[::5].max(axis=1) + 1.0    # ties at the top
+    l[1::7, 36] = 99.0                                     # mask id on top
+    g = ov.top2_gap(l, 36)
+    assert g.shape == (40,)
+    for r in range(40):
+        assert g[r] == _gap_by_definition(l[r], 36), r
+    # the property the GPU tests rely on: two logit rows within e of each other
+    # can only disagree on the argmax where the reference's gap is at most 2 e
+    for trial in range(200):
+        ref = rng.standard_normal(50) * 2
+        e = 10.0 ** rng.uniform(-6, 0)
+        got = ref + rng.uniform(-e, e, 50)
+        if ov.confidence_argmax(got[None], 49)[1][0] != ov.confidence_argmax(ref[None], 49)[1][0]:
+            assert ov.top2_gap(ref, 49) <= 2 * e
+
+
 def _torch_forward(cfg, weights, tokens, bf16):
     """The same model built from torch float64 library routines (rms_norm,
     complex-rotation RoPE, scaled_dot_product_attention with GQA, silu, linear)."""
@@ -197,6 +255,20 @@ def test_forward_bf16_matches_torch_library_model():
     assert err.mean() < 5e-4 and err.max() < 5e-2, (err.mean(), err.max())
     err64 = np.abs(of.forward(cfg, w, tokens, mode="f64") - want)
     assert err64.mean() > 20 * err.mean()
+
+
+def test_forward_bf16_f64acc_matches_torch_library_model():
+    # the same rounding points as "bf16" with float64 products: the torch float64
+    # model with bf16 rounding is that definition, so the two agree to float64
+    # rounding through several layers (no bf16 flips at float64 precision)
+    cfg = synth.reduced(TINY_GQA, dtype="bf16", n_layers=2)
+    w = [t.to(torch.float32).numpy() for t in synth.make_weights(cfg)]
+    tokens = rng.integers(0, cfg.vocab, (2, 19))
+    want = _torch_forward(cfg, w, tokens, bf16=True)
+    got = of.forward(cfg, w, tokens, mode="bf16_f64acc")
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-9)
+    # float32 accumulation ("bf16") is a different model at the bf16-flip level
+    assert np.abs(of.forward(cfg, w, tokens, mode="bf16") - want).max() > 1e-7
 
 
 def test_forward_bidirectional_and_position_sensitive():
