@@ -23,7 +23,7 @@ import sys
 import time
 
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
-FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X fp32 vector ALUs
+FP64_VECTOR_PEAK_TFLOPS = 78.6    # MI355X fp64 vector ALUs (the float32 model's GEMMs accumulate in fp64 FMAs)
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 
 
@@ -91,6 +91,35 @@ def head_bytes(cfg, R):
     return cfg.vocab * cfg.d_model * 2 + R * cfg.d_model * 2 + R * 8
 
 
+def host_machine():
+    """(BLAS threads the oracle's matrix products use, a description of the host):
+    os.cpu_count(), the CPU model string and the BLAS library."""
+    import platform
+    threads, blas = os.cpu_count() or 1, None
+    try:
+        from threadpoolctl import threadpool_info
+        pools = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if pools:
+            threads = max(i.get("num_threads", 1) for i in pools)
+            blas = f"{pools[0].get('internal_api')} {pools[0].get('version')}"
+    except Exception:
+        pass
+    model = platform.processor() or None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = None
+    return threads, {"cpu_count": os.cpu_count(), "cpus_available": affinity, "blas_threads": threads,
+                     "blas": blas, "cpu_model": model}
+
+
 def cpu_baseline(cfg, weights, prompts, wl, forwards_per_gen, budget_s=25.0):
     """The oracle (numpy, float32 matrix products) on the first denoising step of
     the workload: embedding, as many layers as fit in ~budget_s, the final norm +
@@ -102,11 +131,7 @@ def cpu_baseline(cfg, weights, prompts, wl, forwards_per_gen, budget_s=25.0):
     from oracle import controller as oc
     from oracle import forward as of
     from oracle import vocab as ov
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    threads, machine = host_machine()
 
     def host(t):
         return t.to("cpu").to(torch.float32).numpy()
@@ -141,7 +166,7 @@ def cpu_baseline(cfg, weights, prompts, wl, forwards_per_gen, budget_s=25.0):
     s_per_forward = t_embed + per_layer * cfg.n_layers + t_head
     tok_s = B * G / (s_per_forward * forwards_per_gen)
     return {
-        "value": tok_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "value": tok_s, "unit": "tokens/s", "cores": threads, "kind": "oracle", **machine,
         "sample": (f"first denoising step of the workload: embedding, {len(layer_times)} of {cfg.n_layers} "
                    f"layers timed ({per_layer:.2f} s/layer, extrapolated to all layers), final norm + LM head + "
                    f"confidence reduction + controller step ({t_head:.2f} s); {s_per_forward:.1f} s per forward "
@@ -446,6 +471,11 @@ def main():
         # s and budget read, x and commit_step read and written, reason written
         "commit_hbm_frac": B * bl * 33 / (breakdown["commit"]["ms_per_forward"] / 1e3) / 1e9 / HBM_PEAK_GBS,
         "kernel_ms_per_forward": {k: round(v["ms_per_forward"], 4) for k, v in breakdown.items()},
+        # wall time per forward in the timed decodes (the per-class times above
+        # come from a separate pass with events around every class, which adds
+        # their own overhead: the launch-gap budget is read from rocprofv3 traces)
+        "wall_ms_per_forward": dt / total_fwd * 1e3,
+        "launch_groups_per_forward": sum(v["launches_per_forward"] for v in breakdown.values()),
     }
     log(json.dumps(extra))
 
@@ -465,7 +495,7 @@ def main():
         log(f"cpu baseline: {cpu['value']:.4f} tokens/s on {cpu['cores']} threads")
 
     bf16 = cfg.dtype == "bf16"
-    peak = BF16_PEAK_TFLOPS if bf16 else FP32_VECTOR_PEAK_TFLOPS
+    peak = BF16_PEAK_TFLOPS if bf16 else FP64_VECTOR_PEAK_TFLOPS
     out = {
         "metric": "generated tokens/s (LLaDA-8B shape, gen 256) + forward MFMA util vs peak",
         "value": value,
@@ -483,10 +513,10 @@ def main():
                                f"block {bl}, gating {'on' if wl.gating else 'off'}",
                    "batch": B, "prompt_len": P, "gen_len": G, "block_len": bl,
                    "prompt_sets": args.steps, "parallelism": "single GPU"},
-        # the float32 model's GEMMs run on the vector ALUs (gemm_f32_kernel)
+        # the float32 model's GEMMs run on the vector ALUs in fp64 FMAs (gemm_f32_kernel)
         "roofline": {"bound": "mfma" if bf16 else "alu",
                      "kernel": ("gate/up GEMM + SwiGLU (gemm_bf16_kernel, EPI_SWIGLU)" if bf16
-                                else "gate/up GEMM (gemm_f32_kernel)"),
+                                else "gate/up GEMM (gemm_f32_kernel, float64 FMAs)"),
                      "achieved": gu_tflops, "peak": peak, "unit": "TFLOP/s",
                      "frac": gu_tflops / peak, "traffic": measured_traffic(wl.name),
                      "flops_per_launch": flops["gate_up"], "avg_launch_us": gu_avg_s * 1e6,

@@ -9,12 +9,16 @@
  *
  * Conventions (every entry point):
  *  - Pointers documented "device" are HIP device memory owned by the caller;
- *    the library never frees them and keeps none after the call returns
- *    (except the weights borrowed by a model handle, see dllm_model_create).
- *  - Apart from the weight copies a model handle owns (the LM-head copy of
- *    dllm_model_create, the copies of dllm_model_pack_weights), the library
- *    allocates no device memory: scratch space is the caller's `workspace` of
- *    at least dllm_workspace_size() bytes, 256-byte aligned.
+ *    the library never frees them and keeps none after the call returns,
+ *    except those a model handle borrows for its lifetime: the weights, the
+ *    model buffer of dllm_model_create and the buffer of
+ *    dllm_model_pack_weights.
+ *  - The library allocates no device memory.  Every buffer is the caller's,
+ *    sized by a query: the model buffer (dllm_model_buffer_size), the packed
+ *    weights (dllm_model_packed_size), the workspace (dllm_workspace_size) and
+ *    the key/value cache (dllm_kv_cache_size), each 256-byte aligned.  The
+ *    only other resources are host objects of a model handle (one pinned host
+ *    word for the per-step flag read-back, timing events).
  *  - `stream` is a hipStream_t passed as void*; NULL is the null stream.  All
  *    device work is enqueued on it in order; entry points return once the work
  *    is enqueued unless stated otherwise.
@@ -146,6 +150,13 @@ typedef struct dllm_state {
 typedef struct dllm_model dllm_model;
 
 /*
+ * Bytes of the model buffer dllm_model_create needs for cfg: the bf16 LM
+ * head's tiled copy (ceil(V/256)*256*d bf16 values, rounded up to 256 bytes);
+ * 0 for a DLLM_F32 model.  Errors as for dllm_model_create's shape checks.
+ */
+int dllm_model_buffer_size(const dllm_model_cfg* cfg, size_t* bytes);
+
+/*
  * Create a model handle from caller-owned device weights (borrowed for the
  * handle's lifetime).  `weights` is a host array of n_weights =
  * 3 + 9*n_layers device pointers in this order, each row-major, of cfg.dtype
@@ -153,35 +164,38 @@ typedef struct dllm_model dllm_model;
  *   embed [V, d]; per layer: attn_norm [d], wq [Hq*hd, d], wk [Hkv*hd, d],
  *   wv [Hkv*hd, d], wo [d, Hq*hd], mlp_norm [d], w_gate [F, d], w_up [F, d],
  *   w_down [d, F]; then final_norm [d], lm_head [V, d].
- * For DLLM_BF16 the handle also owns a copy of lm_head (ceil(V/256)*256*d
- * bf16 values in a tiled layout that the LM-head kernel streams contiguously),
- * made here and freed by dllm_model_destroy: later writes to the caller's
- * lm_head are not seen.  The copy is taken after a device synchronisation, so
- * the weights may still be being written on any stream when this is called.
- * All other weights are read in place on every call.
- * Errors: DLLM_EINVAL (null pointer, bad count), DLLM_EUNSUPPORTED (shape, or
- * a bf16 LM head above 2 GiB), DLLM_EHIP (a device call failed, allocation
- * included).
+ * model_buf: device, 256-byte aligned, at least dllm_model_buffer_size()
+ * bytes, borrowed for the handle's lifetime (may be NULL for DLLM_F32).  For
+ * DLLM_BF16 a copy of lm_head in the tiled layout that the LM-head kernel
+ * streams contiguously is written there, enqueued on `stream` (ordered after
+ * the caller's earlier work on that stream; other streams must be ordered by
+ * the caller): later writes to the caller's lm_head are not seen.  All other
+ * weights are read in place on every call.
+ * Errors: DLLM_EINVAL (null pointer, bad count, misaligned buffer),
+ * DLLM_ENOMEM (model_buf too small), DLLM_EUNSUPPORTED (shape, or a bf16 LM
+ * head above 2 GiB), DLLM_EHIP.
  */
-int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int32_t n_weights,
-                      dllm_model** out);
+int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int32_t n_weights, void* model_buf,
+                      size_t model_buf_bytes, void* stream, dllm_model** out);
 int dllm_model_destroy(dllm_model* model);
 
 /*
- * Optional, bf16 models: make copies of every layer's q/k/v, output, gate/up
- * and down weights in the tiled MFMA-operand order of the LM head's copy
- * (each 256-row x 64-k block one contiguous 32 KiB run), owned by the handle
- * and freed by dllm_model_destroy (device memory about the size of those
- * weights: ~14 GB for the LLaDA-8B shape).  GEMMs of at most 128 rows -- the
- * block rows of a cached step (dllm_forward_kv and friends) -- then stream
- * these runs instead of the row-major tensors: up to 64 rows through a
- * register-direct kernel (k summed in another order: results agree to
- * rounding, not bit for bit), 65 .. 128 rows through the tiled kernel
- * (bit-identical).  As with the LM head copy, later writes to the caller's
- * weights are not seen.
- * A second call does nothing.  Errors: DLLM_EUNSUPPORTED (fp32 model), DLLM_EHIP.
+ * Optional, bf16 models: copies of every layer's q/k/v, output, gate/up and
+ * down weights in the tiled MFMA-operand order of the LM head's copy (each
+ * 256-row x 64-k block one contiguous 32 KiB run) in the caller's buffer
+ * `buf` (device, 256-byte aligned, at least dllm_model_packed_size() bytes:
+ * about the size of those weights, ~14 GB for the LLaDA-8B shape), borrowed
+ * for the handle's lifetime and enqueued on `stream` as for the model buffer.
+ * GEMMs of at most 128 rows -- the block rows of a cached step
+ * (dllm_forward_kv and friends) -- then stream these runs instead of the
+ * row-major tensors: up to 64 rows through a register-direct kernel (k summed
+ * in another order: results agree to rounding, not bit for bit), 65 .. 128
+ * rows through the tiled kernel (bit-identical).  Later writes to the
+ * caller's weights are not seen.  A later call repacks into its own buffer.
+ * Errors: DLLM_EUNSUPPORTED (fp32 model), DLLM_EINVAL, DLLM_ENOMEM, DLLM_EHIP.
  */
-int dllm_model_pack_weights(dllm_model* model);
+int dllm_model_packed_size(const dllm_model* model, size_t* bytes);
+int dllm_model_pack_weights(dllm_model* model, void* buf, size_t bytes, void* stream);
 
 /*
  * Bytes of workspace needed by dllm_forward / dllm_step / dllm_generate for
@@ -204,14 +218,20 @@ int dllm_workspace_size(const dllm_model* model, int32_t B, int32_t L, int32_t r
  * act = float32 for DLLM_F32 models, bf16 for DLLM_BF16 models; act16 =
  * float32 for DLLM_F32 models and, for DLLM_BF16 models, the bf16 values of v
  * stored as IEEE half (exact within half's range) for the attention kernel's
- * half-precision probability x value product. */
+ * half-precision probability x value product.  Every buffer up to u, the RoPE
+ * tables and the error word lie at offsets that do not depend on `rows`, so
+ * calls with different row counts (dllm_layer, then dllm_head) can share one
+ * workspace of the largest size. */
 typedef struct dllm_ws_layout {
   size_t total, h, a_attn, q, k, vt, attn, a_mlp, u, hb;
 } dllm_ws_layout;
 int dllm_workspace_layout(const dllm_model* model, int32_t B, int32_t L, int32_t rows, dllm_ws_layout* out);
 
 /* h[b*L + l, :] = embed[x[b, l], :] as float32 into the workspace's h.
- * x: device int32 [B, L], each in [0, vocab). */
+ * x: device int32 [B, L], each in [0, vocab).  An id outside that range is
+ * never used as an address: its row of h is zero and the workspace's error
+ * word records it (reported by the next commit on this workspace: see
+ * dllm_step). */
 int dllm_embed(const dllm_model* model, const int32_t* x, int32_t B, int32_t L, void* workspace,
                size_t workspace_bytes, void* stream);
 
@@ -233,7 +253,10 @@ int dllm_layer(const dllm_model* model, int32_t layer, int32_t part, int32_t B, 
 int dllm_head(const dllm_model* model, int32_t B, int32_t L, int32_t row0, int32_t rows, float* conf,
               int32_t* argmax, float* logits, void* workspace, size_t workspace_bytes, void* stream);
 
-/* dllm_embed + every layer + dllm_head: one forward on x [B, L] (device). */
+/* dllm_embed + every layer + dllm_head: one forward on x [B, L] (device).
+ * Afterwards the workspace's h holds the final residual of the head rows only
+ * (the last layer's split-K partials are added by the final norm to those
+ * rows alone). */
 int dllm_forward(const dllm_model* model, const int32_t* x, int32_t B, int32_t L, int32_t row0, int32_t rows,
                  float* conf, int32_t* argmax, float* logits, void* workspace, size_t workspace_bytes,
                  void* stream);
@@ -263,7 +286,11 @@ int dllm_commit(const dllm_cai_params* params, dllm_state* state, const float* c
  * dllm_commit.  conf_out / argmax_out: optional device [B, bl] copies of the
  * step's predictions (NULL on the hot path).  all_done_host: optional pinned
  * host int32; when given the call waits for the step and stores 1 there when
- * every sequence has finished the block.
+ * every sequence has finished the block, and reports the workspace's error
+ * word (then cleared): DLLM_EINVAL if a token id of x was outside [0, vocab)
+ * (its embedding was taken as zero), DLLM_EUNSUPPORTED if a value of v was
+ * beyond IEEE half's range (the attention's half-precision P.V operand; it
+ * was used as +-65504).  The step's decisions were still applied.
  */
 int dllm_step(const dllm_model* model, const dllm_cai_params* params, dllm_state* state, int32_t B, int32_t P,
               int32_t G, int32_t block, int32_t t, float* conf_out, int32_t* argmax_out, int32_t* all_done_host,
@@ -273,7 +300,9 @@ int dllm_step(const dllm_model* model, const dllm_cai_params* params, dllm_state
  * Decode G tokens after the prompt (device int32 [B, P]), block by block
  * (Section 4.3), running dllm_step until each block finishes.  Waits for the
  * stream once per step (the block-finished flag) and returns after the last
- * step.  forwards_host: optional host int32 [G/bl], forwards run per block.
+ * step, or after the first step whose error word is set (the errors of
+ * dllm_step).  The RoPE tables are built once, before the first step.
+ * forwards_host: optional host int32 [G/bl], forwards run per block.
  * conf_trace / argmax_trace: optional device [G/bl, T, B, bl] records of every
  * step's predictions (entries of steps not run are left untouched).
  * total_forwards: optional host int32.

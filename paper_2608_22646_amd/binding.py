@@ -61,9 +61,11 @@ _LIB = None
 
 _SIGS = {
     "dllm_last_error": (_c.c_char_p, []),
-    "dllm_model_create": (_i32, [_c.POINTER(ModelCfg), _c.POINTER(_vp), _i32, _c.POINTER(_vp)]),
+    "dllm_model_buffer_size": (_i32, [_c.POINTER(ModelCfg), _c.POINTER(_sz)]),
+    "dllm_model_create": (_i32, [_c.POINTER(ModelCfg), _c.POINTER(_vp), _i32, _vp, _sz, _vp, _c.POINTER(_vp)]),
     "dllm_model_destroy": (_i32, [_vp]),
-    "dllm_model_pack_weights": (_i32, [_vp]),
+    "dllm_model_packed_size": (_i32, [_vp, _c.POINTER(_sz)]),
+    "dllm_model_pack_weights": (_i32, [_vp, _vp, _sz, _vp]),
     "dllm_workspace_size": (_i32, [_vp, _i32, _i32, _i32, _c.POINTER(_sz)]),
     "dllm_workspace_layout": (_i32, [_vp, _i32, _i32, _i32, _c.POINTER(WsLayout)]),
     "dllm_embed": (_i32, [_vp, _vp, _i32, _i32, _vp, _sz, _vp]),
@@ -118,6 +120,13 @@ def _ptr(t):
 def _stream(stream=None):
     s = stream if stream is not None else torch.cuda.current_stream()
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def device_buffer(nbytes, device="cuda"):
+    """A caller-owned, 256-byte aligned uint8 device tensor of nbytes bytes."""
+    buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + nbytes]
 
 
 # ---------------------------------------------------------------- parameters
@@ -231,22 +240,39 @@ class DecodeState:
 
 
 class Model:
-    """A model handle over caller-owned device weights (kept alive here)."""
+    """A model handle over caller-owned device weights and model buffer (both
+    kept alive here).  The LM-head copy is written on the current stream."""
 
-    def __init__(self, cfg, weights):
+    def __init__(self, cfg, weights, stream=None):
         L = lib()
         self.cfg = cfg
         self.mask_id = cfg.vocab - 1
         self.weights = list(weights)
         self._c = model_cfg(cfg)
+        n = ctypes.c_size_t()
+        check(L.dllm_model_buffer_size(ctypes.byref(self._c), ctypes.byref(n)))
+        dev = self.weights[0].device
+        self.model_buf = device_buffer(n.value, dev) if n.value else None
+        self.packed_buf = None
         arr = (ctypes.c_void_p * len(self.weights))(*[w.data_ptr() for w in self.weights])
         h = ctypes.c_void_p()
-        check(L.dllm_model_create(ctypes.byref(self._c), arr, len(self.weights), ctypes.byref(h)))
+        check(L.dllm_model_create(ctypes.byref(self._c), arr, len(self.weights), _ptr(self.model_buf), n.value,
+                                  _stream(stream), ctypes.byref(h)))
         self.h = h
 
-    def pack_weights(self):
-        """dllm_model_pack_weights: tiled copies of the projection weights for the block-row GEMMs."""
-        check(lib().dllm_model_pack_weights(self.h))
+    def packed_size(self):
+        n = ctypes.c_size_t()
+        check(lib().dllm_model_packed_size(self.h, ctypes.byref(n)))
+        return n.value
+
+    def pack_weights(self, stream=None):
+        """dllm_model_pack_weights: tiled copies of the projection weights for the
+        block-row GEMMs, in a buffer allocated here (once)."""
+        if self.packed_buf is None:
+            n = self.packed_size()
+            buf = device_buffer(n, self.weights[0].device)
+            check(lib().dllm_model_pack_weights(self.h, _ptr(buf), n, _stream(stream)))
+            self.packed_buf = buf
         return self
 
     def close(self):
@@ -267,10 +293,7 @@ class Model:
         return n.value
 
     def workspace(self, B, L, rows, device="cuda"):
-        n = self.workspace_size(B, L, rows)
-        ws = torch.empty(n + 256, dtype=torch.uint8, device=device)
-        off = (-ws.data_ptr()) % 256
-        return ws[off:off + n]
+        return device_buffer(self.workspace_size(B, L, rows), device)
 
     def layout(self, B, L, rows) -> WsLayout:
         out = WsLayout()
@@ -343,9 +366,7 @@ class Model:
         """A caller-owned, 256-byte aligned cache buffer for B sequences of L positions."""
         n = ctypes.c_size_t()
         check(lib().dllm_kv_cache_size(self.h, B, L, ctypes.byref(n)))
-        buf = torch.empty(n.value + 256, dtype=torch.uint8, device=device)
-        off = (-buf.data_ptr()) % 256
-        return buf[off:off + n.value]
+        return device_buffer(n.value, device)
 
     def forward_kv(self, x, row0, rows, kv, refresh, ws=None, logits=False, stream=None):
         """dllm_forward_kv: the refresh forward (refresh=True) or the cached forward of rows [row0, row0 + rows)."""

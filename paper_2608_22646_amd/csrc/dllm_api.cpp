@@ -47,9 +47,9 @@ struct ProfEvent {
 struct dllm_model {
   dllm_model_cfg cfg;
   std::vector<const void*> w;
-  bf16_t* head_tiled = nullptr;  // bf16: owned tiled copy of the LM head
+  bf16_t* head_tiled = nullptr;  // bf16: tiled copy of the LM head, in the caller's model buffer
   // bf16, after dllm_model_pack_weights: packed copies of every layer's q/k/v,
-  // output, gate/up and down weights (one allocation; offsets per layer)
+  // output, gate/up and down weights (in the caller's buffer; offsets per layer)
   bf16_t* packed = nullptr;
   std::vector<size_t> packed_off;  // [layer * 4 + {0: qkv, 1: o, 2: gate/up, 3: down}] in elements
   int32_t* pinned_flag = nullptr;
@@ -66,10 +66,15 @@ struct Layout {
   size_t raw, gate, up, logits;                  // fp32 path
   size_t part_m, part_s, part_i, ticket, hbf;    // bf16 head
   size_t splitk;                                 // bf16 split-K GEMM partials
-  size_t conf, argmax, all_done;                 // step scratch
+  size_t conf, argmax, all_done, err;            // step scratch
   size_t total;
 };
 
+// Buffers whose contents outlive a call (the residual h, the RoPE tables, the
+// error word) and everything sized by B and L alone come first, so their
+// offsets do not depend on `rows`: calls on one workspace with different row
+// counts (dllm_layer, then dllm_head) see the same h and tables.  The buffers
+// sized by the head rows follow.
 Layout make_layout(const dllm_model_cfg& c, int B, int L, int rows) {
   const size_t M = (size_t)B * L, d = c.d_model, F = c.d_ff, hd = c.head_dim;
   const size_t act = c.dtype == DLLM_F32 ? 4 : 2;
@@ -89,23 +94,31 @@ Layout make_layout(const dllm_model_cfg& c, int B, int L, int rows) {
   o.attn = take(M * c.n_heads * hd * act);
   o.a_mlp = take(M * d * act);
   o.u = take(M * F * act);
-  o.hb = take(R * d * act);
   o.cosb = take((size_t)L * hd / 2 * 4);
   o.sinb = take((size_t)L * hd / 2 * 4);
+  o.all_done = take(4);
+  o.err = take(4);
   if (c.dtype == DLLM_F32) {
     o.raw = take(M * (c.n_heads + 2 * c.n_kv_heads) * hd * 4);
     o.gate = take(M * F * 4);
     o.up = take(M * F * 4);
+  } else {
+    o.ticket = take(4);
+    o.hbf = take((size_t)HEAD_FRAG_ROWS * d * 2);
+  }
+  // sized by the head rows
+  o.hb = take(R * d * act);
+  o.conf = take(R * 4);
+  o.argmax = take(R * 4);
+  if (c.dtype == DLLM_F32) {
     o.logits = take(R * c.vocab * 4);
   } else {
     const size_t tiles = head_bf16_tiles(c.vocab);
     o.part_m = take(tiles * R * 4);
     o.part_s = take(tiles * R * 4);
     o.part_i = take(tiles * R * 4);
-    o.ticket = take(4);
-    o.hbf = take((size_t)HEAD_FRAG_ROWS * d * 2);
     // split-K partials of the full forward (B L rows) and of a cached step's
-    // forward (B rows rows)
+    // forward (B rows rows); nothing in them outlives a call
     const int qkv_n = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
     size_t sk = 0;
     for (const int mm : {(int)M, (int)R}) {
@@ -117,9 +130,6 @@ Layout make_layout(const dllm_model_cfg& c, int B, int L, int rows) {
     }
     o.splitk = take(sk);
   }
-  o.conf = take(R * 4);
-  o.argmax = take(R * 4);
-  o.all_done = take(4);
   o.total = off;
   return o;
 }
@@ -207,12 +217,18 @@ void check_kv(const dllm_model* m, int B, int L, const void* kv, size_t bytes) {
 
 // ---------------------------------------------------------------- forward pieces
 // h[b rows + i] = embedding of x[b, row0 + i] (rows = L, row0 = 0: every
-// position); RoPE tables for all L positions.
+// position); with rope set, first the RoPE tables for all L positions, which
+// also clears the error word (a decode builds them once, before its first
+// step, after clearing the word in the state initialisation; each commit
+// clears it after reporting).
 void run_embed(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, void* ws, const Layout& lay,
-               hipStream_t s) {
+               hipStream_t s, bool rope = true) {
   const auto& c = m->cfg;
-  launch_embed(x, W(m, 0), c.dtype, at<float>(ws, lay.h), B, rows, L, row0, c.d_model, s);
-  launch_rope_table(at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), L, c.head_dim, c.rope_base, s);
+  if (rope)
+    launch_rope_table(at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), L, c.head_dim, c.rope_base,
+                      at<int>(ws, lay.err), s);
+  launch_embed(x, W(m, 0), c.dtype, at<float>(ws, lay.h), B, rows, L, row0, c.d_model, c.vocab, at<int>(ws, lay.err),
+               s);
 }
 
 void gemm_bf16(const dllm_model* m, GemmArgs g, void* ws, const Layout& lay, hipStream_t s, int kind,
@@ -315,6 +331,7 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     g.pos0 = pos0;
     g.Hq = c.n_heads;
     g.Hkv = c.n_kv_heads;
+    g.err = at<int>(ws, lay.err);
     gemm_bf16(m, g, ws, lay, s, PK_GEMM);
     {
       ProfScope p(m, PK_ATTN, s);
@@ -399,8 +416,11 @@ void run_layer(const dllm_model* m, int layer, int part, int B, int L, void* ws,
     run_layer_f32(m, layer, part, B, L, ws, lay, s, rows);
 }
 
+// Final norm and LM head on rows [row0, row0 + rows) of every sequence; pend:
+// split-K partials the last layer's down projection left pending (added to the
+// head rows by the final norm; the other rows of h stay without them).
 void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf, int32_t* argmax, float* logits,
-              void* ws, const Layout& lay, hipStream_t s) {
+              void* ws, const Layout& lay, hipStream_t s, const PendingResid* pend = nullptr) {
   const auto& c = m->cfg;
   const int nl = c.n_layers;
   const int R = B * rows;
@@ -409,9 +429,11 @@ void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf
   bf16_t* hbf = c.dtype == DLLM_BF16 && R <= HEAD_FRAG_ROWS ? at<bf16_t>(ws, lay.hbf) : nullptr;
   {
     ProfScope p(m, PK_NORM, s);
+    // the head kernel's ticket is zeroed here (no memset node in a captured step)
     if (c.dtype == DLLM_BF16)
-      launch_rmsnorm_head(at<float>(ws, lay.h), static_cast<const bf16_t*>(W(m, 1 + 9 * nl)), at<bf16_t>(ws, lay.hb),
-                          hbf, B, rows, L, row0, c.d_model, c.rms_eps, s);
+      launch_rmsnorm_head(at<float>(ws, lay.h), pend, static_cast<const bf16_t*>(W(m, 1 + 9 * nl)),
+                          at<bf16_t>(ws, lay.hb), hbf, B, rows, L, row0, c.d_model, c.rms_eps, at<int>(ws, lay.ticket),
+                          s);
     else
       launch_rmsnorm(at<float>(ws, lay.h), W(m, 1 + 9 * nl), at<void>(ws, lay.hb), c.dtype, B, rows, L, row0,
                      c.d_model, c.rms_eps, s);
@@ -437,9 +459,6 @@ void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf
     a.part_s = at<float>(ws, lay.part_s);
     a.part_i = at<int32_t>(ws, lay.part_i);
     a.ticket = at<int>(ws, lay.ticket);
-    // the kernel's last workgroup resets the ticket; clearing it here as well
-    // makes a fresh (uninitialised) workspace safe
-    hip_check(hipMemsetAsync(a.ticket, 0, sizeof(int), s), "hipMemsetAsync");
     launch_head_bf16(a, s);
   }
 }
@@ -523,51 +542,102 @@ void fill_commit_args(const dllm_cai_params* p, dllm_state* st, CommitArgs* a, i
   a->patience = p->patience;
   a->theta_fb = p->theta_fb;
   // fixed schedule: floor(bl / T) per step, one more in the first bl % T steps
-  a->fixed_k = (p->flags & DLLM_F_FIXED) ? p->block_len / T + (t < p->block_len % T ? 1 : 0) : 0;
+  a->fixed = (p->flags & DLLM_F_FIXED) ? 1 : 0;
+  a->fixed_k = a->fixed ? p->block_len / T + (t < p->block_len % T ? 1 : 0) : 0;
 }
 
 // Every layer on the B * Lq rows of h (see LayerRows; kv null: the full
-// sequence with keys/values in the workspace).
-void run_layers(const dllm_model* m, int B, int L, int Lq, int pos0, void* kv, void* ws, const Layout& lay,
-                hipStream_t s) {
+// sequence with keys/values in the workspace).  Each layer's down-projection
+// partials are added by the next layer's first norm; the last layer's are
+// returned for the final norm, which adds them to the head rows only.
+PendingResid run_layers(const dllm_model* m, int B, int L, int Lq, int pos0, void* kv, void* ws, const Layout& lay,
+                        hipStream_t s) {
   const int nl = m->cfg.n_layers;
-  // each layer's down-projection partials are added by the next layer's first
-  // norm; the last layer reduces its own, so h is complete for the head
   PendingResid carry;
   for (int l = 0; l < nl; ++l) {
     LayerRows r{Lq, pos0, nullptr, nullptr};
     if (kv) r = cache_rows(m, kv, l, B, L, Lq, pos0);
     if (m->cfg.dtype == DLLM_BF16)
-      run_layer_bf16(m, l, 2, B, L, ws, lay, s, &carry, l + 1 < nl ? &carry : nullptr, &r);
+      run_layer_bf16(m, l, 2, B, L, ws, lay, s, &carry, &carry, &r);
     else
       run_layer_f32(m, l, 2, B, L, ws, lay, s, &r);
   }
+  return carry;
 }
 
 // The full forward over all L positions, head on rows [row0, row0 + rows);
 // with kv non-null every layer's keys/values are stored in the cache
 // (a refresh step).
 void forward_all(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, float* conf,
-                 int32_t* argmax, float* logits, void* ws, const Layout& lay, hipStream_t s, void* kv = nullptr) {
+                 int32_t* argmax, float* logits, void* ws, const Layout& lay, hipStream_t s, void* kv = nullptr,
+                 bool rope = true) {
   {
     ProfScope p(m, PK_NORM, s);
-    run_embed(m, x, B, L, 0, L, ws, lay, s);
+    run_embed(m, x, B, L, 0, L, ws, lay, s, rope);
   }
-  run_layers(m, B, L, L, 0, kv, ws, lay, s);
-  run_head(m, B, L, row0, rows, conf, argmax, logits, ws, lay, s);
+  const PendingResid pend = run_layers(m, B, L, L, 0, kv, ws, lay, s);
+  run_head(m, B, L, row0, rows, conf, argmax, logits, ws, lay, s, &pend);
 }
 
 // A cached step's forward: only rows [row0, row0 + rows) of each sequence go
 // through the layers, attending over the cache (whose entries at those
 // positions they overwrite); the head runs on all of them.
 void forward_cached(const dllm_model* m, const int32_t* x, int B, int L, int row0, int rows, float* conf,
-                    int32_t* argmax, float* logits, void* kv, void* ws, const Layout& lay, hipStream_t s) {
+                    int32_t* argmax, float* logits, void* kv, void* ws, const Layout& lay, hipStream_t s,
+                    bool rope = true) {
   {
     ProfScope p(m, PK_NORM, s);
-    run_embed(m, x, B, L, row0, rows, ws, lay, s);
+    run_embed(m, x, B, L, row0, rows, ws, lay, s, rope);
   }
-  run_layers(m, B, L, rows, row0, kv, ws, lay, s);
-  run_head(m, B, rows, 0, rows, conf, argmax, logits, ws, lay, s);
+  const PendingResid pend = run_layers(m, B, L, rows, row0, kv, ws, lay, s);
+  run_head(m, B, rows, 0, rows, conf, argmax, logits, ws, lay, s, &pend);
+}
+
+void check_cfg(const dllm_model_cfg* cfg) {
+  require(cfg != nullptr, DLLM_EINVAL, "cfg is NULL");
+  const auto& c = *cfg;
+  require(c.n_layers >= 0 && c.d_model > 0 && c.n_heads > 0 && c.n_kv_heads > 0 && c.head_dim > 0 && c.d_ff > 0 &&
+              c.vocab > 1,
+          DLLM_EINVAL, "model dimensions must be positive");
+  require(c.n_heads % c.n_kv_heads == 0, DLLM_EINVAL, "n_heads must be a multiple of n_kv_heads");
+  require(c.mask_id >= 0 && c.mask_id < c.vocab, DLLM_EINVAL, "mask_id out of range");
+  require(std::isfinite(c.rms_eps) && c.rms_eps > 0 && std::isfinite(c.rope_base) && c.rope_base > 0, DLLM_EINVAL,
+          "rms_eps and rope_base must be positive");
+  require(c.dtype == DLLM_F32 || c.dtype == DLLM_BF16, DLLM_EINVAL, "dtype must be DLLM_F32 or DLLM_BF16");
+  if (c.dtype == DLLM_BF16)
+    require(c.head_dim == 128 && c.d_model % 256 == 0 && c.d_ff % 128 == 0 && c.n_heads % 2 == 0 &&
+                c.n_kv_heads % 2 == 0,
+            DLLM_EUNSUPPORTED,
+            "bf16 path needs head_dim 128, d_model % 256 == 0, d_ff % 128 == 0, even head counts");
+  else
+    require((c.head_dim == 64 || c.head_dim == 128), DLLM_EUNSUPPORTED, "fp32 path needs head_dim 64 or 128");
+  if (c.dtype == DLLM_BF16)
+    require(head_bf16_packed_bytes(c.vocab, c.d_model) <= 0x7fffffffu, DLLM_EUNSUPPORTED,
+            "bf16 LM head larger than 2 GiB");
+}
+
+// Bytes of the packed layer-weight copies, and (off non-null) each copy's
+// element offset: [layer * 4 + {0: q/k/v, 1: output, 2: gate/up, 3: down}].
+size_t packed_layout(const dllm_model* m, std::vector<size_t>* off) {
+  const int nl = m->cfg.n_layers;
+  if (off) off->assign((size_t)nl * 4, 0);
+  size_t total = 0;
+  for (int l = 0; l < nl; ++l)
+    for (int w = 0; w < 4; ++w) {
+      const GemmArgs g = layer_gemm(m, l, w);
+      if (off) (*off)[(size_t)l * 4 + w] = total / sizeof(bf16_t);
+      total += align256(gemm_packed_bytes(g.N, g.K));
+    }
+  return std::max<size_t>(total, 256);
+}
+
+// The step's error word, as the commit kernel reports it (bits above bit 0 of
+// the block-finished word).
+void raise_step_errors(int flag) {
+  const int e = flag >> 1;
+  if (e & ERR_TOKEN_RANGE) fail(DLLM_EINVAL, "a token id is outside [0, vocab)");
+  if (e & ERR_V_RANGE)
+    fail(DLLM_EUNSUPPORTED, "a value of v is beyond IEEE half's range (stored as +-65504 for the attention)");
 }
 
 int finish(const ApiError& e) {
@@ -599,45 +669,40 @@ extern "C" {
 
 const char* dllm_last_error(void) { return g_last_error.c_str(); }
 
-int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int32_t n_weights, dllm_model** out) {
+int dllm_model_buffer_size(const dllm_model_cfg* cfg, size_t* bytes) {
   API_BEGIN
-  require(cfg && weights && out, DLLM_EINVAL, "NULL argument");
+  require(bytes != nullptr, DLLM_EINVAL, "bytes is NULL");
+  check_cfg(cfg);
+  *bytes = cfg->dtype == DLLM_BF16 ? align256(head_bf16_packed_bytes(cfg->vocab, cfg->d_model)) : 0;
+  API_END
+}
+
+int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int32_t n_weights, void* model_buf,
+                      size_t model_buf_bytes, void* stream, dllm_model** out) {
+  API_BEGIN
+  require(weights && out, DLLM_EINVAL, "NULL argument");
+  check_cfg(cfg);
   const auto& c = *cfg;
-  require(c.n_layers >= 0 && c.d_model > 0 && c.n_heads > 0 && c.n_kv_heads > 0 && c.head_dim > 0 && c.d_ff > 0 &&
-              c.vocab > 1,
-          DLLM_EINVAL, "model dimensions must be positive");
-  require(c.n_heads % c.n_kv_heads == 0, DLLM_EINVAL, "n_heads must be a multiple of n_kv_heads");
-  require(c.mask_id >= 0 && c.mask_id < c.vocab, DLLM_EINVAL, "mask_id out of range");
-  require(std::isfinite(c.rms_eps) && c.rms_eps > 0 && std::isfinite(c.rope_base) && c.rope_base > 0, DLLM_EINVAL,
-          "rms_eps and rope_base must be positive");
-  require(c.dtype == DLLM_F32 || c.dtype == DLLM_BF16, DLLM_EINVAL, "dtype must be DLLM_F32 or DLLM_BF16");
-  if (c.dtype == DLLM_BF16)
-    require(c.head_dim == 128 && c.d_model % 256 == 0 && c.d_ff % 128 == 0 && c.n_heads % 2 == 0 &&
-                c.n_kv_heads % 2 == 0,
-            DLLM_EUNSUPPORTED,
-            "bf16 path needs head_dim 128, d_model % 256 == 0, d_ff % 128 == 0, even head counts");
-  else
-    require((c.head_dim == 64 || c.head_dim == 128), DLLM_EUNSUPPORTED, "fp32 path needs head_dim 64 or 128");
   require(n_weights == 3 + 9 * c.n_layers, DLLM_EINVAL, "n_weights must be 3 + 9 * n_layers");
   for (int i = 0; i < n_weights; ++i) require(weights[i] != nullptr, DLLM_EINVAL, "NULL weight pointer");
-  if (c.dtype == DLLM_BF16)
-    require(head_bf16_packed_bytes(c.vocab, c.d_model) <= 0x7fffffffu, DLLM_EUNSUPPORTED,
-            "bf16 LM head larger than 2 GiB");
+  if (c.dtype == DLLM_BF16) {
+    const size_t need = align256(head_bf16_packed_bytes(c.vocab, c.d_model));
+    require(model_buf != nullptr, DLLM_EINVAL, "model_buf is NULL (a bf16 model keeps its LM-head copy there)");
+    require(((uintptr_t)model_buf & 255) == 0, DLLM_EINVAL, "model_buf must be 256-byte aligned");
+    require(model_buf_bytes >= need, DLLM_ENOMEM, "model_buf too small: need " + std::to_string(need) + " bytes");
+  }
   auto* m = new dllm_model();
   m->cfg = c;
   m->w.assign(weights, weights + n_weights);
   try {
     hip_check(hipHostMalloc((void**)&m->pinned_flag, sizeof(int32_t), hipHostMallocDefault), "hipHostMalloc");
     if (c.dtype == DLLM_BF16) {
-      // weights may still be in flight on any stream: wait, copy, wait
-      hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
-      hip_check(hipMalloc((void**)&m->head_tiled, head_bf16_packed_bytes(c.vocab, c.d_model)), "hipMalloc");
-      launch_pack_head_bf16(static_cast<const bf16_t*>(m->w[2 + 9 * c.n_layers]), m->head_tiled, c.vocab,
-                            c.d_model, nullptr);
-      hip_check(hipStreamSynchronize(nullptr), "hipStreamSynchronize");
+      // stream-ordered after the caller's writes of lm_head on that stream
+      m->head_tiled = static_cast<bf16_t*>(model_buf);
+      launch_pack_head_bf16(static_cast<const bf16_t*>(m->w[2 + 9 * c.n_layers]), m->head_tiled, c.vocab, c.d_model,
+                            (hipStream_t)stream);
     }
   } catch (...) {
-    if (m->head_tiled) (void)hipFree(m->head_tiled);
     if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
     delete m;
     throw;
@@ -654,40 +719,36 @@ int dllm_model_destroy(dllm_model* m) {
     (void)hipEventDestroy(e.stop);
   }
   if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
-  if (m->head_tiled) (void)hipFree(m->head_tiled);
-  if (m->packed) (void)hipFree(m->packed);
   delete m;
   API_END
 }
 
-int dllm_model_pack_weights(dllm_model* m) {
+int dllm_model_packed_size(const dllm_model* m, size_t* bytes) {
+  API_BEGIN
+  check_model(m);
+  require(bytes != nullptr, DLLM_EINVAL, "bytes is NULL");
+  require(m->cfg.dtype == DLLM_BF16, DLLM_EUNSUPPORTED, "packed weights are for bf16 models");
+  *bytes = packed_layout(m, nullptr);
+  API_END
+}
+
+int dllm_model_pack_weights(dllm_model* m, void* buf, size_t bytes, void* stream) {
   API_BEGIN
   check_model(m);
   require(m->cfg.dtype == DLLM_BF16, DLLM_EUNSUPPORTED, "packed weights are for bf16 models");
-  if (m->packed) return DLLM_OK;
+  std::vector<size_t> off;
+  const size_t need = packed_layout(m, &off);
+  require(buf != nullptr, DLLM_EINVAL, "buf is NULL");
+  require(((uintptr_t)buf & 255) == 0, DLLM_EINVAL, "buf must be 256-byte aligned");
+  require(bytes >= need, DLLM_ENOMEM, "packed-weight buffer too small: need " + std::to_string(need) + " bytes");
+  bf16_t* dst = static_cast<bf16_t*>(buf);
   const int nl = m->cfg.n_layers;
-  std::vector<size_t> off((size_t)nl * 4);
-  size_t total = 0;
+  // stream-ordered after the caller's writes of the weights on that stream
   for (int l = 0; l < nl; ++l)
-    for (int w = 0; w < 4; ++w) {
-      const GemmArgs g = layer_gemm(m, l, w);
-      off[(size_t)l * 4 + w] = total / sizeof(bf16_t);
-      total += align256(gemm_packed_bytes(g.N, g.K));
-    }
-  bf16_t* buf = nullptr;
-  // the weights may still be in flight on any stream: wait, pack, wait
-  hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
-  hip_check(hipMalloc((void**)&buf, std::max<size_t>(total, 256)), "hipMalloc");
-  try {
-    for (int l = 0; l < nl; ++l)
-      for (int w = 0; w < 4; ++w) launch_pack_gemm_weights(layer_gemm(m, l, w), buf + off[(size_t)l * 4 + w], nullptr);
-    hip_check(hipStreamSynchronize(nullptr), "hipStreamSynchronize");
-  } catch (...) {
-    (void)hipFree(buf);
-    throw;
-  }
+    for (int w = 0; w < 4; ++w)
+      launch_pack_gemm_weights(layer_gemm(m, l, w), dst + off[(size_t)l * 4 + w], (hipStream_t)stream);
   m->packed_off = off;
-  m->packed = buf;
+  m->packed = dst;
   API_END
 }
 
@@ -828,7 +889,7 @@ int dllm_state_init(int32_t mask_id, const int32_t* prompt, int32_t B, int32_t P
   require(B >= 1 && B <= 16 && P >= 0 && G >= 1, DLLM_ESHAPE, "bad sizes");
   require(P == 0 || prompt != nullptr, DLLM_EINVAL, "prompt is NULL");
   launch_state_init(prompt, st->x, st->commit_step, st->reason, st->s, st->budget, st->ell, st->done, B, P, G,
-                    mask_id, (hipStream_t)stream);
+                    mask_id, nullptr, (hipStream_t)stream);
   API_END
 }
 
@@ -851,19 +912,20 @@ namespace {
 // full forward storing the cache) when refresh is set, a cached step otherwise.
 void step_impl(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int B, int P, int G, int block, int t,
                float* conf_out, int32_t* argmax_out, void* ws, const Layout& lay, hipStream_t s, void* kv = nullptr,
-               bool refresh = true) {
+               bool refresh = true, bool rope = true) {
   CommitArgs a{};
   fill_commit_args(p, st, &a, B, P, G, block, t, m->cfg.mask_id);
   const int bl = p->block_len;
   float* conf = conf_out ? conf_out : at<float>(ws, lay.conf);
   int32_t* arg = argmax_out ? argmax_out : at<int32_t>(ws, lay.argmax);
   if (kv && !refresh)
-    forward_cached(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, kv, ws, lay, s);
+    forward_cached(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, kv, ws, lay, s, rope);
   else
-    forward_all(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, ws, lay, s, kv);
+    forward_all(m, st->x, B, P + G, P + block * bl, bl, conf, arg, nullptr, ws, lay, s, kv, rope);
   a.conf = conf;
   a.argmax = arg;
   a.all_done = at<int32_t>(ws, lay.all_done);
+  a.err = at<int>(ws, lay.err);
   ProfScope pr(m, PK_COMMIT, s);
   launch_commit(a, s);
 }
@@ -883,7 +945,8 @@ int dllm_step(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int
     hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
               "hipMemcpyAsync");
     hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
-    *all_done_host = *m->pinned_flag;
+    *all_done_host = *m->pinned_flag & 1;
+    raise_step_errors(*m->pinned_flag);
   }
   API_END
 }
@@ -903,7 +966,8 @@ int dllm_step_kv(const dllm_model* m, const dllm_cai_params* p, int32_t refresh,
     hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
               "hipMemcpyAsync");
     hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
-    *all_done_host = *m->pinned_flag;
+    *all_done_host = *m->pinned_flag & 1;
+    raise_step_errors(*m->pinned_flag);
   }
   API_END
 }
@@ -915,19 +979,26 @@ void generate_impl(const dllm_model* m, const dllm_cai_params* p, const int32_t*
                    int32_t* argmax_trace, void* kv, int refresh_every, void* ws, const Layout& lay, hipStream_t s) {
   const int bl = p->block_len, nb = G / bl, T = steps_T(p);
   launch_state_init(prompt, st->x, st->commit_step, st->reason, st->s, st->budget, st->ell, st->done, B, P, G,
-                    m->cfg.mask_id, s);
+                    m->cfg.mask_id, at<int>(ws, lay.err), s);
+  {  // positions are fixed for the whole decode: one RoPE table
+    ProfScope pr(m, PK_NORM, s);
+    launch_rope_table(at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), P + G, m->cfg.head_dim, m->cfg.rope_base,
+                      nullptr, s);
+  }
   int total = 0;
   for (int blk = 0; blk < nb; ++blk) {
     int n = 0;
     for (int t = 0; t < T; ++t) {
       float* ct = conf_trace ? conf_trace + ((size_t)blk * T + t) * B * bl : nullptr;
       int32_t* at_ = argmax_trace ? argmax_trace + ((size_t)blk * T + t) * B * bl : nullptr;
-      step_impl(m, p, st, B, P, G, blk, t, ct, at_, ws, lay, s, kv, refresh_every == 0 || t % refresh_every == 0);
+      step_impl(m, p, st, B, P, G, blk, t, ct, at_, ws, lay, s, kv, refresh_every == 0 || t % refresh_every == 0,
+                false);
       ++n;
       hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
                 "hipMemcpyAsync");
       hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
-      if (*m->pinned_flag) break;
+      raise_step_errors(*m->pinned_flag);
+      if (*m->pinned_flag & 1) break;
     }
     if (forwards_host) forwards_host[blk] = n;
     total += n;

@@ -6,10 +6,15 @@
 // threshold / budget commits, eta, low-yield counter, grinding fallback,
 // no-mask check, flush of what is still masked when the block ends.
 //
-// Fixed-schedule baseline (fixed_k > 0 this step): the wave commits its
-// fixed_k masked positions of highest confidence (lowest position first on
-// equal confidence; a NaN confidence ranks lowest), found by fixed_k butterfly
-// reductions; no s, B or ell is kept.
+// Fixed-schedule baseline (fixed set): the wave commits its fixed_k masked
+// positions of highest confidence (lowest position first on equal confidence;
+// a NaN confidence ranks lowest), found by fixed_k butterfly reductions --
+// none at a step whose k_t is 0 (steps past the block length when T exceeds
+// it); no s, B or ell is kept.
+//
+// The word *all_done receives 1 when every sequence has finished the block,
+// plus the bits of the step's error word (shifted up by one), which is then
+// cleared.
 #include "kernels.h"
 
 namespace dllm {
@@ -40,7 +45,7 @@ __global__ void __launch_bounds__(1024) commit_kernel(CommitArgs a) {
       }
       int why = 0;
       bool exit = false;
-      if (a.fixed_k > 0) {
+      if (a.fixed) {
         const float ce = c == c ? c : -INFINITY;
         bool sel = false;
         for (int it = 0; it < a.fixed_k; ++it) {
@@ -111,10 +116,15 @@ __global__ void __launch_bounds__(1024) commit_kernel(CommitArgs a) {
   }
   if (p == 0 && b < 16) fin[b] = finished;
   __syncthreads();
-  if (threadIdx.x == 0 && a.all_done) {
+  if (threadIdx.x == 0) {
     int all = 1;
     for (int i = 0; i < a.B; ++i) all &= fin[i];
-    *a.all_done = all;
+    int e = 0;
+    if (a.err) {
+      e = *a.err;
+      *a.err = 0;
+    }
+    if (a.all_done) *a.all_done = all | (e << 1);
   }
 }
 

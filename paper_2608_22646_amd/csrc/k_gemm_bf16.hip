@@ -371,6 +371,20 @@ __device__ __forceinline__ float swap16(float x, bool hi) {
   return __uint_as_float(hi ? r[0] : r[1]);
 }
 
+// v is stored for the attention kernel's half-precision P.V product as the IEEE
+// half of its bf16 value: exact for 2^-17 <= |v| <= 65504 (bf16's 8-bit
+// significand fits half's; below, half's subnormal step 2^-24 bounds the
+// error).  A bf16 value beyond 65504 (i.e. >= 65536) is stored as +-65504 and
+// flagged in the error word.
+__device__ __forceinline__ f16_t v_half(float x, bool& over) {
+  const float b = bf2f(f2bf(x));
+  if (fabsf(b) > 65504.f) {
+    over = true;
+    return f2h(copysignf(65504.f, b));
+  }
+  return f2h(b);
+}
+
 // (sequence, position) of token row m = b L + pos, by a float reciprocal and a
 // one-step fixup: exact for m < 2^24 and B < 2^16 (the estimate of m / L is
 // then off by less than one), several times cheaper than an integer division.
@@ -405,6 +419,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
   barrier_nofence();  // every wave is done reading the ring
 
   const float inv_l = 1.0f / (float)g.Lq;  // rows per sequence
+  bool v_over = false;
   // with two k-groups only the first holds the finished tile; the second
   // joins the barriers and the stores
   if (wave < TL::NWT) {
@@ -480,8 +495,8 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
             }
           } else {  // v: four consecutive rows of column col_in, as IEEE half of the bf16 value
             uint2 pk;
-            pk.x = (uint32_t)f2h(bf2f(f2bf(v[0]))) | ((uint32_t)f2h(bf2f(f2bf(v[1]))) << 16);
-            pk.y = (uint32_t)f2h(bf2f(f2bf(v[2]))) | ((uint32_t)f2h(bf2f(f2bf(v[3]))) << 16);
+            pk.x = (uint32_t)v_half(v[0], v_over) | ((uint32_t)v_half(v[1], v_over) << 16);
+            pk.y = (uint32_t)v_half(v[2], v_over) | ((uint32_t)v_half(v[3], v_over) << 16);
             *reinterpret_cast<uint2*>(blk + col_in * St::VROW + rl0 * 2) = pk;
           }
         }
@@ -490,6 +505,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
   }
 
   }
+  if (EPI == EPI_QKV_ROPE && v_over && g.err) atomicOr(g.err, (int)ERR_V_RANGE);
 
   __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
   barrier_nofence();
@@ -733,7 +749,9 @@ __global__ void splitk_qkv_kernel(const float* __restrict__ part, int S, GemmArg
     dst[d + HALF] = f2bf(x2 * c_ + x1 * s_);
   } else {
     const int rel = n - nq - nkv, head = rel / HD, cj = rel % HD;
-    g.vt[(((size_t)b * g.Hkv + head) * HD + cj) * g.L + pos] = f2h(bf2f(f2bf(sum(n))));
+    bool over = false;
+    g.vt[(((size_t)b * g.Hkv + head) * HD + cj) * g.L + pos] = v_half(sum(n), over);
+    if (over && g.err) atomicOr(g.err, (int)ERR_V_RANGE);
   }
 }
 

@@ -17,31 +17,40 @@ int device_cu_count() {
 }
 
 // One 256-thread block per row; every thread converts a strided set of columns.
-// Row m = b rows + i gathers token x[b, row0 + i].
+// Row m = b rows + i gathers token x[b, row0 + i]; an id outside [0, V) is
+// never used as an address: the row is zero and the error word says so.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ x, const T* __restrict__ E,
-                                                    float* __restrict__ h, int rows, int L, int row0, int d) {
+                                                    float* __restrict__ h, int rows, int L, int row0, int d, int V,
+                                                    int* __restrict__ err) {
   const int m = blockIdx.x, b = m / rows, i = m - b * rows;
-  const size_t src = (size_t)x[(size_t)b * L + row0 + i] * d;
+  const int tok = x[(size_t)b * L + row0 + i];
+  const bool ok = tok >= 0 && tok < V;
+  const size_t src = (size_t)(ok ? tok : 0) * d;
   float* dst = h + (size_t)m * d;
-  for (int c = threadIdx.x; c < d; c += 256) dst[c] = Act<T>::load(E, src + c);
+  for (int c = threadIdx.x; c < d; c += 256) dst[c] = ok ? Act<T>::load(E, src + c) : 0.f;
+  if (!ok && threadIdx.x == 0 && err) atomicOr(err, (int)ERR_TOKEN_RANGE);
 }
 
 void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int B, int rows, int L, int row0, int d,
-                  hipStream_t s) {
+                  int V, int* err, hipStream_t s) {
   const int M = B * rows;
   if (M == 0) return;
   if (dtype == 0)
-    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, x, (const float*)E, h, rows, L, row0, d);
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, x, (const float*)E, h, rows, L, row0, d, V,
+                       err);
   else
-    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(M), dim3(256), 0, s, x, (const bf16_t*)E, h, rows, L, row0, d);
+    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(M), dim3(256), 0, s, x, (const bf16_t*)E, h, rows, L, row0, d, V,
+                       err);
   DLLM_LAUNCH_CHECK("embed");
 }
 
 // angle = pos * base^(-2j/hd) in float64 (positions reach 8k, where a float32
-// angle would already be off by ~1e-3 rad), stored as float32 cos/sin.
-__global__ void rope_table_kernel(float* cosb, float* sinb, int L, int half, double base, int hd) {
+// angle would already be off by ~1e-3 rad), stored as float32 cos/sin.  Thread
+// 0 also clears the forward's error word (err non-null).
+__global__ void rope_table_kernel(float* cosb, float* sinb, int L, int half, double base, int hd, int* err) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0 && err) *err = 0;
   if (i >= L * half) return;
   const int pos = i / half, j = i % half;
   const double inv_freq = pow(base, -2.0 * (double)j / (double)hd);
@@ -51,10 +60,11 @@ __global__ void rope_table_kernel(float* cosb, float* sinb, int L, int half, dou
   sinb[i] = (float)sn;
 }
 
-void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, hipStream_t s) {
+void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, int* err, hipStream_t s) {
   const int n = L * (hd / 2);
   if (n == 0) return;
-  hipLaunchKernelGGL(rope_table_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, cosb, sinb, L, hd / 2, base, hd);
+  hipLaunchKernelGGL(rope_table_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, cosb, sinb, L, hd / 2, base, hd,
+                     err);
   DLLM_LAUNCH_CHECK("rope_table");
 }
 
@@ -285,15 +295,23 @@ void launch_resid_rmsnorm(float* h, const PendingResid& pend, const bf16_t* g, b
 
 // rmsnorm_vec_kernel for the bf16 head rows, also writing the rows in MFMA
 // B-operand order (row r < 32, columns 4c .. 4c+3 are eight contiguous bytes:
-// slice c / 4, lane r + 32 ((c / 2) % 2), elements 4 (c % 2) ..).
+// slice c / 4, lane r + 32 ((c / 2) % 2), elements 4 (c % 2) ..).  With S > 0
+// split-K partials [S, MN] pending from the last residual GEMM, each float4 of
+// the row is first h + ((p_0 + p_1) + ... + p_{S-1}) (splitk_resid_kernel's
+// operations and order), written back to h.  Block 0 also zeroes the LM
+// head's ticket.
 template <int NV>
-__global__ void __launch_bounds__(256) rmsnorm_head_kernel(const float* __restrict__ h, const bf16_t* __restrict__ g,
+__global__ void __launch_bounds__(256) rmsnorm_head_kernel(float* __restrict__ h, const float* __restrict__ part,
+                                                           int S, long MN, const bf16_t* __restrict__ g,
                                                            bf16_t* __restrict__ out, bf16_t* __restrict__ outf,
-                                                           int rows, int L, int row0, int d, float eps) {
+                                                           int rows, int L, int row0, int d, float eps,
+                                                           int* __restrict__ ticket) {
   const int r = blockIdx.x;
   const int b = r / rows, i = r % rows;
-  const float* src = h + ((size_t)b * L + row0 + i) * d;
+  const size_t hrow = (size_t)b * L + row0 + i;
+  float* src = h + hrow * d;
   const int d4 = d / 4;
+  if (ticket && r == 0 && threadIdx.x == 0) *ticket = 0;
   float4 v[NV];
   double ss = 0.0;
 #pragma unroll
@@ -301,15 +319,32 @@ __global__ void __launch_bounds__(256) rmsnorm_head_kernel(const float* __restri
     const int c = threadIdx.x + 256 * j;
     if (c < d4) {
       v[j] = Vec4<float>::load(src, c);
+      if (S > 0) {
+        const size_t pi = hrow * d4 + c;
+        float4 acc = reinterpret_cast<const float4*>(part)[pi];
+#pragma unroll 4
+        for (int z = 1; z < S; ++z) {
+          const float4 p = reinterpret_cast<const float4*>(part + (size_t)z * MN)[pi];
+          acc.x += p.x;
+          acc.y += p.y;
+          acc.z += p.z;
+          acc.w += p.w;
+        }
+        v[j].x += acc.x;
+        v[j].y += acc.y;
+        v[j].z += acc.z;
+        v[j].w += acc.w;
+        Vec4<float>::store(src, c, v[j]);
+      }
       ss += (double)v[j].x * v[j].x + (double)v[j].y * v[j].y + (double)v[j].z * v[j].z + (double)v[j].w * v[j].w;
     }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
-  __shared__ double part[4];
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __shared__ double wsum[4];
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const double tot = (part[0] + part[1]) + (part[2] + part[3]);
+  const double tot = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
   const float rstd = (float)(1.0 / sqrt(tot / (double)d + (double)eps));
   bf16_t* dst = out + (size_t)r * d;
 #pragma unroll
@@ -325,19 +360,27 @@ __global__ void __launch_bounds__(256) rmsnorm_head_kernel(const float* __restri
   }
 }
 
-void launch_rmsnorm_head(const float* h, const bf16_t* g, bf16_t* out, bf16_t* outf, int B, int rows, int L,
-                         int row0, int d, float eps, hipStream_t s) {
+void launch_rmsnorm_head(float* h, const PendingResid* pend, const bf16_t* g, bf16_t* out, bf16_t* outf, int B,
+                         int rows, int L, int row0, int d, float eps, int* ticket, hipStream_t s) {
   if (B * rows == 0) return;
-  if (d % 4 != 0 || d > 8192 || ((uintptr_t)h | (uintptr_t)g | (uintptr_t)out | (uintptr_t)outf) % 16 != 0)
+  const float* part = pend && pend->split > 0 ? pend->part : nullptr;
+  const int S = part ? pend->split : 0;
+  if (d % 4 != 0 || d > 8192 ||
+      ((uintptr_t)h | (uintptr_t)g | (uintptr_t)out | (uintptr_t)outf | (uintptr_t)part) % 16 != 0)
     throw HipError("rmsnorm_head: needs d % 4 == 0, d <= 8192 and 16-byte aligned rows");
   if (outf && B * rows > HEAD_FRAG_ROWS) throw HipError("rmsnorm_head: operand-order copy holds 32 rows");
+  const long MN = (long)B * L * d;
   const int nv = ceil_div(d, 1024);
+  const dim3 grid(B * rows), blk(256);
   if (nv <= 2)
-    hipLaunchKernelGGL(rmsnorm_head_kernel<2>, dim3(B * rows), dim3(256), 0, s, h, g, out, outf, rows, L, row0, d, eps);
+    hipLaunchKernelGGL(rmsnorm_head_kernel<2>, grid, blk, 0, s, h, part, S, MN, g, out, outf, rows, L, row0, d, eps,
+                       ticket);
   else if (nv <= 4)
-    hipLaunchKernelGGL(rmsnorm_head_kernel<4>, dim3(B * rows), dim3(256), 0, s, h, g, out, outf, rows, L, row0, d, eps);
+    hipLaunchKernelGGL(rmsnorm_head_kernel<4>, grid, blk, 0, s, h, part, S, MN, g, out, outf, rows, L, row0, d, eps,
+                       ticket);
   else
-    hipLaunchKernelGGL(rmsnorm_head_kernel<8>, dim3(B * rows), dim3(256), 0, s, h, g, out, outf, rows, L, row0, d, eps);
+    hipLaunchKernelGGL(rmsnorm_head_kernel<8>, grid, blk, 0, s, h, part, S, MN, g, out, outf, rows, L, row0, d, eps,
+                       ticket);
   DLLM_LAUNCH_CHECK("rmsnorm_head");
 }
 
@@ -354,9 +397,11 @@ void launch_rmsnorm(const float* h, const void* g, void* out, int dtype, int B, 
 __global__ void state_init_kernel(const int32_t* __restrict__ prompt, int32_t* __restrict__ x,
                                   int32_t* __restrict__ commit_step, int8_t* __restrict__ reason,
                                   float* __restrict__ sv, int32_t* __restrict__ budget, int32_t* __restrict__ ell,
-                                  int32_t* __restrict__ done, int B, int P, int G, int mask_id) {
+                                  int32_t* __restrict__ done, int B, int P, int G, int mask_id,
+                                  int* __restrict__ err) {
   const int L = P + G;
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0 && err) *err = 0;
   if (i < B * L) {
     const int b = i / L, l = i % L;
     x[i] = l < P ? prompt[(size_t)b * P + l] : mask_id;
@@ -375,11 +420,11 @@ __global__ void state_init_kernel(const int32_t* __restrict__ prompt, int32_t* _
 
 void launch_state_init(const int32_t* prompt, int32_t* x, int32_t* commit_step, int8_t* reason, float* sv,
                        int32_t* budget, int32_t* ell, int32_t* done, int B, int P, int G, int mask_id,
-                       hipStream_t s) {
+                       int* err, hipStream_t s) {
   const int n = B * (P + G);
   if (n == 0) return;
   hipLaunchKernelGGL(state_init_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, s, prompt, x, commit_step, reason,
-                     sv, budget, ell, done, B, P, G, mask_id);
+                     sv, budget, ell, done, B, P, G, mask_id, err);
   DLLM_LAUNCH_CHECK("state_init");
 }
 

@@ -5,18 +5,24 @@
 namespace dllm {
 
 // ---- k_misc.hip ------------------------------------------------------------
-// h[b*rows + i, :] = float(E[x[b*L + row0 + i], :]) for b < B, i < rows.
+// Bits of the workspace's error word, set by kernels that meet an input they
+// cannot represent and reported (then cleared) by the commit kernel.
+enum { ERR_TOKEN_RANGE = 1, ERR_V_RANGE = 2 };
+// h[b*rows + i, :] = float(E[x[b*L + row0 + i], :]) for b < B, i < rows.  An id
+// outside [0, V) gathers a zero row and sets ERR_TOKEN_RANGE in *err.
 void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int B, int rows, int L, int row0, int d,
-                  hipStream_t s);
-// cos/sin [L, hd/2] of pos * base^(-2j/hd), evaluated in float64, stored float32.
-void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, hipStream_t s);
+                  int V, int* err, hipStream_t s);
+// cos/sin [L, hd/2] of pos * base^(-2j/hd), evaluated in float64, stored float32;
+// a non-null err word is cleared first (a forward starts with a clean word).
+void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, int* err, hipStream_t s);
 // out[b*rows + i, :] = act(RMSNorm(h[b*L + row0 + i, :]) * g) for b < B, i < rows.
 void launch_rmsnorm(const float* h, const void* g, void* out, int dtype, int B, int rows, int L, int row0,
                     int d, float eps, hipStream_t s);
-// Decoding state initialisation (see dllm_state_init).
+// Decoding state initialisation (see dllm_state_init); a non-null err word is
+// cleared as well.
 void launch_state_init(const int32_t* prompt, int32_t* x, int32_t* commit_step, int8_t* reason, float* sv,
                        int32_t* budget, int32_t* ell, int32_t* done, int B, int P, int G, int mask_id,
-                       hipStream_t s);
+                       int* err, hipStream_t s);
 
 // ---- fp32 path (k_f32.hip) -------------------------------------------------
 // C[M, N] (+)= A[M, K] W[N, K]^T, all float32 row-major, C row stride ldc.
@@ -62,6 +68,9 @@ struct GemmArgs {
   // optional packed copy of Bv (launch_pack_gemm_weights): launches of at most
   // 128 rows then stream it instead of the row-major tensors
   const bf16_t* Wp;
+  // EPI_QKV_ROPE: error word; a v value beyond IEEE half's range is stored as
+  // +-65504 and sets ERR_V_RANGE
+  int* err;
 };
 int device_cu_count();  // compute units of the current device (256 if it cannot be queried)
 // Split-K partial tiles of a residual GEMM whose reduction into the residual
@@ -108,9 +117,13 @@ constexpr int HEAD_TILE = 256;
 constexpr int HEAD_FRAG_ROWS = 32;
 // Final RMSNorm of the head rows (bf16 model, d % 4 == 0, d <= 8192): out[B*rows,
 // d] row-major as launch_rmsnorm, and, when outf is non-null (B * rows <=
-// HEAD_FRAG_ROWS), the same values in the operand order above.
-void launch_rmsnorm_head(const float* h, const bf16_t* g, bf16_t* out, bf16_t* outf, int B, int rows, int L,
-                         int row0, int d, float eps, hipStream_t s);
+// HEAD_FRAG_ROWS), the same values in the operand order above.  Split-K
+// partials still pending from the last layer's down projection (pend->split >
+// 0, partials [S, B*L, d]) are added to the head rows of h first, as the fused
+// residual norm does; the other rows of h are left without them.  A non-null
+// ticket (the LM head's) is set to zero for the head kernel that follows.
+void launch_rmsnorm_head(float* h, const PendingResid* pend, const bf16_t* g, bf16_t* out, bf16_t* outf, int B,
+                         int rows, int L, int row0, int d, float eps, int* ticket, hipStream_t s);
 size_t head_bf16_packed_bytes(int V, int d);
 void launch_pack_head_bf16(const bf16_t* W, bf16_t* Wt, int V, int d, hipStream_t s);
 
@@ -137,7 +150,11 @@ struct CommitArgs {
   int budget_on, grind_on;
   float s_easy, s_hard; int p_easy, p_hard, b_easy, b_mid, b_hard;
   double eta_bar; int patience; float theta_fb;
-  int fixed_k;         // > 0: fixed-schedule baseline, commit this many tokens this step
+  int fixed;           // fixed-schedule baseline instead of the confidence-aware rule
+  int fixed_k;         // fixed schedule: tokens to commit this step (0 at steps past the block length)
+  // error word of the step's workspace (optional): its bits are reported in
+  // *all_done above bit 0 and the word is cleared
+  int* err;
 };
 void launch_commit(const CommitArgs& a, hipStream_t s);
 

@@ -96,3 +96,27 @@ def assert_bf16_flips(gpu, ref, what, max_frac=2e-3, max_ulps=1.0, rel_floor=3e-
     assert not bad.any(), f"{what}: {int(bad.sum())} elements off by more than {max_ulps} ulp; max {d.max():.3g}"
     assert frac <= max_frac, f"{what}: {frac:.2e} of elements differ (limit {max_frac})"
     return frac
+
+
+def tie_aware_predictor(logits_at, mask_id, gpu_argmax, tol, adopted):
+    """predict(x, blk, t) for the oracle controller from logits_at(x, blk, t) ->
+    [B, bl, V] (the oracle's logits).  Where the GPU recorded another argmax
+    whose oracle logit lies within 2 tol of the oracle's largest one (a logit
+    near-tie: both tokens are correct predictions to the tolerance), the GPU's
+    choice is taken, so the free-running decodes stay comparable; each such
+    adoption is appended to ``adopted`` as (blk, t, b, i)."""
+    def predict(x, blk, t):
+        lg = np.array(logits_at(x, blk, t), dtype=np.float64, copy=True)
+        conf, arg = ov.confidence_argmax(lg, mask_id)
+        g = np.asarray(gpu_argmax[blk, t])
+        lm = lg.copy()
+        lm[..., mask_id] = -np.inf
+        top = lm.max(axis=-1)
+        for b, i in zip(*np.nonzero(g != arg)):
+            gi = int(g[b, i])
+            if 0 <= gi < lg.shape[-1] and gi != mask_id and lm[b, i, gi] >= top[b, i] - 2 * tol:
+                arg[b, i] = gi
+                adopted.append((blk, t, int(b), int(i)))
+        return conf.astype(np.float32), arg
+
+    return predict

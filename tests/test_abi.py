@@ -63,7 +63,7 @@ def test_model_create_rejects_bad_shapes(kw, code):
     n = 3 + 9 * cfg.n_layers
     ptrs = (ctypes.c_void_p * n)(*([0x1000] * n))
     h = ctypes.c_void_p()
-    rc = lib.dllm_model_create(ctypes.byref(cfg), ptrs, n, ctypes.byref(h))
+    rc = lib.dllm_model_create(ctypes.byref(cfg), ptrs, n, None, 0, None, ctypes.byref(h))
     assert rc == code, lib.dllm_last_error()
     assert lib.dllm_last_error().decode() != ""
 
@@ -73,10 +73,54 @@ def test_model_create_rejects_wrong_weight_count_and_nulls():
     cfg = _cfg()
     ptrs = (ctypes.c_void_p * 5)(*([0x1000] * 5))
     h = ctypes.c_void_p()
-    assert lib.dllm_model_create(ctypes.byref(cfg), ptrs, 5, ctypes.byref(h)) == -1
+    assert lib.dllm_model_create(ctypes.byref(cfg), ptrs, 5, None, 0, None, ctypes.byref(h)) == -1
     ptrs = (ctypes.c_void_p * 12)(*([0x1000] * 11 + [None]))
-    assert lib.dllm_model_create(ctypes.byref(cfg), ptrs, 12, ctypes.byref(h)) == -1
-    assert lib.dllm_model_create(None, ptrs, 12, ctypes.byref(h)) == -1
+    assert lib.dllm_model_create(ctypes.byref(cfg), ptrs, 12, None, 0, None, ctypes.byref(h)) == -1
+    assert lib.dllm_model_create(None, ptrs, 12, None, 0, None, ctypes.byref(h)) == -1
+
+
+def test_model_buffer_size():
+    """The model buffer holds the bf16 LM head's tiled copy: vocabulary rows padded
+    to 256, d bf16 values each; an fp32 model needs none."""
+    lib = B.lib()
+    n = ctypes.c_size_t()
+    for V, d in ((64, 256), (126464, 4096), (152064, 3584), (257, 512)):
+        cfg = _cfg(vocab=V, mask_id=V - 1, d_model=d)
+        assert lib.dllm_model_buffer_size(ctypes.byref(cfg), ctypes.byref(n)) == 0, lib.dllm_last_error()
+        assert n.value == -(-V // 256) * 256 * d * 2
+    cfg = _cfg(dtype=B.DLLM_F32, head_dim=64)
+    assert lib.dllm_model_buffer_size(ctypes.byref(cfg), ctypes.byref(n)) == 0 and n.value == 0
+    assert lib.dllm_model_buffer_size(ctypes.byref(_cfg(mask_id=64)), ctypes.byref(n)) == -1
+    assert lib.dllm_model_buffer_size(None, ctypes.byref(n)) == -1
+
+
+def test_model_create_checks_the_caller_buffer():
+    """A bf16 model keeps its LM-head copy in the caller's buffer: a missing,
+    misaligned or short buffer is rejected before any device work."""
+    lib = B.lib()
+    cfg = _cfg()
+    n = 3 + 9 * cfg.n_layers
+    ptrs = (ctypes.c_void_p * n)(*([0x1000] * n))
+    need = ctypes.c_size_t()
+    assert lib.dllm_model_buffer_size(ctypes.byref(cfg), ctypes.byref(need)) == 0
+    h = ctypes.c_void_p()
+    assert lib.dllm_model_create(ctypes.byref(cfg), ptrs, n, None, need.value, None, ctypes.byref(h)) == -1
+    assert lib.dllm_model_create(ctypes.byref(cfg), ptrs, n, ctypes.c_void_p(0x1080), need.value, None,
+                                 ctypes.byref(h)) == -1
+    assert lib.dllm_model_create(ctypes.byref(cfg), ptrs, n, ctypes.c_void_p(0x1000), need.value - 256, None,
+                                 ctypes.byref(h)) == -4
+    assert "model_buf" in lib.dllm_last_error().decode()
+
+
+def test_library_allocates_no_device_memory():
+    """Every device buffer is the caller's: no allocation, free or device-wide
+    synchronisation anywhere in the library's sources."""
+    csrc = os.path.join(ROOT, "paper_2608_22646_amd", "csrc")
+    banned = re.compile(r"\b(hipMalloc\w*|hipFree\w*|hipExtMalloc\w*|hipMallocManaged|hipDeviceSynchronize|"
+                        r"hipMemset\w*)\s*\(")
+    for f in sorted(os.listdir(csrc)):
+        text = re.sub(r"//[^\n]*|/\*.*?\*/", "", open(os.path.join(csrc, f)).read(), flags=re.S)
+        assert not banned.findall(text), (f, banned.findall(text))
 
 
 def _commit_rc(ctl=None, **kw):

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from helpers import assert_state_equal, replay, say
+from helpers import assert_state_equal, oracle_params, replay, say
 from oracle import controller as oc
 from paper_2608_22646_amd import binding as B
 from paper_2608_22646_amd import synth
@@ -87,6 +87,7 @@ CASES = [
     ("uniform", 2, 32, 2, True, dict(fixed=True, steps_per_block=12)),
     ("grid", 2, 64, 2, True, dict(fixed=True, steps_per_block=64)),
     ("uniform", 2, 4, 3, True, dict(fixed=True, steps_per_block=3)),
+    ("uniform", 2, 32, 2, True, dict(fixed=True, steps_per_block=40)),   # T > block length
 ]
 PRESETS = ["cai", "cai_gate_off", "apd", "apd_block", "apd_block_budget", "fixed_threshold_0.9",
            "fixed_threshold_0.7", "apd_0.9_to_0.5", "fixed_schedule"]
@@ -131,6 +132,38 @@ def test_commit_fixed_schedule_hand_trace():
     assert st.commit_step.cpu().tolist() == [[1, 0, 3, 2]]
     assert st.reason.cpu().tolist() == [[B.R_FIXED] * 4]
     assert st.x.cpu().tolist() == [[0, 0, 11, 20, 33, 42]]
+
+
+def test_commit_fixed_schedule_step_with_no_quota():
+    """T = 40 > block length 32: k_t = 0 at local steps 32..39, where the fixed
+    schedule commits nothing (not the confidence-gated rule); the last step
+    flushes.  Driven directly on a fresh block, against the oracle's step."""
+    ctl = B.Controller(block_len=32, fixed=True, steps_per_block=40)
+    Bn, P, G = 2, 3, 32
+    prompts = synth.make_ints((Bn, P), 41, 0, MASK)
+    conf = synth.make_uniform((Bn, 32), 42).to(torch.float32)
+    arg = synth.make_ints((Bn, 32), 43, 0, MASK)
+    p = oracle_params(ctl)
+    for t in (33, 39):
+        say(f"commit fixed schedule, quota-free step t={t}")
+        st = B.DecodeState(Bn, P, G)
+        B.state_init(MASK, prompts.cuda(), G, st)
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        B.commit(ctl, st, conf.cuda(), arg.cuda(), 0, t, MASK, flag)
+        torch.cuda.synchronize()
+        ref = oc.init_state(prompts.numpy(), G, MASK)
+        done = []
+        for b in range(Bn):
+            _, exited = oc.step_sequence(ref, b, P, 0, t, conf[b].numpy(), arg[b].numpy().astype(np.int64), 0, p)
+            done.append(exited)
+        np.testing.assert_array_equal(st.commit_step.cpu().numpy(), ref.commit_step)
+        np.testing.assert_array_equal(st.reason.cpu().numpy().astype(np.int64), ref.reason)
+        np.testing.assert_array_equal(st.x.cpu().numpy(), ref.x)
+        assert int(flag.item()) == int(all(done))
+        if t == 33:
+            assert (st.commit_step.cpu().numpy() == -1).all(), "a quota-free step committed tokens"
+        else:
+            assert (st.reason.cpu().numpy() == B.R_FLUSH).all()
 
 
 # hand-derived traces (the same ones that pin the oracle) run through the kernel

@@ -1,0 +1,87 @@
+"""End-to-end bf16 parity by depth: the LLaDA-8B-shaped forward on the GPU
+against the oracle's bf16 forward (float32 products), logits and confidences of
+the first block (Box 1), teacher-forced on the workload's first input (prompt
+set 0 + 256 masks), after 1, 2, 4, 8, 16 and 32 layers.
+
+Two correct float32 accumulation orders of a bf16 model drift apart by bf16
+rounding flips that later layers carry forward; the oracle's own float32 and
+float64 runs of this model and input differ by the amounts in
+tests/golden/bf16_drift_llada.json.  The bars are derived from that table: the
+GPU may differ from the float32 oracle by at most twice the oracle's own
+spread at that depth (logits), and by at most 2e-2 or twice the table's
+spread, whichever is larger (confidences).  An argmax may differ only where
+the oracle's top-two logit gap is within twice the measured logit error.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import say, to_np
+from oracle import forward as of
+from oracle import vocab as ov
+from paper_2608_22646_amd import binding as B
+from paper_2608_22646_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+DRIFT = {r["depth"]: r for r in json.load(open(os.path.join(HERE, "golden", "bf16_drift_llada.json")))["rows"]}
+DEPTHS = (1, 2, 4, 8, 16, 32)
+
+
+def bars(depth):
+    r = DRIFT[depth]
+    return 2.0 * r["logit_max_abs_diff"], max(2e-2, 2.0 * r["conf_max_abs_diff"])
+
+
+def test_llada_forward_against_oracle_by_depth():
+    wl = synth.WORKLOADS["llada_b1"]
+    cfg = wl.model
+    P, G, bl = wl.prompt_len, wl.gen_len, wl.block_len
+    L = P + G
+    say("llada_b1 depth parity: weights")
+    w = synth.make_weights(cfg, "cuda")
+    model = B.Model(cfg, w)
+    x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((1, G), cfg.mask_id)], axis=1)
+    ws = model.workspace(1, L, bl)
+    # layer calls (rows 0) and head calls (rows bl) share h and the RoPE tables
+    l0, lb = model.layout(1, L, 0), model.layout(1, L, bl)
+    assert [getattr(l0, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")] == \
+        [getattr(lb, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")]
+    model.embed(torch.from_numpy(x.astype(np.int32)).cuda(), ws)
+    h = to_np(w[0], np.float32)[x].astype(np.float64)
+    cos, sin = of.rope_tables(L, cfg.head_dim, cfg.rope_base)
+    final_norm, lm = to_np(w[-2]), to_np(w[-1])
+    rows = np.arange(P, P + bl)
+    report = []
+    for l in range(cfg.n_layers):
+        model.layer(l, 2, 1, L, ws)
+        lw = [to_np(t) for t in w[1 + 9 * l: 10 + 9 * l]]
+        h = of.layer(cfg, lw, h, cos, sin, "bf16")
+        del lw
+        depth = l + 1
+        if depth not in DEPTHS:
+            continue
+        say(f"llada_b1 depth {depth}: head")
+        conf_g, arg_g, lg_g = model.head(1, L, P, bl, ws, logits=True)
+        torch.cuda.synchronize()
+        lg_ref, _ = of.lm_head(cfg, h[0, rows, :], final_norm, lm, "bf16")
+        conf_ref, arg_ref = ov.confidence_argmax(lg_ref, cfg.mask_id)
+        lg = to_np(lg_g[0], np.float64)
+        err = np.abs(lg - lg_ref)
+        err[:, cfg.mask_id] = 0
+        cerr = np.abs(to_np(conf_g[0], np.float64) - conf_ref).max()
+        bar_l, bar_c = bars(depth)
+        diff = arg_g[0].cpu().numpy() != arg_ref
+        gap = ov.top2_gap(lg_ref, cfg.mask_id)
+        rec = dict(depth=depth, logit_err=float(err.max()), logit_bar=bar_l, conf_err=float(cerr), conf_bar=bar_c,
+                   argmax_diff=int(diff.sum()))
+        report.append(rec)
+        say("  " + json.dumps(rec))
+        assert err.max() <= bar_l, rec
+        assert cerr <= bar_c, rec
+        assert np.all(gap[diff] <= 2 * err.max()), rec
+    assert [r["depth"] for r in report] == list(DEPTHS)

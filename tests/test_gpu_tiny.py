@@ -8,13 +8,14 @@ with gating on and off, the fixed-schedule baseline and three ablation presets.
     logit near-tie (reported);
   * the oracle controller replayed on the GPU's own predictions reproduces the
     GPU's decisions bit for bit;
-  * the free-running oracle decode equals the GPU decode.
+  * the free-running oracle decode equals the GPU decode (at a logit near-tie
+    the oracle takes the GPU's token, equally correct to the tolerance).
 """
 import numpy as np
 import pytest
 import torch
 
-from helpers import assert_state_equal, oracle_params, replay, say, to_np, x_at_step
+from helpers import assert_state_equal, oracle_params, replay, say, tie_aware_predictor, to_np, x_at_step
 from oracle import controller as oc
 from oracle import forward as of
 from oracle import vocab as ov
@@ -83,12 +84,16 @@ def test_tiny_generate_matches_oracle(tiny, name):
             assert np.all(gap[diff] < 2 * TOL), "argmax differs away from a near-tie"
             near += int(diff.sum())
 
-    # (3) free-running oracle decode
-    pred = oc.model_predictor(lambda x, rows: of.forward(cfg, wnp, x, rows=rows), P, bl, cfg.mask_id)
+    # (3) free-running oracle decode (at a logit near-tie the oracle takes the
+    # GPU's token, equally correct to the tolerance, so it is never skipped)
+    adopted = []
+    pred = tie_aware_predictor(
+        lambda x, blk, t: of.forward(cfg, wnp, x, rows=np.arange(P + blk * bl, P + (blk + 1) * bl)),
+        cfg.mask_id, at, TOL, adopted)
     free = oc.generate(pred, prompts.numpy(), G, cfg.mask_id, oracle_params(ctl))
-    if near == 0:
-        assert_state_equal(st, res.forwards, free, s_tol=TOL)
-    say(f"tiny {name}: forwards {res.forwards}, argmax near-ties {near}")
+    assert_state_equal(st, res.forwards, free, s_tol=TOL)
+    assert len(adopted) <= near
+    say(f"tiny {name}: forwards {res.forwards}, argmax near-ties {near}, adopted in the free run {len(adopted)}")
     if ctl.fixed:
         assert res.forwards == [ctl.T] * (G // bl)
 
