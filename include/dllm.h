@@ -253,6 +253,25 @@ int dllm_layer(const dllm_model* model, int32_t layer, int32_t part, int32_t B, 
 int dllm_head(const dllm_model* model, int32_t B, int32_t L, int32_t row0, int32_t rows, float* conf,
               int32_t* argmax, float* logits, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * dllm_head without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same final RMSNorm + LM head + vocabulary reduction,
+ * with the same kernels and results bit for bit, reading the final residual
+ * from the caller's h (device float32 [B*L, d], 16-byte aligned, read only)
+ * and keeping its scratch (normed rows, per-workgroup partials, the merge
+ * ticket) in a static device array of 8 MiB that the library holds on each GPU
+ * it runs on until the process ends.  No call allocates.  The array is shared
+ * by every call on that GPU: calls that overlap on one GPU (other streams,
+ * other threads) race and must be ordered by the caller; each call starts by
+ * zeroing what must start at zero.  conf/argmax/logits as for dllm_head.
+ * Errors: DLLM_ENOMEM when the head rows need more than the static scratch
+ * (bf16: up to 256 rows at d <= 8192 fit; float32: B*rows*(d + V)*4 bytes
+ * must fit), the checks of dllm_head otherwise.
+ */
+int dllm_head_noalloc(const dllm_model* model, const float* h, int32_t B, int32_t L, int32_t row0, int32_t rows,
+                      float* conf, int32_t* argmax, float* logits, void* stream);
+
 /* dllm_embed + every layer + dllm_head: one forward on x [B, L] (device).
  * Afterwards the workspace's h holds the final residual of the head rows only
  * (the last layer's split-K partials are added by the final norm to those

@@ -72,6 +72,7 @@ _SIGS = {
     "dllm_layer": (_i32, [_vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
     "dllm_head": (_i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "dllm_forward": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "dllm_head_noalloc": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "dllm_state_init": (_i32, [_i32, _vp, _i32, _i32, _i32, _c.POINTER(State), _vp]),
     "dllm_commit": (_i32, [_c.POINTER(CaiParams), _c.POINTER(State), _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                            _i32, _vp, _vp]),
@@ -315,6 +316,16 @@ class Model:
         lg = torch.empty((B * rows, self.cfg.vocab), dtype=torch.float32, device=dev) if logits else None
         check(lib().dllm_head(self.h, B, L, row0, rows, _ptr(conf), _ptr(arg), _ptr(lg), _ptr(ws), ws.numel(),
                               _stream(stream)))
+        return conf.view(B, rows), arg.view(B, rows), (lg.view(B, rows, -1) if logits else None)
+
+    def head_noalloc(self, h, B, L, row0, rows, logits=False, stream=None):
+        """dllm_head_noalloc on the caller's residual h (float32 [B*L, d])."""
+        dev = h.device
+        conf = torch.empty((B * rows,), dtype=torch.float32, device=dev)
+        arg = torch.empty((B * rows,), dtype=torch.int32, device=dev)
+        lg = torch.empty((B * rows, self.cfg.vocab), dtype=torch.float32, device=dev) if logits else None
+        check(lib().dllm_head_noalloc(self.h, _ptr(h), B, L, row0, rows, _ptr(conf), _ptr(arg), _ptr(lg),
+                                      _stream(stream)))
         return conf.view(B, rows), arg.view(B, rows), (lg.view(B, rows, -1) if logits else None)
 
     def forward(self, x, row0, rows, ws=None, logits=False, stream=None):

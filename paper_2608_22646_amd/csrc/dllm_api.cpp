@@ -12,6 +12,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include <string>
 #include <vector>
@@ -416,36 +417,66 @@ void run_layer(const dllm_model* m, int layer, int part, int B, int L, void* ws,
     run_layer_f32(m, layer, part, B, L, ws, lay, s, rows);
 }
 
-// Final norm and LM head on rows [row0, row0 + rows) of every sequence; pend:
-// split-K partials the last layer's down projection left pending (added to the
-// head rows by the final norm; the other rows of h stay without them).
-void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf, int32_t* argmax, float* logits,
-              void* ws, const Layout& lay, hipStream_t s, const PendingResid* pend = nullptr) {
+// Buffers of the final norm and LM head: the residual h they read and their
+// scratch (normed rows, the operand-order copy, the per-workgroup partials and
+// ticket of the bf16 head; the logits of the float32 head).
+struct HeadBufs {
+  float* h;
+  void* hb;
+  bf16_t* hbf;
+  float* logits;
+  float* part_m;
+  float* part_s;
+  int32_t* part_i;
+  int* ticket;
+};
+
+HeadBufs head_bufs(void* ws, const Layout& lay, const dllm_model_cfg& c) {
+  HeadBufs b{};
+  b.h = at<float>(ws, lay.h);
+  b.hb = at<void>(ws, lay.hb);
+  if (c.dtype == DLLM_F32) {
+    b.logits = at<float>(ws, lay.logits);
+  } else {
+    b.hbf = at<bf16_t>(ws, lay.hbf);
+    b.part_m = at<float>(ws, lay.part_m);
+    b.part_s = at<float>(ws, lay.part_s);
+    b.part_i = at<int32_t>(ws, lay.part_i);
+    b.ticket = at<int>(ws, lay.ticket);
+  }
+  return b;
+}
+
+// Final norm and LM head on rows [row0, row0 + rows) of every sequence of
+// hb.h ([B*L, d]); pend: split-K partials the last layer's down projection
+// left pending (added to the head rows by the final norm; the other rows of h
+// stay without them).
+void run_head_bufs(const dllm_model* m, int B, int L, int row0, int rows, float* conf, int32_t* argmax,
+                   float* logits, const HeadBufs& hb, hipStream_t s, const PendingResid* pend = nullptr) {
   const auto& c = m->cfg;
   const int nl = c.n_layers;
   const int R = B * rows;
   // bf16: up to HEAD_FRAG_ROWS head rows also go to an MFMA-operand-order copy
   // for the streaming head kernel
-  bf16_t* hbf = c.dtype == DLLM_BF16 && R <= HEAD_FRAG_ROWS ? at<bf16_t>(ws, lay.hbf) : nullptr;
+  bf16_t* hbf = c.dtype == DLLM_BF16 && R <= HEAD_FRAG_ROWS ? hb.hbf : nullptr;
   {
     ProfScope p(m, PK_NORM, s);
     // the head kernel's ticket is zeroed here (no memset node in a captured step)
     if (c.dtype == DLLM_BF16)
-      launch_rmsnorm_head(at<float>(ws, lay.h), pend, static_cast<const bf16_t*>(W(m, 1 + 9 * nl)),
-                          at<bf16_t>(ws, lay.hb), hbf, B, rows, L, row0, c.d_model, c.rms_eps, at<int>(ws, lay.ticket),
-                          s);
+      launch_rmsnorm_head(hb.h, pend, static_cast<const bf16_t*>(W(m, 1 + 9 * nl)), static_cast<bf16_t*>(hb.hb), hbf,
+                          B, rows, L, row0, c.d_model, c.rms_eps, hb.ticket, s);
     else
-      launch_rmsnorm(at<float>(ws, lay.h), W(m, 1 + 9 * nl), at<void>(ws, lay.hb), c.dtype, B, rows, L, row0,
-                     c.d_model, c.rms_eps, s);
+      launch_rmsnorm(hb.h, W(m, 1 + 9 * nl), hb.hb, c.dtype, B, rows, L, row0, c.d_model, c.rms_eps, s);
   }
   ProfScope p(m, PK_HEAD, s);
   if (c.dtype == DLLM_F32) {
-    float* lg = logits ? logits : at<float>(ws, lay.logits);
-    launch_gemm_f32(at<float>(ws, lay.hb), Wf(m, 2 + 9 * nl), lg, R, c.vocab, c.d_model, c.vocab, false, s);
+    float* lg = logits ? logits : hb.logits;
+    launch_gemm_f32(static_cast<const float*>(hb.hb), Wf(m, 2 + 9 * nl), lg, R, c.vocab, c.d_model, c.vocab, false,
+                    s);
     launch_vocab_reduce_f32(lg, R, c.vocab, c.mask_id, conf, argmax, s);
   } else {
     HeadArgs a{};
-    a.hb = at<bf16_t>(ws, lay.hb);
+    a.hb = static_cast<const bf16_t*>(hb.hb);
     a.hbf = hbf;
     a.W = m->head_tiled;
     a.R = R;
@@ -455,12 +486,17 @@ void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf
     a.conf = conf;
     a.argmax = argmax;
     a.logits = logits;
-    a.part_m = at<float>(ws, lay.part_m);
-    a.part_s = at<float>(ws, lay.part_s);
-    a.part_i = at<int32_t>(ws, lay.part_i);
-    a.ticket = at<int>(ws, lay.ticket);
+    a.part_m = hb.part_m;
+    a.part_s = hb.part_s;
+    a.part_i = hb.part_i;
+    a.ticket = hb.ticket;
     launch_head_bf16(a, s);
   }
+}
+
+void run_head(const dllm_model* m, int B, int L, int row0, int rows, float* conf, int32_t* argmax, float* logits,
+              void* ws, const Layout& lay, hipStream_t s, const PendingResid* pend = nullptr) {
+  run_head_bufs(m, B, L, row0, rows, conf, argmax, logits, head_bufs(ws, lay, m->cfg), s, pend);
 }
 
 // ---------------------------------------------------------------- controller
@@ -645,6 +681,58 @@ int finish(const ApiError& e) {
   return e.code;
 }
 
+}  // namespace
+
+// ---------------------------------------------------------------- static scratch
+// Scratch of dllm_head_noalloc: one array per GPU, resident until the process
+// ends.  Host code never uses the name (a host-side stand-in); the device
+// address comes from hipGetSymbolAddress, taken once per device.
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+// The current device's copy of `scratch` (looked up on its first use on that
+// device, with the device current).
+void* device_scratch() {
+  int dev = -1;
+  hip_check(hipGetDevice(&dev), "hipGetDevice");
+  require(dev >= 0 && dev < MAX_DEVICES, DLLM_EUNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    hip_check(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    require(p != nullptr, DLLM_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
+// The head's scratch carved out of `base` (nullptr: sizes only); returns the bytes.
+size_t noalloc_head_layout(const dllm_model_cfg& c, int R, char* base, HeadBufs* b) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* at = base ? base + off : nullptr;
+    off += align256(bytes);
+    return at;
+  };
+  const size_t act = c.dtype == DLLM_F32 ? 4 : 2;
+  b->hb = take((size_t)R * c.d_model * act);
+  if (c.dtype == DLLM_F32) {
+    b->logits = reinterpret_cast<float*>(take((size_t)R * c.vocab * 4));
+  } else {
+    const size_t slots = (size_t)head_bf16_tiles(c.vocab) * R * 4;
+    b->hbf = reinterpret_cast<bf16_t*>(take((size_t)HEAD_FRAG_ROWS * c.d_model * 2));
+    b->part_m = reinterpret_cast<float*>(take(slots));
+    b->part_s = reinterpret_cast<float*>(take(slots));
+    b->part_i = reinterpret_cast<int32_t*>(take(slots));
+    b->ticket = reinterpret_cast<int*>(take(4));
+  }
+  return off;
+}
 }  // namespace
 
 #define API_BEGIN \
@@ -848,6 +936,27 @@ int dllm_head(const dllm_model* m, int32_t B, int32_t L, int32_t row0, int32_t r
   Layout lay;
   check_ws(m, B, L, rows, ws, ws_bytes, &lay);
   run_head(m, B, L, row0, rows, conf, argmax, logits, ws, lay, (hipStream_t)stream);
+  API_END
+}
+
+int dllm_head_noalloc(const dllm_model* m, const float* h, int32_t B, int32_t L, int32_t row0, int32_t rows,
+                      float* conf, int32_t* argmax, float* logits, void* stream) {
+  API_BEGIN
+  check_model(m);
+  require(h && conf && argmax, DLLM_EINVAL, "h/conf/argmax is NULL");
+  require(((uintptr_t)h & 15) == 0, DLLM_EINVAL, "h must be 16-byte aligned");
+  require(B >= 1 && B <= 16, DLLM_EUNSUPPORTED, "batch must be in [1, 16]");
+  require(L >= 1 && row0 >= 0 && rows >= 1 && row0 + rows <= L, DLLM_ESHAPE, "rows out of range");
+  if (m->cfg.dtype == DLLM_BF16)
+    require((long)B * rows <= head_bf16_max_rows(), DLLM_EUNSUPPORTED, "B * rows exceeds the LM-head kernel limit");
+  HeadBufs hb{};
+  const size_t need = noalloc_head_layout(m->cfg, B * rows, nullptr, &hb);
+  require(need <= NOALLOC_SCRATCH_BYTES, DLLM_ENOMEM,
+          "dllm_head_noalloc needs " + std::to_string(need) + " bytes of scratch; the static scratch holds " +
+              std::to_string(NOALLOC_SCRATCH_BYTES));
+  noalloc_head_layout(m->cfg, B * rows, static_cast<char*>(device_scratch()), &hb);
+  hb.h = const_cast<float*>(h);  // read only: no split-K partials are pending here
+  run_head_bufs(m, B, L, row0, rows, conf, argmax, logits, hb, (hipStream_t)stream);
   API_END
 }
 
