@@ -390,9 +390,11 @@ int dllm_generate_kv(const dllm_model* model, const dllm_cai_params* params, int
                      void* kv_cache, size_t kv_bytes, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Per-kernel timing with HIP events recorded on the launch stream around each
- * launch of the selected kernel classes.  kind: 0 = q/k/v, output and down
- * GEMMs, 1 = attention, 2 = LM head + reduction, 3 = commit, 4 = norms and
- * embedding, 5 = gate/up GEMM.  dllm_prof_enable(model, mask) starts recording
+ * launch of the selected kernel classes.  kind: 0 = q/k/v GEMM (with RoPE),
+ * 1 = attention, 2 = LM head + reduction, 3 = commit, 4 = norms and
+ * embedding (with the residual GEMMs' split-K partials they fold in), 5 =
+ * gate/up GEMM (with SwiGLU), 6 = output projection, 7 = down projection.
+ * dllm_prof_enable(model, mask) starts recording
  * the kinds whose bit (1 << kind) is set and clears earlier records (mask 0
  * stops); dllm_prof_read waits for the recorded work and returns the summed
  * duration in milliseconds and the launch count of one kind.  Events are host

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libdllm.so")
 DLLM_F32, DLLM_BF16 = 0, 1
 F_BLOCK_SCHED, F_POS, F_BUDGET, F_GRIND, F_FIXED = 1, 2, 4, 8, 16
 R_MASKED, R_THRESH, R_BUDGET, R_GRIND, R_FLUSH, R_FIXED = 0, 1, 2, 3, 4, 5
-PROF_GEMM, PROF_ATTN, PROF_HEAD, PROF_COMMIT, PROF_NORM, PROF_GATEUP = range(6)
+PROF_QKV, PROF_ATTN, PROF_HEAD, PROF_COMMIT, PROF_NORM, PROF_GATEUP, PROF_OPROJ, PROF_DOWN = range(8)
 
 _c = ctypes
 _i32, _u32, _f32, _f64, _vp, _sz = _c.c_int32, _c.c_uint32, _c.c_float, _c.c_double, _c.c_void_p, _c.c_size_t

@@ -178,7 +178,7 @@ struct ProfScope {
   }
 };
 
-enum { PK_GEMM = 0, PK_ATTN = 1, PK_HEAD = 2, PK_COMMIT = 3, PK_NORM = 4, PK_GATEUP = 5 };
+enum { PK_QKV = 0, PK_ATTN = 1, PK_HEAD = 2, PK_COMMIT = 3, PK_NORM = 4, PK_GATEUP = 5, PK_OPROJ = 6, PK_DOWN = 7 };
 
 const void* W(const dllm_model* m, int i) { return m->w[i]; }
 const bf16_t* Wb(const dllm_model* m, int i) { return static_cast<const bf16_t*>(m->w[i]); }
@@ -333,7 +333,7 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     g.Hq = c.n_heads;
     g.Hkv = c.n_kv_heads;
     g.err = at<int>(ws, lay.err);
-    gemm_bf16(m, g, ws, lay, s, PK_GEMM);
+    gemm_bf16(m, g, ws, lay, s, PK_QKV);
     {
       ProfScope p(m, PK_ATTN, s);
       launch_attn_bf16(g.q, g.k, g.vt, at<bf16_t>(ws, lay.attn), B, Lq, L, c.n_heads, c.n_kv_heads, s);
@@ -342,7 +342,7 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     o.M = M;
     o.A = at<bf16_t>(ws, lay.attn);
     o.resid = h;
-    gemm_bf16(m, o, ws, lay, s, PK_GEMM, part == 2 ? &mid : nullptr);
+    gemm_bf16(m, o, ws, lay, s, PK_OPROJ, part == 2 ? &mid : nullptr);
   }
   if (part == 1 || part == 2) {
     norm_rows_bf16(m, h, part == 1 ? carry_in : &mid, W(m, base + 5), at<void>(ws, lay.a_mlp), B, Lq, s);
@@ -355,7 +355,7 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     dn.M = M;
     dn.A = at<bf16_t>(ws, lay.u);
     dn.resid = h;
-    gemm_bf16(m, dn, ws, lay, s, PK_GEMM, carry_out);
+    gemm_bf16(m, dn, ws, lay, s, PK_DOWN, carry_out);
   }
 }
 
@@ -377,7 +377,7 @@ void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void*
       launch_rmsnorm(h, W(m, base + 0), a, 0, B, Lq, Lq, 0, d, c.rms_eps, s);
     }
     {
-      ProfScope p(m, PK_GEMM, s);
+      ProfScope p(m, PK_QKV, s);
       launch_gemm_f32(a, Wf(m, base + 1), raw, M, nq, d, nraw, false, s);
       launch_gemm_f32(a, Wf(m, base + 2), raw + nq, M, nkv, d, nraw, false, s);
       launch_gemm_f32(a, Wf(m, base + 3), raw + nq + nkv, M, nkv, d, nraw, false, s);
@@ -389,7 +389,7 @@ void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void*
       launch_attn_f32(at<float>(ws, lay.q), kk, vv, at<float>(ws, lay.attn), B, Lq, L, c.n_heads, c.n_kv_heads, hd,
                       s);
     }
-    ProfScope p(m, PK_GEMM, s);
+    ProfScope p(m, PK_OPROJ, s);
     launch_gemm_f32(at<float>(ws, lay.attn), Wf(m, base + 4), h, M, d, nq, d, true, s);
   }
   if (part == 1 || part == 2) {
@@ -404,7 +404,7 @@ void run_layer_f32(const dllm_model* m, int layer, int part, int B, int L, void*
       launch_gemm_f32(a, Wf(m, base + 7), at<float>(ws, lay.up), M, F, d, F, false, s);
     }
     launch_swiglu_f32(at<float>(ws, lay.gate), at<float>(ws, lay.up), at<float>(ws, lay.u), (long)M * F, s);
-    ProfScope p(m, PK_GEMM, s);
+    ProfScope p(m, PK_DOWN, s);
     launch_gemm_f32(at<float>(ws, lay.u), Wf(m, base + 8), h, M, d, F, d, true, s);
   }
 }
@@ -1152,7 +1152,7 @@ int dllm_generate_kv(const dllm_model* m, const dllm_cai_params* p, int32_t refr
 int dllm_prof_enable(dllm_model* m, int32_t enable) {
   API_BEGIN
   check_model(m);
-  require(enable >= 0 && enable < 64, DLLM_EINVAL, "enable must be a bit mask of kinds 0..5");
+  require(enable >= 0 && enable < 256, DLLM_EINVAL, "enable must be a bit mask of kinds 0..7");
   m->prof_mask = (uint32_t)enable;
   m->n_events = 0;
   API_END

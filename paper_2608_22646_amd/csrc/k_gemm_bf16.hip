@@ -927,6 +927,320 @@ RowsPlan rows_plan(int M, int N, int K) {
   return best;
 }
 
+// ---- Register-direct weights, activations through LDS (a few hundred rows) --
+//
+// At a few hundred rows (the batch-1 forward) every tile of the LDS-staged
+// kernel above reads both operands out of LDS: a 64 x 96 wave tile moves 160
+// bytes of LDS per 64 x 96 x 2 flops per k, near gfx950's LDS/MFMA balance, and
+// a third of its issue slots go to the DMA bursts and the per-k-step barrier.
+// Here the weights come from their packed copy (each 32-row x 16-k MFMA operand
+// one lane-ordered 1 KiB run) straight into a P-slice register ring, so only
+// the activation tile is staged: per wave 32 TI bytes of LDS per k against 32
+// TI x 32 TJ x 2 flops.  W is the MFMA A operand, the activation rows the B
+// operand, so a lane ends with 16 virtual weight rows of one token row: the
+// SwiGLU pair (gate, up) and the rotate-half pair (d, d + 64) of an output sit
+// in registers r and r + 8 of one lane and the epilogues need no exchange.
+//
+// Workgroup: 4 waves (one per SIMD).  NWN of them sit side by side along N,
+// each owning TJ 32-row groups of Bv; KG = 4 / NWN k-groups split every 64-k
+// step (group g takes the 16-k slices g 4/KG .. of it), their accumulators
+// added through LDS after the loop.  The activation tile [BM, 64 KSTEPS] of a
+// stage streams by LDS-DMA into an AS-stage ring (128-byte rows, swizzled as
+// above), one barrier per stage.  Past the last stage the DMA and the weight
+// loads are issued again on the last valid addresses (their results are never
+// used), so every wait below counts a fixed number of later loads.
+template <int TI_, int TJ_, int NWN_, int KSTEPS_, int AS_, int P_>
+struct WdTile {
+  static constexpr int TI = TI_, TJ = TJ_, NWN = NWN_, KG = 4 / NWN_, KSTEPS = KSTEPS_, AS = AS_, P = P_;
+  static constexpr int NW = 4, NTH = 256;
+  static constexpr int BM = 32 * TI, BN = 32 * TJ * NWN;
+  static constexpr int SPS = 4 * KSTEPS;                // 16-k slices per stage
+  static constexpr int SPG = 4 / KG;                    // slices of a 64-k step one k-group takes
+  static constexpr int U = SPS / KG;                    // slices per stage one wave computes
+  static constexpr int STAGE = BM * 128 * KSTEPS;       // LDS bytes per stage
+  static constexpr int IA = BM * KSTEPS / 8 / NW;       // LDS-DMA instructions per wave per stage
+  static constexpr int IU = IA / U;                     // ... issued in each of its slices
+  static constexpr int R = P > U ? P / U : 1;           // stages unrolled per loop iteration
+  static_assert(NWN * KG == 4, "four waves");
+  static_assert(BM * KSTEPS % (8 * NW) == 0, "activation rows split evenly over the DMA loads");
+  static_assert(IU * U == IA && IU >= 1, "the stage's DMA spreads evenly over the wave's slices");
+  static_assert(P % U == 0 || U % P == 0, "register ring slots fixed at compile time");
+  static_assert(AS >= 3, "a stage is filled while the one before it is read");
+  static_assert(U % 2 == 0, "fragment register sets alternate within a stage");
+  // Issue order of a wave in stage s: per slice, IU DMA loads of stage
+  // s + AS - 1 (into the slot stage s - 1 left), then (last slice) the wait
+  // and barrier, the MFMAs, TJ weight loads for the slice P later.  At the
+  // last slice of stage t the wave waits for its DMA of stage t + 1; loads
+  // issued after the last of them: the steady count (stage t + 1 issued in
+  // stage t + 2 - AS) or the first stages' (stages 1 .. AS - 2 issued before
+  // the loop), clamped to vmcnt's range.  And before the loop, the loads after
+  // its DMA of stage 0.
+  static constexpr int PER = TJ + IU;  // loads per slice
+  static constexpr int C1 = TJ + (AS - 3) * U * PER + (U - 1) * PER + IU;
+  static constexpr int C0 = (AS - 3) * IA + P * TJ + (U - 1) * PER + IU;
+  static constexpr int CMIN = C0 < C1 ? C0 : C1;
+  static constexpr int CWAIT = CMIN < 63 ? CMIN : 63;
+  static constexpr int CFIRST = ((AS - 2) * IA + P * TJ) < 63 ? (AS - 2) * IA + P * TJ : 63;
+  static constexpr size_t LDS = (size_t)AS * STAGE;
+  static constexpr size_t MERGE = KG == 1 ? 0 : (size_t)NWN * TI * TJ * 16 * 64 * 4;
+  static constexpr size_t LDS_BYTES = LDS > MERGE ? LDS : MERGE;
+};
+// Batch-1 gate/up (M = 512, N = 24576): 4 x 64 = 256 workgroups of 128 x 384
+using WdWide = WdTile<4, 3, 4, 2, 4, 8>;
+// q/k/v-sized launches: 128 x 192 in two k-groups (M = 512, N = 12288: 256 workgroups)
+using WdKg2 = WdTile<4, 3, 2, 2, 4, 8>;
+
+template <class TL, int EPI>
+__global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  constexpr int TI = TL::TI, TJ = TL::TJ, U = TL::U, P = TL::P, AS = TL::AS, R = TL::R;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave % TL::NWN, kg = wave / TL::NWN;
+  const int MT = (g.M + TL::BM - 1) / TL::BM, T = MT * (g.N / TL::BN);
+  // XCD x runs workgroups i = x mod 8: it takes a contiguous run of the
+  // (N tile, M tile) order, so the M tiles of one weight tile share its L2
+  const int i = blockIdx.x, x = i & 7;
+  const int li = x * (T >> 3) + min(x, T & 7) + (i >> 3);
+  const int m0 = (li % MT) * TL::BM, n0 = (li / MT) * TL::BN;
+  const int nk = g.K / 64, nst = nk / TL::KSTEPS;
+
+  // activation DMA: instruction q of wave w fills rows 8 (4 q + w) .. +7 of the
+  // stage's row space [KSTEPS][BM] (sub-block = row / BM); lane l writes row +
+  // l/8, slot l%8, holding the row's chunk (l%8) ^ ((row >> 1) & 7)
+  const int lr = lane >> 3, lc = (lane & 7) ^ (((wave & 1) << 2) | (lr >> 1));
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, 0x7fffffff, 0x00020000);
+  uint32_t voa[TL::IA];
+#pragma unroll
+  for (int q = 0; q < TL::IA; ++q) {
+    const int r = 8 * (4 * q + wave) + lr, sb = r / TL::BM, row = min(m0 + r % TL::BM, g.M - 1);
+    voa[q] = (uint32_t)(((size_t)row * g.K + sb * 64 + lc * 8) * 2);
+  }
+  // DMA instruction q of stage t (past the end: the last stage again, never read)
+  auto issue_a = [&](int t, int q) {
+    t = min(t, nst - 1);
+    char* base = lds + (t % AS) * TL::STAGE;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + 8 * (4 * q + wave) * 128), 16, voa[q],
+                                             t * TL::KSTEPS * 128, 0, 0);
+  };
+  // weights: group G = n0 / 32 + wn TJ + j of the packed copy.  The wave's
+  // slice uu of stage t is 16-k slice t SPS + 4 (uu / SPG) + kg SPG + uu % SPG.
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)g.Wp, 0, 0x7fffffff, 0x00020000);
+  uint32_t wbase[TJ];
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) {
+    const int G = n0 / 32 + wn * TJ + j;
+    wbase[j] = (uint32_t)((((size_t)(G >> 3) * nk * 8 + (G & 7)) * 4) * 1024 + lane * 16 +
+                          (kg * TL::SPG) * 1024);
+  }
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  u32x4_t wbuf[P][TJ];
+  // operand j of the wave's slice uu (compile-time) of stage t, into ring slot
+  auto load_w = [&](int t, int uu, int slot, int j) {
+    t = min(t, nst - 1);  // past the end: the last stage again, never used
+    const uint32_t off = (uint32_t)(t * (TL::KSTEPS * 32768) + (uu / TL::SPG) * 32768 + (uu % TL::SPG) * 1024);
+    wbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rw, wbase[j] + off, 0, 2);  // non-temporal
+  };
+  // activation operands of slice uu of the stage in LDS at base
+  const int lrow = lane & 31, lhalf = lane >> 5;
+  bf16x8_t af[2][TI];
+  auto frag = [&](const char* base, int uu, int set) {
+    const int sb = uu / TL::SPG, sl = kg * TL::SPG + uu % TL::SPG;
+#pragma unroll
+    for (int ii = 0; ii < TI; ++ii)
+      af[set][ii] = *reinterpret_cast<const bf16x8_t*>(base + sb * TL::BM * 128 + swz(32 * ii + lrow, 2 * sl + lhalf));
+  };
+
+  f32x16_t acc[TJ][TI];
+#pragma unroll
+  for (int j = 0; j < TJ; ++j)
+#pragma unroll
+    for (int ii = 0; ii < TI; ++ii)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[j][ii][r] = 0.f;
+
+#pragma unroll
+  for (int t = 0; t < AS - 1; ++t)
+#pragma unroll
+    for (int q = 0; q < TL::IA; ++q) issue_a(t, q);
+#pragma unroll
+  for (int v = 0; v < P; ++v)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) load_w(v / U, v % U, v, j);
+  wait_vm_lds<TL::CFIRST>();
+  barrier_nofence();
+  frag(lds, 0, 0);
+
+  for (int t0 = 0; t0 < nst; t0 += R) {
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr) {
+      const int t = t0 + rr;
+      const char* base = lds + (t % AS) * TL::STAGE;
+#pragma unroll
+      for (int uu = 0; uu < U; ++uu) {
+        const int slot = (rr * U + uu) % P;
+        // the slice that reuses this ring slot: P slices later
+        const int tn = t + (uu + P) / U, un = (uu + P) % U;
+        __builtin_amdgcn_sched_barrier(0);
+        // a share of stage t + AS - 1 into the slot stage t - 1 left (every
+        // wave passed the barrier that ended it)
+#pragma unroll
+        for (int q = 0; q < TL::IU; ++q) issue_a(t + AS - 1, uu * TL::IU + q);
+        if (uu + 1 < U) {
+          frag(base, uu + 1, (uu + 1) & 1);
+        } else {
+          // this wave's DMA of stage t + 1 has landed once at most CWAIT later
+          // loads are outstanding; after the barrier every wave's has, and
+          // every wave is done reading stage t
+          wait_vm_lds<TL::CWAIT>();
+          barrier_nofence();
+          frag(lds + ((t + 1) % AS) * TL::STAGE, 0, 0);
+        }
+        // MFMAs operand-major; each weight operand's slot is refilled right
+        // after its last use
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+#pragma unroll
+          for (int ii = 0; ii < TI; ++ii)
+            acc[j][ii] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wbuf[slot][j]),
+                                                                af[uu & 1][ii], acc[j][ii], 0, 0, 0);
+          load_w(tn, un, slot, j);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x020, TL::IU, 0);  // the DMA share
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+          if (j == 0) {
+#pragma unroll
+            for (int ii = 0; ii < TI; ++ii) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // an MFMA
+              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // a fragment read of the next slice
+            }
+          } else {
+            __builtin_amdgcn_sched_group_barrier(0x008, TI, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // the refill of operand j
+        }
+      }
+    }
+  }
+  wait_vm_lds<0>();
+  barrier_nofence();  // the ring is idle
+
+  if (TL::KG == 2) {
+    // acc(group 0) += acc(group 1) through LDS, lane-contiguous float4s
+    float4* xa = reinterpret_cast<float4*>(lds) + (size_t)wn * (TI * TJ * 4 * 64) + lane;
+    if (kg == 1) {
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+#pragma unroll
+        for (int ii = 0; ii < TI; ++ii)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            xa[((j * TI + ii) * 4 + q) * 64] =
+                make_float4(acc[j][ii][4 * q], acc[j][ii][4 * q + 1], acc[j][ii][4 * q + 2], acc[j][ii][4 * q + 3]);
+    }
+    wait_vm_lds<0>();
+    barrier_nofence();
+    if (kg == 1) return;
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int ii = 0; ii < TI; ++ii)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = xa[((j * TI + ii) * 4 + q) * 64];
+          acc[j][ii][4 * q] += v.x;
+          acc[j][ii][4 * q + 1] += v.y;
+          acc[j][ii][4 * q + 2] += v.z;
+          acc[j][ii][4 * q + 3] += v.w;
+        }
+  }
+
+  // Epilogue.  Lane l holds, for token row m = m0 + 32 ii + l % 32 and group G,
+  // virtual rows 32 G + 8 (r / 4) + 4 (l / 32) + r % 4 in register r.
+  constexpr int HD = 128, HALF = 64;
+  const int nq = g.Hq * HD, nkv = g.Hkv * HD;
+  const float inv_l = 1.0f / (float)g.Lq;
+  bool v_over = false;
+#pragma unroll
+  for (int ii = 0; ii < TI; ++ii) {
+    const int m = m0 + 32 * ii + lrow;
+    if (m >= g.M) continue;
+    int b = 0, p = 0;
+    if (EPI == EPI_QKV_ROPE) {
+      const int2 bp = seq_pos(m, g.Lq, inv_l);
+      b = bp.x;
+      p = bp.y;
+    }
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int G = n0 / 32 + wn * TJ + j;
+      const f32x16_t& a = acc[j][ii];
+      if (EPI == EPI_SWIGLU) {
+        // registers 0..7: gate of f = 16 G + 8 (r / 4) + 4 (l / 32) + r % 4, r + 8: up of the same f
+        const int F = g.N / 2;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float gt = a[4 * q + e], up = a[4 * q + 8 + e];
+            o[e] = __fdividef(gt, 1.0f + __expf(-gt)) * up;
+          }
+          *reinterpret_cast<uint2*>(g.out + (size_t)m * F + 16 * G + 8 * q + 4 * lhalf) =
+              make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+        }
+      } else if (EPI == EPI_QKV_ROPE) {
+        const int vb = 32 * G;
+        if (vb < nq + nkv) {
+          // registers 0..7: dimension d = 16 blk + 8 (r / 4) + 4 (l / 32) + r % 4
+          // of the head, r + 8: d + 64
+          const bool isq = vb < nq;
+          const int rel = isq ? vb : vb - nq, head = rel / HD, blk = (rel % HD) >> 5;
+          const int pos = g.pos0 + p;
+          bf16_t* dst = isq ? g.q + (((size_t)b * g.Hq + head) * g.Lq + p) * HD
+                            : g.k + (((size_t)b * g.Hkv + head) * g.L + pos) * HD;
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const int d = 16 * blk + 8 * q + 4 * lhalf;
+            const float4 c4 = *reinterpret_cast<const float4*>(g.cosb + (size_t)pos * HALF + d);
+            const float4 s4 = *reinterpret_cast<const float4*>(g.sinb + (size_t)pos * HALF + d);
+            const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, ss[4] = {s4.x, s4.y, s4.z, s4.w};
+            float lo[4], hi[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float x1 = a[4 * q + e], x2 = a[4 * q + 8 + e];
+              lo[e] = x1 * cc[e] - x2 * ss[e];
+              hi[e] = x2 * cc[e] + x1 * ss[e];
+            }
+            *reinterpret_cast<uint2*>(dst + d) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+            *reinterpret_cast<uint2*>(dst + d + HALF) =
+                make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
+          }
+        } else {
+          const int rel = vb - nq - nkv, head = rel / HD, cj0 = rel % HD;
+          f16_t* dst = g.vt + (((size_t)b * g.Hkv + head) * HD + cj0) * g.L + g.pos0 + p;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[(size_t)(8 * (r >> 2) + 4 * lhalf + (r & 3)) * g.L] = v_half(a[r], v_over);
+        }
+      } else {  // EPI_RESID: h[m, n] += result, n = 32 G + 8 q + 4 (l / 32) + e
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float4* hp = reinterpret_cast<float4*>(g.resid + (size_t)m * g.N + 32 * G + 8 * q + 4 * lhalf);
+          float4 h = *hp;
+          h.x += a[4 * q];
+          h.y += a[4 * q + 1];
+          h.z += a[4 * q + 2];
+          h.w += a[4 * q + 3];
+          *hp = h;
+        }
+      }
+    }
+  }
+  if (EPI == EPI_QKV_ROPE && v_over && g.err) atomicOr(g.err, (int)ERR_V_RANGE);
+#endif
+}
+
 struct Plan {
   int bm, bn, kg, split;
 };
@@ -1099,6 +1413,44 @@ void launch_gemm_rows(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   DLLM_LAUNCH_CHECK("gemm_rows epilogue");
 }
 
+template <class TL, int EPI>
+void launch_wd_tile(const GemmArgs& g, hipStream_t s) {
+  const int T = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
+  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_wd_kernel<TL, EPI>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)TL::LDS_BYTES);
+  hip_check(attr, "hipFuncSetAttribute(gemm_wd)");
+  hipLaunchKernelGGL((gemm_wd_kernel<TL, EPI>), dim3(T), dim3(TL::NTH), TL::LDS_BYTES, s, g);
+}
+
+// Register-direct-weight tile for a launch (0: none, 1: WdWide, 2: WdKg2):
+// SwiGLU and q/k/v GEMMs of 129 .. 1024 rows with the packed copy, when the
+// tile's workgroups fill at least 7/8 of the rounds they take on the compute
+// units (batch-1 LLaDA-8B shape at 512 rows: gate/up on WdWide 99 -> 88 us,
+// q/k/v on WdKg2 65 -> 60 us); of two such tiles the one with less work per
+// compute unit (rounds x tile area), the wider one on ties (gate/up on WdKg2
+// is 512 workgroups in two rounds: 108 us).  Elsewhere the LDS-staged tiles
+// stay.
+int wd_choice(const GemmArgs& a) {
+  if (!a.Wp || a.M <= 128 || a.M > 1024 || (a.epi != EPI_SWIGLU && a.epi != EPI_QKV_ROPE)) return 0;
+  const int nk = a.K / 64;
+  const long cus = device_cu_count();
+  int best = 0;
+  double best_t = 1e30;
+  auto consider = [&](int id, int BM, int BN, int KSTEPS, int R) {
+    if (a.N % BN != 0 || nk % KSTEPS != 0 || (nk / KSTEPS) % R != 0) return;
+    const long T = (long)((a.M + BM - 1) / BM) * (a.N / BN), rounds = (T + cus - 1) / cus;
+    if (8 * T < 7 * rounds * cus) return;
+    const double t = (double)rounds * BM * BN;  // per compute unit: rounds x tile area (4 waves either way)
+    if (t < best_t - 1e-9) {
+      best_t = t;
+      best = id;
+    }
+  };
+  consider(1, WdWide::BM, WdWide::BN, WdWide::KSTEPS, WdWide::R);
+  consider(2, WdKg2::BM, WdKg2::BN, WdKg2::KSTEPS, WdKg2::R);
+  return best;
+}
+
 void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   if (defer) *defer = PendingResid{};
   if (a.M == 0) return;
@@ -1111,6 +1463,21 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
     throw HipError("gemm_bf16: q/k/v rows must be whole windows of Lq positions inside the sequence");
   if (a.Wp && rows_path(a.M, a.N, a.K)) {  // few rows from the packed copy: register-direct
     launch_gemm_rows(a, s, defer);
+    return;
+  }
+  if (const int wd = wd_choice(a)) {  // a few hundred rows: register-direct weights, staged activations
+    auto go = [&](auto tl) {
+      using TL = decltype(tl);
+      if (a.epi == EPI_SWIGLU)
+        launch_wd_tile<TL, EPI_SWIGLU>(a, s);
+      else
+        launch_wd_tile<TL, EPI_QKV_ROPE>(a, s);
+    };
+    if (wd == 1)
+      go(WdWide{});
+    else
+      go(WdKg2{});
+    DLLM_LAUNCH_CHECK("gemm_wd");
     return;
   }
   const Plan p = plan(a.M, a.N, a.K, a.epi);

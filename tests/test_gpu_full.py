@@ -67,11 +67,15 @@ def check_invariants(st, forwards, P, G, bl, T, mask_id, ctl):
             assert cs[b, blk * bl:(blk + 1) * bl].max() + 1 <= forwards[blk]
 
 
-@pytest.mark.parametrize("name", WORKLOADS)
-def test_full_size_stages_and_head(models, name):
+@pytest.mark.parametrize("name,packed", [(n, False) for n in WORKLOADS] + [("llada_b1", True)])
+def test_full_size_stages_and_head(models, name, packed):
+    """packed: a second handle on the same weights with the packed copies, so
+    the batch-1 q/k/v and gate/up GEMMs stream their weights register-direct."""
     wl = synth.WORKLOADS[name]
     cfg = wl.model
     w, model = models(cfg)
+    if packed:
+        model = B.Model(cfg, w).pack_weights()
     Bn, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
     L = P + G
     sample_layers = [0, cfg.n_layers - 1]
@@ -85,7 +89,7 @@ def test_full_size_stages_and_head(models, name):
     keys = np.sort(rng.choice(L, 64, replace=False))
     for l in range(cfg.n_layers):
         if l in sample_layers:
-            say(f"{name}: stages of layer {l}")
+            say(f"{name}{' (packed)' if packed else ''}: stages of layer {l}")
             st = check_layer(model, cfg, wnp, ws, Bn, L, l, rows=rows, key_rows=keys)
             say("  " + ", ".join(f"{k}={v:.2e}" for k, v in st.items()))
         else:
@@ -94,6 +98,9 @@ def test_full_size_stages_and_head(models, name):
     head_rows = np.sort(rng.choice(Bn * bl, min(16, Bn * bl), replace=False))
     hs = check_head(model, cfg, wnp, ws, Bn, L, P, bl, sample=head_rows)
     say(f"  head {hs}")
+    if packed:
+        model.close()
+        torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("G", [64, 512])

@@ -1,0 +1,65 @@
+"""The register-direct-weight GEMM (gemm_wd_kernel): q/k/v + RoPE and
+gate/up + SwiGLU launches of 129..1024 rows on a model with packed weight
+copies, when its tiles fill the compute units.
+
+One layer at the LLaDA-8B widths (d 4096, 32 heads MHA, FFN 12288): q/k/v is
+N = 12288 (128 x 192 tiles in two k-groups: 64 column tiles), gate/up N =
+24576 (128 x 384 tiles: 64 column tiles); with 4 row tiles either launch is
+256 workgroups, so rows 385..512 take it:
+  * M = 400, one sequence: the last row tile holds 16 rows (rows past M are
+    loaded clamped and never stored);
+  * M = 400, two sequences of 200: row tiles straddle the sequence boundary
+    (the epilogue's row -> (sequence, position) mapping for q/k/v^T);
+  * M = 512: the batch-1 decode shape.
+Every stage is checked against the oracle on the GPU's own stage inputs (the
+bars of gpu_stages), and the fused forward against per-layer calls (bitwise).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_stages import check_head, check_layer
+from helpers import say
+from paper_2608_22646_amd import binding as B
+from paper_2608_22646_amd import synth
+from test_gpu_bf16 import forward_equals_layer_calls
+
+pytestmark = pytest.mark.gpu
+
+WIDE_MHA = synth.ModelConfig("wide-mha-bf16", n_layers=1, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128,
+                             d_ff=12288, vocab=4000, rope_base=500000.0, dtype="bf16",
+                             lm_head_std=5 / math.sqrt(4096), norm_gain_std=0.1)
+
+
+@pytest.fixture(scope="module")
+def wide_mha():
+    w_cpu = synth.make_weights(WIDE_MHA, "cpu")
+    model = B.Model(WIDE_MHA, [w.to("cuda") for w in w_cpu]).pack_weights()
+    yield model, [w.to(torch.float32).numpy() for w in w_cpu]
+    model.close()
+
+
+@pytest.mark.parametrize("Bn,P,G", [(1, 336, 64), (2, 136, 64), (1, 448, 64)])
+def test_wd_stages(wide_mha, Bn, P, G):
+    model, wnp = wide_mha
+    L = P + G
+    say(f"register-direct GEMM stages B={Bn} L={L} (M={Bn * L})")
+    x = synth.make_ints((Bn, L), 31, 0, WIDE_MHA.vocab - 1).cuda()
+    ws = model.workspace(Bn, L, 32)
+    model.embed(x, ws)
+    rng = np.random.default_rng(3)
+    # sampled rows: every 128-row tile, both sequences, the last rows
+    rows = np.unique(np.concatenate([rng.choice(Bn * L, 60, replace=False), [0, 127, 128, 199, 200, Bn * L - 1]]))
+    st = check_layer(model, WIDE_MHA, wnp, ws, Bn, L, 0, rows=rows)
+    say("  " + ", ".join(f"{k}={v:.2e}" for k, v in st.items()))
+    hs = check_head(model, WIDE_MHA, wnp, ws, Bn, L, P, 32)
+    say(f"  head: {hs}")
+
+
+@pytest.mark.parametrize("Bn,P,G", [(2, 136, 64), (1, 448, 64)])
+def test_wd_forward_matches_layer_by_layer(wide_mha, Bn, P, G):
+    model, _ = wide_mha
+    say(f"register-direct GEMM: fused forward vs layer calls B={Bn} L={P + G}")
+    forward_equals_layer_calls(model, WIDE_MHA, Bn, P, G, seed=33)
