@@ -425,7 +425,11 @@ def main():
         log(f"warmup {i}: forwards {res.total_forwards} {res.forwards}")
     torch.cuda.synchronize()
 
-    model.prof_enable([Bd.PROF_GATEUP])          # clears the warm-up records
+    # clears the warm-up records; one gate/up launch per forward (layer 0's) is
+    # bracketed by events, so the measurement costs the timed decodes ~2 x 3 us
+    # per forward rather than 2 x 3 us per layer
+    model.prof_every(cfg.n_layers)
+    model.prof_enable([Bd.PROF_GATEUP])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     total_fwd = 0
@@ -439,6 +443,7 @@ def main():
     log(f"forwards per decode of the {args.steps} prompt sets: {fwd_each}")
     gu_ms, gu_n = model.prof_read(Bd.PROF_GATEUP)
     model.prof_enable([])
+    model.prof_every(1)
 
     flops = forward_flops(cfg, B, L)
     gu_avg_s = gu_ms / gu_n / 1e3

@@ -17,8 +17,9 @@
  *    sized by a query: the model buffer (dllm_model_buffer_size), the packed
  *    weights (dllm_model_packed_size), the workspace (dllm_workspace_size) and
  *    the key/value cache (dllm_kv_cache_size), each 256-byte aligned.  The
- *    only other resources are host objects of a model handle (one pinned host
- *    word for the per-step flag read-back, timing events).
+ *    only other resources are host objects of a model handle (one coherent
+ *    pinned host word the commit kernel publishes each step's done flag to,
+ *    timing events).
  *  - `stream` is a hipStream_t passed as void*; NULL is the null stream.  All
  *    device work is enqueued on it in order; entry points return once the work
  *    is enqueued unless stated otherwise.
@@ -303,8 +304,9 @@ int dllm_commit(const dllm_cai_params* params, dllm_state* state, const float* c
 /*
  * One denoising step: dllm_forward on state->x for block `block`'s rows, then
  * dllm_commit.  conf_out / argmax_out: optional device [B, bl] copies of the
- * step's predictions (NULL on the hot path).  all_done_host: optional pinned
- * host int32; when given the call waits for the step and stores 1 there when
+ * step's predictions (NULL on the hot path).  all_done_host: optional host
+ * int32; when given the call waits for the step (polling the word the commit
+ * kernel publishes to the model's pinned flag) and stores 1 there when
  * every sequence has finished the block, and reports the workspace's error
  * word (then cleared): DLLM_EINVAL if a token id of x was outside [0, vocab)
  * (its embedding was taken as zero), DLLM_EUNSUPPORTED if a value of v was
@@ -401,6 +403,12 @@ int dllm_generate_kv(const dllm_model* model, const dllm_cai_params* params, int
  * objects kept by the model handle (no device memory). */
 int dllm_prof_enable(dllm_model* model, int32_t enable);
 int dllm_prof_read(dllm_model* model, int32_t kind, double* total_ms, int64_t* launches);
+/* Record only one launch in `every` (>= 1; default 1) of each enabled kind,
+ * the first of each run of `every`: each record brackets its launch with two
+ * events on the stream, which cost the stream a few microseconds each, so a
+ * timed decode samples (e.g. one of a forward's n_layers launches of a
+ * kind).  Resets the per-kind launch counts; DLLM_EINVAL if every < 1. */
+int dllm_prof_every(dllm_model* model, int32_t every);
 
 /* Message of the last failure on the calling thread ("" if none). */
 const char* dllm_last_error(void);

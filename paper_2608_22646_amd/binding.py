@@ -90,6 +90,7 @@ _SIGS = {
                                 _vp, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
     "dllm_prof_enable": (_i32, [_vp, _i32]),
     "dllm_prof_read": (_i32, [_vp, _i32, _c.POINTER(_f64), _c.POINTER(_c.c_int64)]),
+    "dllm_prof_every": (_i32, [_vp, _i32]),
 }
 
 
@@ -441,6 +442,10 @@ class Model:
         for k in kinds:
             mask |= 1 << k
         check(lib().dllm_prof_enable(self.h, mask))
+
+    def prof_every(self, every):
+        """dllm_prof_every: record one launch in `every` of each enabled kind."""
+        check(lib().dllm_prof_every(self.h, every))
 
     def prof_read(self, kind):
         ms = ctypes.c_double()

@@ -7,17 +7,20 @@
 //   gate/up+swiglu, down+residual] -> final norm of the block rows -> fused LM
 //   head + vocabulary reduction -> commit.
 // dllm_generate runs the semi-autoregressive block loop (Section 4.3) and
-// reads the 4-byte block-finished flag back once per step.
+// waits once per step for the block-finished flag, which the commit kernel
+// publishes to a coherent pinned host word the host polls.
 #include <math.h>
 #include <string.h>
 
 #include <algorithm>
+#include <chrono>
 #include <mutex>
 
 #include <string>
 #include <vector>
 
 #include "../../include/dllm.h"
+
 #include "kernels.h"
 
 using namespace dllm;
@@ -53,8 +56,14 @@ struct dllm_model {
   // output, gate/up and down weights (in the caller's buffer; offsets per layer)
   bf16_t* packed = nullptr;
   std::vector<size_t> packed_off;  // [layer * 4 + {0: qkv, 1: o, 2: gate/up, 3: down}] in elements
-  int32_t* pinned_flag = nullptr;
+  // coherent pinned word the commit kernel publishes each step's done/error
+  // word to (tagged with the step's sequence number), and its device address
+  int32_t* step_flag = nullptr;
+  int32_t* step_flag_dev = nullptr;
+  int step_seq = 0;
   uint32_t prof_mask = 0;  // bit k: record launches of kind k
+  int prof_every = 1;      // record one launch in prof_every of each kind
+  int64_t prof_seen[8] = {};
   std::vector<ProfEvent> events;
   size_t n_events = 0;
 };
@@ -163,6 +172,7 @@ struct ProfScope {
   ProfEvent* ev = nullptr;
   ProfScope(const dllm_model* mc, int kind, hipStream_t st) : m(const_cast<dllm_model*>(mc)), s(st) {
     if (!(m->prof_mask & (1u << kind))) return;
+    if (m->prof_seen[kind]++ % m->prof_every != 0) return;
     if (m->n_events == m->events.size()) {
       ProfEvent e{};
       hip_check(hipEventCreate(&e.start), "hipEventCreate");
@@ -783,7 +793,10 @@ int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int
   m->cfg = c;
   m->w.assign(weights, weights + n_weights);
   try {
-    hip_check(hipHostMalloc((void**)&m->pinned_flag, sizeof(int32_t), hipHostMallocDefault), "hipHostMalloc");
+    hip_check(hipHostMalloc((void**)&m->step_flag, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent),
+              "hipHostMalloc");
+    *m->step_flag = 0;
+    hip_check(hipHostGetDevicePointer((void**)&m->step_flag_dev, m->step_flag, 0), "hipHostGetDevicePointer");
     if (c.dtype == DLLM_BF16) {
       // stream-ordered after the caller's writes of lm_head on that stream
       m->head_tiled = static_cast<bf16_t*>(model_buf);
@@ -791,7 +804,7 @@ int dllm_model_create(const dllm_model_cfg* cfg, const void* const* weights, int
                             (hipStream_t)stream);
     }
   } catch (...) {
-    if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
+    if (m->step_flag) (void)hipHostFree(m->step_flag);
     delete m;
     throw;
   }
@@ -806,7 +819,7 @@ int dllm_model_destroy(dllm_model* m) {
     (void)hipEventDestroy(e.start);
     (void)hipEventDestroy(e.stop);
   }
-  if (m->pinned_flag) (void)hipHostFree(m->pinned_flag);
+  if (m->step_flag) (void)hipHostFree(m->step_flag);
   delete m;
   API_END
 }
@@ -1019,9 +1032,11 @@ int dllm_commit(const dllm_cai_params* p, dllm_state* st, const float* conf, con
 namespace {
 // One denoising step.  kv null: the full forward; else a refresh step (the
 // full forward storing the cache) when refresh is set, a cached step otherwise.
+// One denoising step; with seq > 0 the commit also publishes its done/error
+// word to the model's pinned step flag under that sequence number (wait_step).
 void step_impl(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int B, int P, int G, int block, int t,
                float* conf_out, int32_t* argmax_out, void* ws, const Layout& lay, hipStream_t s, void* kv = nullptr,
-               bool refresh = true, bool rope = true) {
+               bool refresh = true, bool rope = true, int seq = 0) {
   CommitArgs a{};
   fill_commit_args(p, st, &a, B, P, G, block, t, m->cfg.mask_id);
   const int bl = p->block_len;
@@ -1035,8 +1050,40 @@ void step_impl(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, in
   a.argmax = arg;
   a.all_done = at<int32_t>(ws, lay.all_done);
   a.err = at<int>(ws, lay.err);
+  if (seq > 0) {
+    a.host_flag = m->step_flag_dev;
+    a.seq = seq;
+  }
   ProfScope pr(m, PK_COMMIT, s);
   launch_commit(a, s);
+}
+
+// Sequence number for the next published step (1 .. 2^23 - 1, wrapping).
+int next_seq(const dllm_model* m) {
+  auto* mm = const_cast<dllm_model*>(m);
+  mm->step_seq = mm->step_seq % 0x7fffff + 1;
+  return mm->step_seq;
+}
+
+// The done/error word of the step published under seq: the host polls the
+// pinned flag the commit kernel stores to (it sees the word microseconds after
+// the store; a stream synchronisation after a device-to-host copy costs the
+// GPU a few hundred microseconds of idle time per step).  A word that has not
+// arrived after 20 ms falls back to synchronising the stream, which returns
+// once the step has run or reports its error.
+int wait_step(const dllm_model* m, hipStream_t s, int seq) {
+  volatile int32_t* f = m->step_flag;
+  const auto t0 = std::chrono::steady_clock::now();
+  for (long i = 1;; ++i) {
+    const int v = *f;
+    if ((v >> 8) == seq) return v & 0xff;
+    if ((i & 1023) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
+    __builtin_ia32_pause();
+  }
+  hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
+  const int v = *f;
+  if ((v >> 8) != seq) fail(DLLM_EHIP, "the step's done flag was not published");
+  return v & 0xff;
 }
 }  // namespace
 
@@ -1049,13 +1096,12 @@ int dllm_step(const dllm_model* m, const dllm_cai_params* p, dllm_state* st, int
   Layout lay;
   check_ws(m, B, P + G, p->block_len, ws, ws_bytes, &lay);
   hipStream_t s = (hipStream_t)stream;
-  step_impl(m, p, st, B, P, G, block, t, conf_out, argmax_out, ws, lay, s);
+  const int seq = all_done_host ? next_seq(m) : 0;
+  step_impl(m, p, st, B, P, G, block, t, conf_out, argmax_out, ws, lay, s, nullptr, true, true, seq);
   if (all_done_host) {
-    hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
-              "hipMemcpyAsync");
-    hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
-    *all_done_host = *m->pinned_flag & 1;
-    raise_step_errors(*m->pinned_flag);
+    const int flag = wait_step(m, s, seq);
+    *all_done_host = flag & 1;
+    raise_step_errors(flag);
   }
   API_END
 }
@@ -1070,13 +1116,12 @@ int dllm_step_kv(const dllm_model* m, const dllm_cai_params* p, int32_t refresh,
   Layout lay;
   check_ws(m, B, P + G, p->block_len, ws, ws_bytes, &lay);
   hipStream_t s = (hipStream_t)stream;
-  step_impl(m, p, st, B, P, G, block, t, conf_out, argmax_out, ws, lay, s, kv, refresh != 0);
+  const int seq = all_done_host ? next_seq(m) : 0;
+  step_impl(m, p, st, B, P, G, block, t, conf_out, argmax_out, ws, lay, s, kv, refresh != 0, true, seq);
   if (all_done_host) {
-    hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
-              "hipMemcpyAsync");
-    hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
-    *all_done_host = *m->pinned_flag & 1;
-    raise_step_errors(*m->pinned_flag);
+    const int flag = wait_step(m, s, seq);
+    *all_done_host = flag & 1;
+    raise_step_errors(flag);
   }
   API_END
 }
@@ -1100,18 +1145,18 @@ void generate_impl(const dllm_model* m, const dllm_cai_params* p, const int32_t*
     for (int t = 0; t < T; ++t) {
       float* ct = conf_trace ? conf_trace + ((size_t)blk * T + t) * B * bl : nullptr;
       int32_t* at_ = argmax_trace ? argmax_trace + ((size_t)blk * T + t) * B * bl : nullptr;
+      const int seq = next_seq(m);
       step_impl(m, p, st, B, P, G, blk, t, ct, at_, ws, lay, s, kv, refresh_every == 0 || t % refresh_every == 0,
-                false);
+                false, seq);
       ++n;
-      hip_check(hipMemcpyAsync(m->pinned_flag, at<int32_t>(ws, lay.all_done), 4, hipMemcpyDeviceToHost, s),
-                "hipMemcpyAsync");
-      hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
-      raise_step_errors(*m->pinned_flag);
-      if (*m->pinned_flag & 1) break;
+      const int flag = wait_step(m, s, seq);
+      raise_step_errors(flag);
+      if (flag & 1) break;
     }
     if (forwards_host) forwards_host[blk] = n;
     total += n;
   }
+  hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");  // the last commit has returned
   if (total_forwards) *total_forwards = total;
 }
 }  // namespace
@@ -1155,6 +1200,16 @@ int dllm_prof_enable(dllm_model* m, int32_t enable) {
   require(enable >= 0 && enable < 256, DLLM_EINVAL, "enable must be a bit mask of kinds 0..7");
   m->prof_mask = (uint32_t)enable;
   m->n_events = 0;
+  for (auto& c : m->prof_seen) c = 0;
+  API_END
+}
+
+int dllm_prof_every(dllm_model* m, int32_t every) {
+  API_BEGIN
+  check_model(m);
+  require(every >= 1, DLLM_EINVAL, "every must be >= 1");
+  m->prof_every = every;
+  for (auto& c : m->prof_seen) c = 0;
   API_END
 }
 

@@ -14,7 +14,8 @@
 //
 // The word *all_done receives 1 when every sequence has finished the block,
 // plus the bits of the step's error word (shifted up by one), which is then
-// cleared.
+// cleared; the same word tagged with the step's sequence number goes to the
+// host's pinned flag when one is given.
 #include "kernels.h"
 
 namespace dllm {
@@ -124,7 +125,12 @@ __global__ void __launch_bounds__(1024) commit_kernel(CommitArgs a) {
       e = *a.err;
       *a.err = 0;
     }
-    if (a.all_done) *a.all_done = all | (e << 1);
+    const int word = all | (e << 1);
+    if (a.all_done) *a.all_done = word;
+    // a vector store to host memory at system scope; relaxed: the word is all
+    // the host reads before its next launch (device data it may read later
+    // goes through stream-ordered copies)
+    if (a.host_flag) __hip_atomic_store(a.host_flag, (a.seq << 8) | word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
 }
 

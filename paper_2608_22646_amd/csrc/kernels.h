@@ -155,6 +155,11 @@ struct CommitArgs {
   // error word of the step's workspace (optional): its bits are reported in
   // *all_done above bit 0 and the word is cleared
   int* err;
+  // optional word in coherent pinned host memory: receives seq << 8 | the
+  // *all_done value with a system-scope release, so the host can wait for the
+  // step by polling it instead of a stream synchronisation
+  int* host_flag;
+  int seq;
 };
 void launch_commit(const CommitArgs& a, hipStream_t s);
 
