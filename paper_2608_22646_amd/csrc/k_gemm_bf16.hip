@@ -989,6 +989,9 @@ struct WdTile {
 using WdWide = WdTile<4, 3, 4, 2, 4, 8>;
 // q/k/v-sized launches: 128 x 192 in two k-groups (M = 512, N = 12288: 256 workgroups)
 using WdKg2 = WdTile<4, 3, 2, 2, 4, 8>;
+// residual projections (N = d_model): 128 x 256, split over K (M = 512, N =
+// 4096: 64 tiles x 4 splits)
+using WdRes = WdTile<4, 2, 4, 2, 4, 8>;
 
 template <class TL, int EPI>
 __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
@@ -997,13 +1000,16 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
   constexpr int TI = TL::TI, TJ = TL::TJ, U = TL::U, P = TL::P, AS = TL::AS, R = TL::R;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave % TL::NWN, kg = wave / TL::NWN;
-  const int MT = (g.M + TL::BM - 1) / TL::BM, T = MT * (g.N / TL::BN);
+  const int MT = (g.M + TL::BM - 1) / TL::BM, T = MT * (g.N / TL::BN), S = (int)gridDim.x / T;
   // XCD x runs workgroups i = x mod 8: it takes a contiguous run of the
-  // (N tile, M tile) order, so the M tiles of one weight tile share its L2
-  const int i = blockIdx.x, x = i & 7;
-  const int li = x * (T >> 3) + min(x, T & 7) + (i >> 3);
-  const int m0 = (li % MT) * TL::BM, n0 = (li / MT) * TL::BN;
-  const int nk = g.K / 64, nst = nk / TL::KSTEPS;
+  // (K split, N tile, M tile) order, so the M tiles of one weight tile share
+  // its L2 and, split, an XCD streams one k-range of the weights
+  const int i = blockIdx.x, x = i & 7, TS = (int)gridDim.x;
+  const int li = x * (TS >> 3) + min(x, TS & 7) + (i >> 3);
+  const int tile = li % T, z = li / T;
+  const int m0 = (tile % MT) * TL::BM, n0 = (tile / MT) * TL::BN;
+  // split z takes the stages [z nst, (z + 1) nst) of K
+  const int nk = g.K / 64, nst = nk / TL::KSTEPS / S, st0 = z * nst;
 
   // activation DMA: instruction q of wave w fills rows 8 (4 q + w) .. +7 of the
   // stage's row space [KSTEPS][BM] (sub-block = row / BM); lane l writes row +
@@ -1021,7 +1027,7 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
     t = min(t, nst - 1);
     char* base = lds + (t % AS) * TL::STAGE;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(base + 8 * (4 * q + wave) * 128), 16, voa[q],
-                                             t * TL::KSTEPS * 128, 0, 0);
+                                             (st0 + t) * TL::KSTEPS * 128, 0, 0);
   };
   // weights: group G = n0 / 32 + wn TJ + j of the packed copy.  The wave's
   // slice uu of stage t is 16-k slice t SPS + 4 (uu / SPG) + kg SPG + uu % SPG.
@@ -1038,7 +1044,8 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
   // operand j of the wave's slice uu (compile-time) of stage t, into ring slot
   auto load_w = [&](int t, int uu, int slot, int j) {
     t = min(t, nst - 1);  // past the end: the last stage again, never used
-    const uint32_t off = (uint32_t)(t * (TL::KSTEPS * 32768) + (uu / TL::SPG) * 32768 + (uu % TL::SPG) * 1024);
+    const uint32_t off =
+        (uint32_t)((st0 + t) * (TL::KSTEPS * 32768) + (uu / TL::SPG) * 32768 + (uu % TL::SPG) * 1024);
     wbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rw, wbase[j] + off, 0, 2);  // non-temporal
   };
   // activation operands of slice uu of the stage in LDS at base
@@ -1223,6 +1230,11 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) dst[(size_t)(8 * (r >> 2) + 4 * lhalf + (r & 3)) * g.L] = v_half(a[r], v_over);
         }
+      } else if (S > 1) {  // EPI_RESID split over K: partial z [M, N] float32, summed in z order later
+        float* part = g.splitk_buf + (size_t)z * g.M * g.N + (size_t)m * g.N + 32 * G + 4 * lhalf;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<float4*>(part + 8 * q) = make_float4(a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]);
       } else {  // EPI_RESID: h[m, n] += result, n = 32 G + 8 q + 4 (l / 32) + e
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -1239,6 +1251,53 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
   }
   if (EPI == EPI_QKV_ROPE && v_over && g.err) atomicOr(g.err, (int)ERR_V_RANGE);
 #endif
+}
+
+// Register-direct-weight plan for a launch of 129 .. 1024 rows with the packed
+// copy (tile 0: none, 1: WdWide, 2: WdKg2, 3: WdRes; split over K), taken when
+// the tile's workgroups fill at least 7/8 of the rounds they take on the
+// compute units.  SwiGLU and q/k/v (no split): of WdWide and WdKg2 the one
+// with less work per compute unit (rounds x tile area), the wider one on ties
+// -- batch-1 LLaDA-8B shape at 512 rows: gate/up on WdWide 99 -> 86 us (on
+// WdKg2, 512 workgroups in two rounds: 108 us), q/k/v on WdKg2 65 -> 60 us.
+// Residual GEMMs on WdRes, the split by a time model: rounds x the tile's
+// multiply-adds at the gate/up kernel's measured rate, plus the float32
+// partials written here and read back by the next norm (~8 TB/s); the
+// split's k-range must be whole stages of at least 2048 k.  Elsewhere the
+// LDS-staged tiles stay.
+struct WdPlan {
+  int tile, split;
+};
+WdPlan wd_plan(int M, int N, int K, int epi) {
+  WdPlan best{0, 1};
+  if (M <= 128 || M > 1024 || K % 64 != 0) return best;
+  const int nk = K / 64;
+  const long cus = device_cu_count();
+  double best_t = 1e30;
+  auto consider = [&](int id, int BM, int BN, int KSTEPS, int R, int split) {
+    if (N % BN != 0 || nk % (KSTEPS * split) != 0 || (nk / KSTEPS / split) % R != 0) return;
+    const long T = (long)((M + BM - 1) / BM) * (N / BN) * split, rounds = (T + cus - 1) / cus;
+    if (8 * T < 7 * rounds * cus) return;
+    // us: 85.6 us for one round of 128 x 384 x 4096 (gate/up at 512 rows)
+    double t = 85.6 * (double)rounds * BM * BN * (K / split) / (128.0 * 384 * 4096);
+    if (split > 1) t += 8.0 * split * (double)M * N / 8e6;
+    if (t < best_t - 1e-9) {
+      best_t = t;
+      best = WdPlan{id, split};
+    }
+  };
+  if (epi == EPI_SWIGLU || epi == EPI_QKV_ROPE) {
+    consider(1, WdWide::BM, WdWide::BN, WdWide::KSTEPS, WdWide::R, 1);
+    consider(2, WdKg2::BM, WdKg2::BN, WdKg2::KSTEPS, WdKg2::R, 1);
+  } else if (epi == EPI_RESID) {
+    // only splits of at least 2048 k: the output projection at 512 rows (K =
+    // 4096, split 4) ran 27 us + 9.9 us for its partials in the norm against
+    // 26.4 + 8.1 on the LDS-staged 128 x 128 tile at split 2; the down
+    // projection (K = 12288, split 4) 54.9 + 9.9 against 52.5 + 14.6 at split 8
+    for (int split = 1; split <= 8 && K / split >= 2048; ++split)
+      consider(3, WdRes::BM, WdRes::BN, WdRes::KSTEPS, WdRes::R, split);
+  }
+  return best;
 }
 
 struct Plan {
@@ -1359,6 +1418,8 @@ bool rows_path(int M, int N, int K) { return M >= 1 && M <= 64 && N % 32 == 0 &&
 size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi) {
   const Plan p = plan(M, N, K, epi);
   size_t b = p.split > 1 ? (size_t)p.split * M * N * sizeof(float) : 0;
+  const WdPlan wp = wd_plan(M, N, K, epi);  // with packed weights
+  if (wp.tile && wp.split > 1) b = std::max(b, (size_t)wp.split * M * N * sizeof(float));
   if (rows_path(M, N, K)) b = std::max(b, (size_t)rows_plan(M, N, K).split * M * N * sizeof(float));
   return b;
 }
@@ -1414,42 +1475,14 @@ void launch_gemm_rows(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
 }
 
 template <class TL, int EPI>
-void launch_wd_tile(const GemmArgs& g, hipStream_t s) {
+void launch_wd_tile(const GemmArgs& g, int split, hipStream_t s) {
   const int T = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
   static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_wd_kernel<TL, EPI>,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)TL::LDS_BYTES);
   hip_check(attr, "hipFuncSetAttribute(gemm_wd)");
-  hipLaunchKernelGGL((gemm_wd_kernel<TL, EPI>), dim3(T), dim3(TL::NTH), TL::LDS_BYTES, s, g);
+  hipLaunchKernelGGL((gemm_wd_kernel<TL, EPI>), dim3(T * split), dim3(TL::NTH), TL::LDS_BYTES, s, g);
 }
 
-// Register-direct-weight tile for a launch (0: none, 1: WdWide, 2: WdKg2):
-// SwiGLU and q/k/v GEMMs of 129 .. 1024 rows with the packed copy, when the
-// tile's workgroups fill at least 7/8 of the rounds they take on the compute
-// units (batch-1 LLaDA-8B shape at 512 rows: gate/up on WdWide 99 -> 88 us,
-// q/k/v on WdKg2 65 -> 60 us); of two such tiles the one with less work per
-// compute unit (rounds x tile area), the wider one on ties (gate/up on WdKg2
-// is 512 workgroups in two rounds: 108 us).  Elsewhere the LDS-staged tiles
-// stay.
-int wd_choice(const GemmArgs& a) {
-  if (!a.Wp || a.M <= 128 || a.M > 1024 || (a.epi != EPI_SWIGLU && a.epi != EPI_QKV_ROPE)) return 0;
-  const int nk = a.K / 64;
-  const long cus = device_cu_count();
-  int best = 0;
-  double best_t = 1e30;
-  auto consider = [&](int id, int BM, int BN, int KSTEPS, int R) {
-    if (a.N % BN != 0 || nk % KSTEPS != 0 || (nk / KSTEPS) % R != 0) return;
-    const long T = (long)((a.M + BM - 1) / BM) * (a.N / BN), rounds = (T + cus - 1) / cus;
-    if (8 * T < 7 * rounds * cus) return;
-    const double t = (double)rounds * BM * BN;  // per compute unit: rounds x tile area (4 waves either way)
-    if (t < best_t - 1e-9) {
-      best_t = t;
-      best = id;
-    }
-  };
-  consider(1, WdWide::BM, WdWide::BN, WdWide::KSTEPS, WdWide::R);
-  consider(2, WdKg2::BM, WdKg2::BN, WdKg2::KSTEPS, WdKg2::R);
-  return best;
-}
 
 void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
   if (defer) *defer = PendingResid{};
@@ -1465,19 +1498,28 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
     launch_gemm_rows(a, s, defer);
     return;
   }
-  if (const int wd = wd_choice(a)) {  // a few hundred rows: register-direct weights, staged activations
-    auto go = [&](auto tl) {
-      using TL = decltype(tl);
-      if (a.epi == EPI_SWIGLU)
-        launch_wd_tile<TL, EPI_SWIGLU>(a, s);
-      else
-        launch_wd_tile<TL, EPI_QKV_ROPE>(a, s);
-    };
-    if (wd == 1)
-      go(WdWide{});
+  const WdPlan wp = a.Wp ? wd_plan(a.M, a.N, a.K, a.epi) : WdPlan{0, 1};
+  if (wp.tile) {  // a few hundred rows: register-direct weights, staged activations
+    if (wp.tile == 1)
+      a.epi == EPI_SWIGLU ? launch_wd_tile<WdWide, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdWide, EPI_QKV_ROPE>(a, 1, s);
+    else if (wp.tile == 2)
+      a.epi == EPI_SWIGLU ? launch_wd_tile<WdKg2, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdKg2, EPI_QKV_ROPE>(a, 1, s);
     else
-      go(WdKg2{});
+      launch_wd_tile<WdRes, EPI_RESID>(a, wp.split, s);
     DLLM_LAUNCH_CHECK("gemm_wd");
+    if (wp.split > 1 && defer) {
+      *defer = PendingResid{a.splitk_buf, wp.split};  // the next norm adds them
+    } else if (wp.split > 1) {
+      const long MN = (long)a.M * a.N;
+      switch (wp.split) {
+#define DLLM_CASE(S_) \
+  case S_: launch_splitk_resid<S_>(a.splitk_buf, a.resid, MN, s); break;
+        DLLM_CASE(2) DLLM_CASE(3) DLLM_CASE(4) DLLM_CASE(5) DLLM_CASE(6) DLLM_CASE(7) DLLM_CASE(8)
+#undef DLLM_CASE
+        default: throw HipError("gemm_wd: split must be 1 .. 8");
+      }
+      DLLM_LAUNCH_CHECK("splitk_resid");
+    }
     return;
   }
   const Plan p = plan(a.M, a.N, a.K, a.epi);
