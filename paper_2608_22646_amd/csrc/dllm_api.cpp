@@ -76,6 +76,7 @@ struct Layout {
   size_t raw, gate, up, logits;                  // fp32 path
   size_t part_m, part_s, part_i, ticket, hbf;    // bf16 head
   size_t splitk;                                 // bf16 split-K GEMM partials
+  size_t attn_part, attn_ticket;                 // bf16 key-split attention states and tickets
   size_t conf, argmax, all_done, err;            // step scratch
   size_t total;
 };
@@ -115,6 +116,8 @@ Layout make_layout(const dllm_model_cfg& c, int B, int L, int rows) {
   } else {
     o.ticket = take(4);
     o.hbf = take((size_t)HEAD_FRAG_ROWS * d * 2);
+    o.attn_ticket = take((size_t)B * c.n_heads * 4);
+    o.attn_part = take(attn_split_bytes(B, c.n_heads));
   }
   // sized by the head rows
   o.hb = take(R * d * act);
@@ -238,8 +241,9 @@ void run_embed(const dllm_model* m, const int32_t* x, int B, int L, int row0, in
   if (rope)
     launch_rope_table(at<float>(ws, lay.cosb), at<float>(ws, lay.sinb), L, c.head_dim, c.rope_base,
                       at<int>(ws, lay.err), s);
+  const bool bf = c.dtype == DLLM_BF16;
   launch_embed(x, W(m, 0), c.dtype, at<float>(ws, lay.h), B, rows, L, row0, c.d_model, c.vocab, at<int>(ws, lay.err),
-               s);
+               s, bf ? at<int>(ws, lay.attn_ticket) : nullptr, bf ? B * c.n_heads : 0);
 }
 
 void gemm_bf16(const dllm_model* m, GemmArgs g, void* ws, const Layout& lay, hipStream_t s, int kind,
@@ -346,7 +350,8 @@ void run_layer_bf16(const dllm_model* m, int layer, int part, int B, int L, void
     gemm_bf16(m, g, ws, lay, s, PK_QKV);
     {
       ProfScope p(m, PK_ATTN, s);
-      launch_attn_bf16(g.q, g.k, g.vt, at<bf16_t>(ws, lay.attn), B, Lq, L, c.n_heads, c.n_kv_heads, s);
+      launch_attn_bf16(g.q, g.k, g.vt, at<bf16_t>(ws, lay.attn), B, Lq, L, c.n_heads, c.n_kv_heads, s,
+                       at<float>(ws, lay.attn_part), at<int>(ws, lay.attn_ticket));
     }
     GemmArgs o = layer_gemm(m, layer, 1);
     o.M = M;

@@ -16,6 +16,9 @@
 // its range.  The K rows of the S^T product are fed in a permuted order inside
 // each 16-key group (kperm), so the scores a lane holds for one P.V slice are
 // 8 consecutive keys and its V^T operand is a single 16-byte LDS read.
+#include <algorithm>
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace dllm {
@@ -709,11 +712,299 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
 #endif
 }
 
+// Key-split variant for at most 32 queries per (sequence, head) -- a cached
+// step's block rows against every cached position: the keys of a head are
+// split over NS workgroups of NWS waves, wave w of split s taking the 32-key
+// tiles s nt / NS + w, + NWS, ... (nt tiles in all).  With one query group a
+// tile is read by exactly one wave, so its K and V^T fragments go straight
+// from memory into registers (the next tile's loads in flight under the
+// current one's MFMAs): no LDS ring and no barrier in the loop.  The waves'
+// running (max, sum, output) states are merged in wave order through LDS; with
+// NS > 1 the workgroup publishes the merged state (device-coherent stores) and
+// takes a ticket of its (sequence, head), and the last of the NS workgroups
+// merges the NS states in split order (wave w the output dimensions 32 w ..),
+// writes the bf16 rows and re-arms the ticket.  Tickets start at zero (the
+// forward's embedding kernel clears them) and every launch leaves them zero.
+constexpr int CPOL_SC1_A = 16;  // cache-policy bit: coherent at device (agent) scope
+constexpr int SPLIT_STATE = 17 * 64 * 16;  // bytes of one published state: 16 float4 of o + (m, l) per lane
+
+template <int NWS>
+__global__ void __launch_bounds__(64 * NWS, 1) attn_split_kernel(const bf16_t* __restrict__ q,
+                                                                 const bf16_t* __restrict__ k,
+                                                                 const f16_t* __restrict__ vt,
+                                                                 bf16_t* __restrict__ out, float* __restrict__ part,
+                                                                 int* __restrict__ ticket, int Lq, int L, int Hq,
+                                                                 int Hkv, int NS) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __shared__ float4 xch[NWS > 1 ? NWS - 1 : 1][17][64];
+  __shared__ int last_flag;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // XCD-aware 1-D grid over (sequence, head, split), the splits of a head adjacent
+  const int T = (int)gridDim.x, per = T >> 3, rem = T & 7, xi = (int)blockIdx.x & 7;
+  const int lin = xi * per + min(xi, rem) + ((int)blockIdx.x >> 3);
+  const int s = lin % NS, bh = lin / NS, h = bh % Hq, b = bh / Hq, g = h / (Hq / Hkv);
+  const int lq = lane & 31, half = lane >> 5;
+  const int nt = (L + KT2 - 1) / KT2, tb = (int)((long)s * nt / NS), te = (int)((long)(s + 1) * nt / NS);
+  const bf16_t* kh = k + ((size_t)b * Hkv + g) * L * HD;
+  const f16_t* vh = vt + ((size_t)b * Hkv + g) * HD * L;
+  // reads past this head's K or V^T return zeros (buffer bound)
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, 0, L * HD * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, 0, HD * L * 2, 0x00020000);
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  // K operand i of a tile at key t0: key t0 + kperm(lq), dimensions 16 i + 8 half ..;
+  // V^T operand (jk, ds): dimension 32 ds + lq, keys t0 + 16 jk + 8 half ..
+  const uint32_t ko = (uint32_t)((kperm(lq) * HD + half * 8) * 2), vo = (uint32_t)((lq * L + half * 8) * 2);
+  u32x4_t kb[2][8], vb[2][8];
+  auto load = [&](int t, int set) {
+    const int t0 = t * KT2;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      kb[set][i] = __builtin_amdgcn_raw_buffer_load_b128(rk, ko + (uint32_t)((t0 * HD + 16 * i) * 2), 0, 0);
+#pragma unroll
+    for (int jk = 0; jk < 2; ++jk)
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+        vb[set][jk * 4 + ds] =
+            __builtin_amdgcn_raw_buffer_load_b128(rv, vo + (uint32_t)((ds * 32 * L + t0 + 16 * jk) * 2), 0, 0);
+  };
+
+  bf16x8_t qf[8];
+  {
+    const int qi = lq;
+    const bf16_t* qrow = q + (((size_t)b * Hq + h) * Lq + (qi < Lq ? qi : 0)) * HD;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + ks * 16 + half * 8);
+      if (qi >= Lq) qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+  }
+  f32x16_t o[4];
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ds][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float sc = 1.4426950408889634f / sqrtf((float)HD);
+
+  // one 32-key tile from fragment set S_ (compile-time), the next tile's
+  // fragments loading into the other set meanwhile
+  auto step = [&](int t, auto set_c) {
+    constexpr int cur = decltype(set_c)::value;
+    if (t + NWS < te) load(t + NWS, cur ^ 1);
+    const int t0 = t * KT2;
+    f32x16_t s2, s2b;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s2[r] = s2b[r] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+      s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kb[cur][i]), qf[i], s2, 0, 0, 0);
+      s2b = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kb[cur][i + 1]), qf[i + 1], s2b, 0,
+                                                    0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s2[r] += s2b[r];
+    float mt = -INFINITY;
+    if (t0 + KT2 <= L) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s2[r]);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = t0 + kperm(8 * (r >> 2) + 4 * half + (r & 3));
+        if (key >= L) s2[r] = -INFINITY;
+        mt = fmaxf(mt, s2[r]);
+      }
+    }
+    mt = max_pair32(mt) * sc;
+    if (__ballot(mt > m_run + 8.0f) != 0ull) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = exp2_hw(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[ds][r] *= alpha;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = exp2_hw(fmaf(s2[r], sc, -m_run));
+      s2[r] = p;
+      psum += p;
+    }
+    l_run += psum;
+#pragma unroll
+    for (int jk = 0; jk < 2; ++jk) {
+      f16x8_t pf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)s2[jk * 8 + e];
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+        o[ds] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, vb[cur][jk * 4 + ds]), pf, o[ds],
+                                                       0, 0, 0);
+    }
+  };
+  int t = tb + wave;
+  if (t < te) load(t, 0);
+  while (t < te) {
+    step(t, std::integral_constant<int, 0>{});
+    t += NWS;
+    if (t >= te) break;
+    step(t, std::integral_constant<int, 1>{});
+    t += NWS;
+  }
+
+  // merge the waves in wave order; a wave that saw no key (m = -inf) adds nothing
+  if (NWS > 1) {
+    if (wave > 0) {
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq)
+          xch[wave - 1][ds * 4 + rq][lane] =
+              make_float4(o[ds][4 * rq], o[ds][4 * rq + 1], o[ds][4 * rq + 2], o[ds][4 * rq + 3]);
+      xch[wave - 1][16][lane] = make_float4(m_run, l_run, 0.f, 0.f);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      float m = m_run;
+#pragma unroll
+      for (int e = 0; e < NWS - 1; ++e) m = fmaxf(m, xch[e][16][lane].x);
+      const float a0 = m_run == -INFINITY ? 0.f : exp2_hw(m_run - m);
+      l_run *= a0;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[ds][r] *= a0;
+#pragma unroll
+      for (int e = 0; e < NWS - 1; ++e) {
+        const float me = xch[e][16][lane].x, le = xch[e][16][lane].y;
+        const float ae = me == -INFINITY ? 0.f : exp2_hw(me - m);
+        l_run += le * ae;
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+          for (int rq = 0; rq < 4; ++rq) {
+            const float4 v = xch[e][ds * 4 + rq][lane];
+            o[ds][4 * rq] += v.x * ae;
+            o[ds][4 * rq + 1] += v.y * ae;
+            o[ds][4 * rq + 2] += v.z * ae;
+            o[ds][4 * rq + 3] += v.w * ae;
+          }
+      }
+      m_run = m;
+    }
+  }
+
+  auto store_rows = [&](const f32x16_t* oo, int ds0, int nds, float l) {
+    const float inv = 1.0f / sum_pair32(l);
+    if (lq >= Lq) return;
+    bf16_t* orow = out + ((size_t)b * Lq + lq) * ((size_t)Hq * HD) + (size_t)h * HD;
+    for (int ds = ds0; ds < ds0 + nds; ++ds)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int d = ds * 32 + 8 * rg + 4 * half;
+        uint2 w;
+        w.x = pack_bf16x2(oo[ds - ds0][rg * 4 + 0] * inv, oo[ds - ds0][rg * 4 + 1] * inv);
+        w.y = pack_bf16x2(oo[ds - ds0][rg * 4 + 2] * inv, oo[ds - ds0][rg * 4 + 3] * inv);
+        *reinterpret_cast<uint2*>(orow + d) = w;
+      }
+  };
+  if (NS == 1) {
+    if (wave == 0) store_rows(o, 0, 4, l_run);
+    return;
+  }
+
+  // publish the workgroup's state: lane-contiguous float4s [17][64] per (sequence, head, split)
+  const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc((void*)part, 0, 0x7fffffff, 0x00020000);
+  if (wave == 0) {
+    const uint32_t base = (uint32_t)(((size_t)bh * NS + s) * SPLIT_STATE) + lane * 16;
+#pragma unroll
+    for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const u32x4_t v = {__float_as_uint(o[ds][4 * rq]), __float_as_uint(o[ds][4 * rq + 1]),
+                           __float_as_uint(o[ds][4 * rq + 2]), __float_as_uint(o[ds][4 * rq + 3])};
+        __builtin_amdgcn_raw_buffer_store_b128(v, rp, base + (ds * 4 + rq) * 1024, 0, CPOL_SC1_A);
+      }
+    const u32x4_t ml = {__float_as_uint(m_run), __float_as_uint(l_run), 0u, 0u};
+    __builtin_amdgcn_raw_buffer_store_b128(ml, rp, base + 16 * 1024, 0, CPOL_SC1_A);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) last_flag = atomicAdd(ticket + bh, 1) == NS - 1;
+  __syncthreads();
+  if (!last_flag) return;
+
+  // last workgroup of the head: wave w merges output dimensions 32 ds .. 32 ds
+  // + 31, ds = w, w + NWS, .., of every split in split order (the merged m first)
+  for (int ds = wave; ds < 4; ds += NWS) {
+    // the splits' states in rounds of ZB, all loads of a round in flight at
+    // once; an online merge in split order (the running max raised, the
+    // accumulated rows rescaled)
+    constexpr int ZB = 4;
+    float m = -INFINITY, l = 0.f;
+    f32x16_t acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    for (int z0 = 0; z0 < NS; z0 += ZB) {
+      u32x4_t ml[ZB], ov[ZB][4];
+#pragma unroll
+      for (int j = 0; j < ZB; ++j) {
+        const int z = min(z0 + j, NS - 1);
+        const uint32_t base = (uint32_t)(((size_t)bh * NS + z) * SPLIT_STATE) + lane * 16;
+        ml[j] = __builtin_amdgcn_raw_buffer_load_b128(rp, base + 16 * 1024, 0, CPOL_SC1_A);
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq)
+          ov[j][rq] = __builtin_amdgcn_raw_buffer_load_b128(rp, base + (ds * 4 + rq) * 1024, 0, CPOL_SC1_A);
+      }
+#pragma unroll
+      for (int j = 0; j < ZB; ++j) {
+        if (z0 + j >= NS) break;
+        const float mz = __uint_as_float(ml[j][0]);
+        if (mz == -INFINITY) continue;  // a split that saw no key adds nothing
+        const float mn = fmaxf(m, mz);
+        const float ar = m == -INFINITY ? 0.f : exp2_hw(m - mn), az = exp2_hw(mz - mn);
+        m = mn;
+        l = l * ar + __uint_as_float(ml[j][1]) * az;
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[4 * rq + e] = acc[4 * rq + e] * ar + __uint_as_float(ov[j][rq][e]) * az;
+      }
+    }
+    store_rows(&acc, ds, 1, l);
+  }
+  if (tid == 0) ticket[bh] = 0;
+#endif
+}
+
 }  // namespace
 
+size_t attn_split_bytes(int B, int Hq) { return (size_t)std::max(B * Hq, 512) * SPLIT_STATE; }
+
 void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int Lq, int L, int Hq,
-                      int Hkv, hipStream_t s) {
+                      int Hkv, hipStream_t s, float* split_part, int* split_ticket) {
   if (B * Lq == 0) return;
+  if (Lq <= QW && split_part && split_ticket) {
+    // one query group per head: the keys split over NS workgroups of 4 waves
+    // when that fills 7/8 of the CUs, else of 2 waves (shorter sequences)
+    const long bh = (long)B * Hq, cus = std::min(device_cu_count(), 512);
+    const int nt = (L + KT2 - 1) / KT2;
+    auto splits = [&](int nws) { return (int)std::max(1L, std::min<long>(cus / bh, (nt + nws - 1) / nws)); };
+    const int ns4 = splits(4);
+    if (8 * bh * ns4 >= 7 * cus || ns4 == 1) {
+      hipLaunchKernelGGL(attn_split_kernel<4>, dim3(bh * ns4), dim3(256), 0, s, q, k, vt, out, split_part,
+                         split_ticket, Lq, L, Hq, Hkv, ns4);
+    } else {
+      const int ns2 = splits(2);
+      hipLaunchKernelGGL(attn_split_kernel<2>, dim3(bh * ns2), dim3(128), 0, s, q, k, vt, out, split_part,
+                         split_ticket, Lq, L, Hq, Hkv, ns2);
+    }
+    DLLM_LAUNCH_CHECK("attn_split");
+    return;
+  }
   if (L % 8 == 0) {
     // streaming kernel: 8 waves (256 queries) per workgroup when that still gives
     // two or more workgroups per CU over the launch, else 4 waves; when even the

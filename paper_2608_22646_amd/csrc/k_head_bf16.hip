@@ -94,13 +94,14 @@ __device__ __forceinline__ size_t head_bf16_packed_bytes_dev(int V, int d) {
 // result (lane holds vocabulary entries v0 + 8 (r/4) + 4 half + r%4, r < 16),
 // merged across the lane pair: valid in the half == 0 lane.  Writes the logits
 // too when a debug buffer is given.
+template <bool LG = true>
 __device__ __forceinline__ Stat tile_stat(const HeadArgs& a, const f32x16_t& acc, int row, int v0, int half) {
   Stat st{-INFINITY, 0.f, 0x7fffffff};
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int v = v0 + 8 * (r >> 2) + 4 * half + (r & 3);
     const float x = acc[r];
-    if (a.logits && row < a.R && v < a.V) a.logits[(size_t)row * a.V + v] = x;
+    if (LG && a.logits && row < a.R && v < a.V) a.logits[(size_t)row * a.V + v] = x;
     if (v < a.V && v != a.mask_id && x > st.m) {
       st.m = x;
       st.i = v;
@@ -395,6 +396,193 @@ __global__ void __launch_bounds__(256, 1) head_stream_kernel(HeadArgs a) {
 #endif
 }
 
+// Register-direct variant for more than 32 head rows (batched decodes): the
+// workgroup tile is one 256-row vocabulary tile of the copy x all head rows
+// (up to 32 TI); wave w owns the tile's 32-row groups 2w and 2w + 1, whose
+// 1 KiB operands stream straight from the copy into a register ring of P slices
+// (non-temporal; four slices at 256 head rows, where the accumulators fill the
+// AGPRs), while the head rows' 64-k slice of each k-step is staged by LDS-DMA
+// in a 4-stage ring (one barrier per k-step) that all four waves read.
+// In the LDS-ring kernel above every wave re-reads all head rows from LDS for
+// its 32 vocabulary rows; here each head-row fragment serves two MFMAs and the
+// vocabulary rows never touch LDS.  Per slice a wave runs 2 TI MFMAs with W as
+// the A operand; at the end of a tile the lanes' entries are reduced
+// (tile_stat), merged across the waves through LDS into the per-row running
+// statistics, and the workgroups' partials merged as in the other kernels.
+// The ring's issue order and wait counts are those of the register-direct GEMM
+// (stages of one 64-k step: four slices per stage, two DMA loads per slice).
+template <int TI, bool LG>
+__global__ void __launch_bounds__(256, 1) head_wd_kernel(HeadArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  // a 4-slice weight ring at 256 head rows, where the accumulators fill the AGPRs
+  constexpr int NW = 4, NT = 256, TJ = 2, AS = 4, P = TI == 8 ? 4 : 8, U = 4, BM = 32 * TI, R2 = P / U;
+  constexpr int STAGE = BM * 128;   // head rows x 64 k
+  constexpr int IA = BM / 8 / NW;   // DMA loads per wave per stage
+  constexpr int IU = IA / U;        // ... per slice
+  static_assert(IU * U == IA && IU >= 1 && HEAD_TILE == 32 * TJ * NW, "tile shape");
+  constexpr int PER = TJ + IU;
+  constexpr int C1 = TJ + (AS - 3) * U * PER + (U - 1) * PER + IU;
+  constexpr int C0 = (AS - 3) * IA + P * TJ + (U - 1) * PER + IU;
+  constexpr int CMIN = C0 < C1 ? C0 : C1;
+  constexpr int CWAIT = CMIN < 63 ? CMIN : 63;
+  constexpr int CFIRST = ((AS - 2) * IA + P * TJ) < 63 ? (AS - 2) * IA + P * TJ : 63;
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  __shared__ Stat wst[NW][BM];
+  __shared__ Stat fin[NT];
+  __shared__ int last_flag;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lrow = lane & 31, lhalf = lane >> 5;
+  const int G = gridDim.x, nk = a.d / BK;
+  const int ntiles = (a.V + HEAD_TILE - 1) / HEAD_TILE;
+  const int my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / G + 1 : 0;
+  const int units = my_tiles * nk;  // stages: (tile, 64-k step)
+
+  // head-row DMA: instruction q of wave w fills rows 8 (4 q + w) .. +7; lane l
+  // writes row + l/8, slot l%8 holding chunk (l%8) ^ ((row >> 1) & 7); rows
+  // past R repeat the last row (never used)
+  const int dr = lane >> 3, dc = (lane & 7) ^ (((wave & 1) << 2) | (dr >> 1));
+  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc((void*)a.hb, 0, 0x7fffffff, 0x00020000);
+  uint32_t voh[IA];
+#pragma unroll
+  for (int q = 0; q < IA; ++q) {
+    const int row = min(8 * (4 * q + wave) + dr, a.R - 1);
+    voh[q] = (uint32_t)(((size_t)row * a.d + dc * 8) * 2);
+  }
+  // stage u's LDS slot and head-row k offset (past the end: the last stage
+  // again, never read), and the byte offset of its 32 KiB (tile, k-step) run
+  // of the copy; computed once per stage
+  auto a_soff = [&](int u) { return (min(u, units - 1) % nk) * BK * 2; };
+  auto w_run = [&](int u) {
+    u = min(u, units - 1);
+    const int i = u / nk;
+    return (uint32_t)(((size_t)(blockIdx.x + i * G) * nk + (u - i * nk)) * (HEAD_TILE / 32) * 4 * 1024);
+  };
+  auto issue_a = [&](int slot, int soff, int q) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rh, (lds_ptr_t)(lds + slot * STAGE + 8 * (4 * q + wave) * 128), 16,
+                                             voh[q], soff, 0, 0);
+  };
+  const uint32_t wbytes = (uint32_t)head_bf16_packed_bytes_dev(a.V, a.d);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, 0, wbytes, 0x00020000);
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  u32x4_t wbuf[P][TJ];
+  const uint32_t wlane = (uint32_t)(2 * wave * 4 * 1024 + lane * 16);
+  // operand j (group 2 wave + j of the tile) of slice sl of the stage whose run starts at run
+  auto load_w = [&](uint32_t run, int sl, int slot, int j) {
+    wbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rw, run + wlane + (uint32_t)((j * 4 + sl) * 1024), 0,
+                                                          CPOL_NT);
+  };
+  bf16x8_t af[2][TI];
+  auto frag = [&](const char* base, int sl, int set) {
+#pragma unroll
+    for (int ii = 0; ii < TI; ++ii)
+      af[set][ii] = *reinterpret_cast<const bf16x8_t*>(base + swz(32 * ii + lrow, 2 * sl + lhalf));
+  };
+  f32x16_t acc[TJ][TI];
+#pragma unroll
+  for (int j = 0; j < TJ; ++j)
+#pragma unroll
+    for (int ii = 0; ii < TI; ++ii)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[j][ii][r] = 0.f;
+  Stat run{-INFINITY, 0.f, 0x7fffffff};  // thread r < R: running statistics of head row r
+
+  static_assert(P % U == 0, "slices P later are in stage u + P / U");
+  if (units > 0) {
+#pragma unroll
+    for (int t = 0; t < AS - 1; ++t)
+#pragma unroll
+      for (int q = 0; q < IA; ++q) issue_a(t, a_soff(t), q);
+#pragma unroll
+    for (int v = 0; v < P; ++v)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) load_w(w_run(v / U), v % U, v, j);
+    wait_vm_lds<CFIRST>();
+    barrier_nofence_h();
+    frag(lds, 0, 0);
+  }
+  for (int ti = 0; ti < my_tiles; ++ti) {
+    for (int k0 = 0; k0 < nk; k0 += R2) {
+#pragma unroll
+      for (int rr = 0; rr < R2; ++rr) {
+        const int u = ti * nk + k0 + rr;
+        const char* base = lds + (u % AS) * STAGE;
+        // this stage's loads: the DMA of stage u + AS - 1, the weights of stage u + P / U
+        const int aslot = (u + AS - 1) % AS, asoff = a_soff(u + AS - 1);
+        const uint32_t wnext = w_run(u + P / U);
+#pragma unroll
+        for (int sl = 0; sl < U; ++sl) {
+          const int slot = (rr * U + sl) % P;
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int q = 0; q < IU; ++q) issue_a(aslot, asoff, sl * IU + q);
+          if (sl + 1 < U) {
+            frag(base, sl + 1, (sl + 1) & 1);
+          } else {
+            wait_vm_lds<CWAIT>();
+            barrier_nofence_h();
+            frag(lds + ((u + 1) % AS) * STAGE, 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) {
+#pragma unroll
+            for (int ii = 0; ii < TI; ++ii)
+              acc[j][ii] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wbuf[slot][j]),
+                                                                  af[sl & 1][ii], acc[j][ii], 0, 0, 0);
+            load_w(wnext, sl, slot, j);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x020, IU, 0);
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) {
+            if (j == 0) {
+#pragma unroll
+              for (int ii = 0; ii < TI; ++ii) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+              }
+            } else {
+              __builtin_amdgcn_sched_group_barrier(0x008, TI, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // end of a vocabulary tile: lane holds head row 32 ii + lrow, entries
+    // v0 + 8 (r / 4) + 4 lhalf + r % 4 of group 2 wave + j
+    const int t = blockIdx.x + ti * G;
+#pragma unroll
+    for (int ii = 0; ii < TI; ++ii) {
+      Stat st = tile_stat<LG>(a, acc[0][ii], 32 * ii + lrow, t * HEAD_TILE + (2 * wave) * 32, lhalf);
+      st = merge(st, tile_stat<LG>(a, acc[1][ii], 32 * ii + lrow, t * HEAD_TILE + (2 * wave + 1) * 32, lhalf));
+      if (lhalf == 0) wst[wave][32 * ii + lrow] = st;
+      __builtin_amdgcn_sched_barrier(0);  // one row block at a time (register pressure)
+    }
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int ii = 0; ii < TI; ++ii)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[j][ii][r] = 0.f;
+    // debug logits stores count in vmcnt too: drain them so the ring's
+    // counts keep describing its loads only
+    if (LG) wait_vm_lds<0>();
+    // an LDS barrier that leaves the ring's loads in flight; wst is next
+    // written a whole tile (and many barriers) later
+    wait_vm_lds<63>();
+    barrier_nofence_h();
+    if (tid < a.R) {
+      Stat w = wst[0][tid];
+#pragma unroll
+      for (int x = 1; x < NW; ++x) w = merge(w, wst[x][tid]);
+      run = merge(run, w);
+    }
+  }
+  wait_vm_lds<0>();
+  publish_and_merge<NT>(a, run, tid, fin, last_flag);
+#endif
+}
+
 // one thread per 16-byte vector of the tiled copy, in destination order
 __global__ void pack_head_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Wt, int V, int d, size_t nvec) {
   const int nk = d / 64;
@@ -491,10 +679,33 @@ void launch_head_bf16(const HeadArgs& a, hipStream_t s) {
       hipLaunchKernelGGL((head_stream_kernel<2, 16>), dim3(grid), dim3(256), 0, s, a);
     else
       hipLaunchKernelGGL((head_stream_kernel<1, 16>), dim3(grid), dim3(256), 0, s, a);
+  } else if (rg > 2) {
+    // register-direct vocabulary rows (65..256 head rows): 256-row vocabulary
+    // tiles spread evenly over at most one workgroup per CU
+    const int ntiles = (a.V + HEAD_TILE - 1) / HEAD_TILE, cus = std::min(device_cu_count(), MAX_WG);
+    const int per = (ntiles + cus - 1) / cus, grid = (ntiles + per - 1) / per;
+    // the variant that also stores the logits (a debug buffer) is its own kernel
+    auto go1 = [&](auto tic, auto lgc) {
+      constexpr int TI = decltype(tic)::value;
+      constexpr bool LG = decltype(lgc)::value;
+      constexpr size_t lds = (size_t)4 * TI * 32 * 128;
+      static const hipError_t attr = hipFuncSetAttribute((const void*)head_wd_kernel<TI, LG>,
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      hip_check(attr, "hipFuncSetAttribute(head_wd)");
+      hipLaunchKernelGGL((head_wd_kernel<TI, LG>), dim3(grid), dim3(256), lds, s, a);
+    };
+    auto go = [&](auto tic) {
+      if (a.logits)
+        go1(tic, std::true_type{});
+      else
+        go1(tic, std::false_type{});
+    };
+    if (rg <= 4)
+      go(std::integral_constant<int, 4>{});
+    else
+      go(std::integral_constant<int, 8>{});
   } else if (rg <= 1) HeadCfg<1, 256, 8, 4>::launch(a, s);
-  else if (rg <= 2) HeadCfg<2, 256, 8, 3>::launch(a, s);
-  else if (rg <= 4) HeadCfg<4, 128, 4, 3>::launch(a, s);
-  else HeadCfg<8, 128, 4, 3>::launch(a, s);
+  else HeadCfg<2, 256, 8, 3>::launch(a, s);
   DLLM_LAUNCH_CHECK("head_bf16");
 }
 

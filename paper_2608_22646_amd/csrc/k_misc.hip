@@ -22,8 +22,10 @@ int device_cu_count() {
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ x, const T* __restrict__ E,
                                                     float* __restrict__ h, int rows, int L, int row0, int d, int V,
-                                                    int* __restrict__ err) {
+                                                    int* __restrict__ err, int* __restrict__ zero, int nzero) {
   const int m = blockIdx.x, b = m / rows, i = m - b * rows;
+  if (m == 0)
+    for (int z = threadIdx.x; z < nzero; z += 256) zero[z] = 0;
   const int tok = x[(size_t)b * L + row0 + i];
   const bool ok = tok >= 0 && tok < V;
   const size_t src = (size_t)(ok ? tok : 0) * d;
@@ -33,15 +35,16 @@ __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ 
 }
 
 void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int B, int rows, int L, int row0, int d,
-                  int V, int* err, hipStream_t s) {
+                  int V, int* err, hipStream_t s, int* zero, int nzero) {
   const int M = B * rows;
   if (M == 0) return;
+  if (!zero) nzero = 0;
   if (dtype == 0)
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, x, (const float*)E, h, rows, L, row0, d, V,
-                       err);
+                       err, zero, nzero);
   else
     hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(M), dim3(256), 0, s, x, (const bf16_t*)E, h, rows, L, row0, d, V,
-                       err);
+                       err, zero, nzero);
   DLLM_LAUNCH_CHECK("embed");
 }
 

@@ -9,9 +9,10 @@ namespace dllm {
 // cannot represent and reported (then cleared) by the commit kernel.
 enum { ERR_TOKEN_RANGE = 1, ERR_V_RANGE = 2 };
 // h[b*rows + i, :] = float(E[x[b*L + row0 + i], :]) for b < B, i < rows.  An id
-// outside [0, V) gathers a zero row and sets ERR_TOKEN_RANGE in *err.
+// outside [0, V) gathers a zero row and sets ERR_TOKEN_RANGE in *err.  The
+// nzero ints at zero (the forward's attention tickets) are set to 0.
 void launch_embed(const int32_t* x, const void* E, int dtype, float* h, int B, int rows, int L, int row0, int d,
-                  int V, int* err, hipStream_t s);
+                  int V, int* err, hipStream_t s, int* zero = nullptr, int nzero = 0);
 // cos/sin [L, hd/2] of pos * base^(-2j/hd), evaluated in float64, stored float32;
 // a non-null err word is cleared first (a forward starts with a clean word).
 void launch_rope_table(float* cosb, float* sinb, int L, int hd, double base, int* err, hipStream_t s);
@@ -102,9 +103,12 @@ size_t gemm_bf16_splitk_bytes(int M, int N, int K, int epi);
 
 // Non-causal attention of Lq queries per sequence (q [B, Hq, Lq, 128]) over L
 // keys (k [B, Hkv, L, 128], v^T [B, Hkv, 128, L] as IEEE half):
-// out[b*Lq + l, h*128 + j] (bf16).
+// out[b*Lq + l, h*128 + j] (bf16).  With split_part (attn_split_bytes(B, Hq)
+// bytes) and split_ticket (B * Hq ints, zero; left zero) a launch of at most 32
+// queries per sequence splits the keys of each head over several workgroups.
+size_t attn_split_bytes(int B, int Hq);
 void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t* out, int B, int Lq, int L, int Hq,
-                      int Hkv, hipStream_t s);
+                      int Hkv, hipStream_t s, float* split_part = nullptr, int* split_ticket = nullptr);
 
 // The bf16 LM head is read from a tiled copy: vocabulary tiles of HEAD_TILE rows,
 // each stored as d/64 consecutive [HEAD_TILE, 64] blocks, rows past V zero;
