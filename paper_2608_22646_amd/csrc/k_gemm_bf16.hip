@@ -990,8 +990,9 @@ using WdWide = WdTile<4, 3, 4, 2, 4, 8>;
 // q/k/v-sized launches: 128 x 192 in two k-groups (M = 512, N = 12288: 256 workgroups)
 using WdKg2 = WdTile<4, 3, 2, 2, 4, 8>;
 // residual projections (N = d_model): 128 x 256, split over K (M = 512, N =
-// 4096: 64 tiles x 4 splits)
+// 4096: 64 tiles x 4 splits), or 128 x 128 in two k-groups (128 tiles x 2)
 using WdRes = WdTile<4, 2, 4, 2, 4, 8>;
+using WdRes2 = WdTile<4, 2, 2, 2, 4, 8>;
 
 template <class TL, int EPI>
 __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
@@ -1254,17 +1255,18 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
 }
 
 // Register-direct-weight plan for a launch of 129 .. 1024 rows with the packed
-// copy (tile 0: none, 1: WdWide, 2: WdKg2, 3: WdRes; split over K), taken when
-// the tile's workgroups fill at least 7/8 of the rounds they take on the
-// compute units.  SwiGLU and q/k/v (no split): of WdWide and WdKg2 the one
-// with less work per compute unit (rounds x tile area), the wider one on ties
-// -- batch-1 LLaDA-8B shape at 512 rows: gate/up on WdWide 99 -> 86 us (on
-// WdKg2, 512 workgroups in two rounds: 108 us), q/k/v on WdKg2 65 -> 60 us.
-// Residual GEMMs on WdRes, the split by a time model: rounds x the tile's
-// multiply-adds at the gate/up kernel's measured rate, plus the float32
-// partials written here and read back by the next norm (~8 TB/s); the
-// split's k-range must be whole stages of at least 2048 k.  Elsewhere the
-// LDS-staged tiles stay.
+// copy (tile 0: none, 1: WdWide, 2: WdKg2, 3: WdRes, 4: WdRes2; split over K),
+// taken when the tile's workgroups fill at least 7/8 of the rounds they take
+// on the compute units.  At these sizes a workgroup is bounded by the bytes
+// its CU pulls through the vector-memory path, (BM + BN) x its k-range x 2
+// (the texture-address unit ~80% busy on the gate/up launch), so the time
+// model is rounds x (20.4 us per MB + 5 us), calibrated on the LLaDA-8B shape
+// at 512 rows (gate/up WdWide 85.6 us, q/k/v WdKg2 59.3, down WdRes at split 4
+// 54.9, output projection WdRes2 at split 2 26.1, down WdRes2 at split 2
+// 60.9), plus for split-K the partials the next norm reads (~1.5 us per split
+// per 2^21 outputs: the fused norm at 512 x 4096 took 7.6 / 10.6 / 14.6 us
+// with 2 / 4 / 8 of them); a split's k-range must be whole stages of at
+// least 2048 k.  Elsewhere the LDS-staged tiles stay.
 struct WdPlan {
   int tile, split;
 };
@@ -1278,9 +1280,8 @@ WdPlan wd_plan(int M, int N, int K, int epi) {
     if (N % BN != 0 || nk % (KSTEPS * split) != 0 || (nk / KSTEPS / split) % R != 0) return;
     const long T = (long)((M + BM - 1) / BM) * (N / BN) * split, rounds = (T + cus - 1) / cus;
     if (8 * T < 7 * rounds * cus) return;
-    // us: 85.6 us for one round of 128 x 384 x 4096 (gate/up at 512 rows)
-    double t = 85.6 * (double)rounds * BM * BN * (K / split) / (128.0 * 384 * 4096);
-    if (split > 1) t += 8.0 * split * (double)M * N / 8e6;
+    double t = (double)rounds * (20.4e-6 * (BM + BN) * (double)(K / split) * 2 + 5.0);
+    if (split > 1) t += 1.5 * split * (double)M * N / (1 << 21);
     if (t < best_t - 1e-9) {
       best_t = t;
       best = WdPlan{id, split};
@@ -1294,8 +1295,10 @@ WdPlan wd_plan(int M, int N, int K, int epi) {
     // 4096, split 4) ran 27 us + 9.9 us for its partials in the norm against
     // 26.4 + 8.1 on the LDS-staged 128 x 128 tile at split 2; the down
     // projection (K = 12288, split 4) 54.9 + 9.9 against 52.5 + 14.6 at split 8
-    for (int split = 1; split <= 8 && K / split >= 2048; ++split)
+    for (int split = 1; split <= 8 && K / split >= 2048; ++split) {
       consider(3, WdRes::BM, WdRes::BN, WdRes::KSTEPS, WdRes::R, split);
+      consider(4, WdRes2::BM, WdRes2::BN, WdRes2::KSTEPS, WdRes2::R, split);
+    }
   }
   return best;
 }
@@ -1504,8 +1507,10 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
       a.epi == EPI_SWIGLU ? launch_wd_tile<WdWide, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdWide, EPI_QKV_ROPE>(a, 1, s);
     else if (wp.tile == 2)
       a.epi == EPI_SWIGLU ? launch_wd_tile<WdKg2, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdKg2, EPI_QKV_ROPE>(a, 1, s);
-    else
+    else if (wp.tile == 3)
       launch_wd_tile<WdRes, EPI_RESID>(a, wp.split, s);
+    else
+      launch_wd_tile<WdRes2, EPI_RESID>(a, wp.split, s);
     DLLM_LAUNCH_CHECK("gemm_wd");
     if (wp.split > 1 && defer) {
       *defer = PendingResid{a.splitk_buf, wp.split};  // the next norm adds them
