@@ -126,9 +126,11 @@ def _head_model(V, d, mask_id_at_top=True):
 
 # up to 32 head rows use the streaming kernel (R = 32, 20: ragged vocabulary
 # tiles; V = 150000: 640-row tiles, five groups per wave, the last one ragged);
-# more use the LDS-ring kernel (R = 64, 60, 256)
+# 33..64 use the LDS-ring kernel (R = 64, 60); 65..256 the register-direct
+# kernel (R = 96: four 32-row groups, the last past R; R = 150 with V = 150000:
+# eight groups, ragged rows and a last vocabulary tile past V; R = 256)
 @pytest.mark.parametrize("Bn,rows,V", [(1, 32, 4096), (1, 32, 4000), (1, 20, 2176), (2, 32, 4000), (8, 32, 4096),
-                                       (3, 20, 2176), (1, 32, 150000)])
+                                       (3, 20, 2176), (1, 32, 150000), (3, 32, 4000), (5, 30, 150000)])
 def test_head_exact_logit_fixture(Bn, rows, V):
     """Hidden rows of +-1 (RMSNorm is then the identity) and integer weights make
     every logit an exact small integer in float32, so the argmax (with ties going
