@@ -949,9 +949,10 @@ RowsPlan rows_plan(int M, int N, int K) {
 // above), one barrier per stage.  Past the last stage the DMA and the weight
 // loads are issued again on the last valid addresses (their results are never
 // used), so every wait below counts a fixed number of later loads.
-template <int TI_, int TJ_, int NWN_, int KSTEPS_, int AS_, int P_>
+template <int TI_, int TJ_, int NWN_, int KSTEPS_, int AS_, int P_, int PF_ = 0>
 struct WdTile {
   static constexpr int TI = TI_, TJ = TJ_, NWN = NWN_, KG = 4 / NWN_, KSTEPS = KSTEPS_, AS = AS_, P = P_;
+  static constexpr int PF = PF_;  // stages ahead of the L2 prefetch of the weight tile (0: none)
   static constexpr int NW = 4, NTH = 256;
   static constexpr int BM = 32 * TI, BN = 32 * TJ * NWN;
   static constexpr int SPS = 4 * KSTEPS;                // 16-k slices per stage
@@ -984,15 +985,20 @@ struct WdTile {
   static constexpr size_t LDS = (size_t)AS * STAGE;
   static constexpr size_t MERGE = KG == 1 ? 0 : (size_t)NWN * TI * TJ * 16 * 64 * 4;
   static constexpr size_t LDS_BYTES = LDS > MERGE ? LDS : MERGE;
+  static constexpr size_t LDS_ALLOC = LDS_BYTES + 256;  // + the prefetch loads' scratch word per lane
 };
 // Batch-1 gate/up (M = 512, N = 24576): 4 x 64 = 256 workgroups of 128 x 384
 using WdWide = WdTile<4, 3, 4, 2, 4, 8>;
 // q/k/v-sized launches: 128 x 192 in two k-groups (M = 512, N = 12288: 256 workgroups)
 using WdKg2 = WdTile<4, 3, 2, 2, 4, 8>;
 // residual projections (N = d_model): 128 x 256, split over K (M = 512, N =
-// 4096: 64 tiles x 4 splits), or 128 x 128 in two k-groups (128 tiles x 2)
-using WdRes = WdTile<4, 2, 4, 2, 4, 8>;
-using WdRes2 = WdTile<4, 2, 2, 2, 4, 8>;
+// 4096: 64 tiles x 4 splits), or 128 x 128 in two k-groups (128 tiles x 2);
+// both prefetch their weights two stages ahead into L2 (LLaDA-8B shape at 512
+// rows: down 54.0 -> 51.7 us, output projection 26.9 -> 25.6 us; on the
+// gate/up and q/k/v tiles the same prefetch halved the L1-miss latency and
+// changed nothing, 85.8 / 60.4 us either way)
+using WdRes = WdTile<4, 2, 4, 2, 4, 8, 2>;
+using WdRes2 = WdTile<4, 2, 2, 2, 4, 8, 2>;
 
 template <class TL, int EPI>
 __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
@@ -1043,6 +1049,28 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
     wbase[j] = (uint32_t)((((size_t)(G >> 3) * nk * 8 + (G & 7)) * 4) * 1024 + lane * 16 +
                           (kg * TL::SPG) * 1024);
   }
+  // L2 prefetch (PF > 0): the MT row tiles that share this weight tile each
+  // touch one 128-byte line per lane of their share of its stage PF ahead
+  // (dword LDS-DMA loads into a scratch word per lane of LDS: no registers
+  // held), so that the weight loads of all of them find the lines in their
+  // XCD's L2
+  constexpr int NG = TJ * TL::NWN, LPS = NG * 32 * TL::KSTEPS;
+  const int LP = (LPS + MT - 1) / MT, NI = (LP + 63) / 64;
+  uint32_t pfo[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int pl = min((tile % MT) * LP + min((wave + 4 * q) * 64 + lane, LP - 1), LPS - 1);
+    const int ks = pl / (NG * 32), rem = pl % (NG * 32), G = n0 / 32 + rem / 32;
+    pfo[q] = (uint32_t)(((size_t)(G >> 3) * nk + ks) * 32768 + (G & 7) * 4096 + (rem % 32) * 128);
+  }
+  auto prefetch = [&](int t) {
+    if (TL::PF == 0 || t >= nst) return;
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+      if (wave + 4 * q < NI)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(lds + TL::LDS_BYTES), 4, pfo[q],
+                                                 (st0 + t) * (TL::KSTEPS * 32768), 0, 0);
+  };
   typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
   u32x4_t wbuf[P][TJ];
   // operand j of the wave's slice uu (compile-time) of stage t, into ring slot
@@ -1093,6 +1121,10 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
         // the slice that reuses this ring slot: P slices later
         const int tn = t + (uu + P) / U, un = (uu + P) % U;
         __builtin_amdgcn_sched_barrier(0);
+        if (TL::PF > 0 && uu == 0) {
+          prefetch(t + TL::PF);
+          __builtin_amdgcn_sched_barrier(0);
+        }
         // a share of stage t + AS - 1 into the slot stage t - 1 left (every
         // wave passed the barrier that ended it)
 #pragma unroll
@@ -1484,9 +1516,9 @@ template <class TL, int EPI>
 void launch_wd_tile(const GemmArgs& g, int split, hipStream_t s) {
   const int T = ((g.M + TL::BM - 1) / TL::BM) * (g.N / TL::BN);
   static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_wd_kernel<TL, EPI>,
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)TL::LDS_BYTES);
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)TL::LDS_ALLOC);
   hip_check(attr, "hipFuncSetAttribute(gemm_wd)");
-  hipLaunchKernelGGL((gemm_wd_kernel<TL, EPI>), dim3(T * split), dim3(TL::NTH), TL::LDS_BYTES, s, g);
+  hipLaunchKernelGGL((gemm_wd_kernel<TL, EPI>), dim3(T * split), dim3(TL::NTH), TL::LDS_ALLOC, s, g);
 }
 
 
