@@ -37,6 +37,7 @@ CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_2264
 TRAFFIC = {
     "gate_up": ("gemm_gateup_llada_b1_traffic.txt", "k_gemm_bf16.hip", "gemm_source_sha256"),
     "lm_head": ("head_stream_llada_b1_traffic.txt", "k_head_bf16.hip", "head_source_sha256"),
+    "resid_norm": ("resid_rmsnorm_llada_b1_traffic.txt", "k_misc.hip", "misc_source_sha256"),
 }
 
 
@@ -489,6 +490,11 @@ def main():
         "lm_head_hbm_frac": hbytes / head_s / 1e9 / HBM_PEAK_GBS,
         # algorithmic bytes of one LM-head launch and what the HBM counters read
         "lm_head_bytes": {"algorithmic": hbytes, "traffic": measured_traffic(wl.name, "lm_head")},
+        # the norm that follows the down projection adds that GEMM's split-K
+        # partials to the residual: the bytes of the norm alone (residual read
+        # and written, bf16 rows written) and what the HBM counters read for it
+        "resid_norm_bytes": {"norm_only": B * L * cfg.d_model * 10 if cfg.dtype == "bf16" else None,
+                             "traffic": measured_traffic(wl.name, "resid_norm")},
         # the commit kernel is latency-bound (~5 us for a few KB): conf, argmax,
         # s and budget read, x and commit_step read and written, reason written
         "commit_hbm_frac": B * bl * 33 / (breakdown["commit"]["ms_per_forward"] / 1e3) / 1e9 / HBM_PEAK_GBS,

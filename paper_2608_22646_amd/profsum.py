@@ -51,8 +51,9 @@ def traffic(fetch, write, cfetch, cwrite, substr, copy_bytes, command):
     tb = (f_kib * ff + w_kib * fw) * 1024.0
     # the source the counted kernel is built from, hashed so that a reader of
     # the summary can tell when the kernel has changed since
-    name = "head" if "head_stream" in substr else "gemm"
-    src = os.path.join(HERE, "csrc", "k_head_bf16.hip" if name == "head" else "k_gemm_bf16.hip")
+    name, fname = (("head", "k_head_bf16.hip") if "head_stream" in substr else
+                   ("misc", "k_misc.hip") if "rmsnorm" in substr else ("gemm", "k_gemm_bf16.hip"))
+    src = os.path.join(HERE, "csrc", fname)
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
     print(f"# HBM traffic of one launch from rocprofv3 --pmc counters\n# command: {command}")
     print(f"# kernel: launches whose name contains '{substr}'")
