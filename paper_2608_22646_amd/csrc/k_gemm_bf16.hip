@@ -335,18 +335,20 @@ __device__ __forceinline__ void epi_unit(const GemmArgs& g, int wave, int lane, 
 // even touching 32 cache lines per instruction).  Instead each wave writes its
 // finished values into the LDS ring (free once the main loop is done) in the
 // destination's order, and the workgroup then stores 16-byte chunks.
-template <class TL>
-struct Stage {
+template <int BM, int BN>
+struct StageGeo {
   // SwiGLU: [BM][BN/2] bf16, rows padded by 16 bytes (conflict-free writes)
-  static constexpr int SW_ROW = TL::BN + 16;
-  static constexpr int SW_BYTES = TL::BM * SW_ROW;
+  static constexpr int SW_ROW = BN + 16;
+  static constexpr int SW_BYTES = BM * SW_ROW;
   // q/k/v: one area per 32-column block; a q/k block holds [BM][32] bf16
   // (64-byte rows: dimensions d .. d+15, then d+64 .. d+79), a v block
   // [32][BM] half (v^T, each column padded by 16 bytes)
-  static constexpr int VROW = (TL::BM + 8) * 2;
-  static constexpr int BLK = (TL::BM * 64 > 32 * VROW) ? TL::BM * 64 : 32 * VROW;
-  static constexpr int QKV_BYTES = TL::BN / 32 * BLK;
+  static constexpr int VROW = (BM + 8) * 2;
+  static constexpr int BLK = (BM * 64 > 32 * VROW) ? BM * 64 : 32 * VROW;
+  static constexpr int QKV_BYTES = BN / 32 * BLK;
 };
+template <class TL>
+struct Stage : StageGeo<TL::BM, TL::BN> {};
 
 // k-group merge area: the second group's accumulators, [NWT][TI*TJ][4][64 lanes] float4
 template <class TL>
@@ -399,6 +401,76 @@ __device__ __forceinline__ int2 seq_pos(int m, int L, float inv_l) {
     ++b;
   }
   return make_int2(b, p);
+}
+
+// Store phase of the staged epilogues: the workgroup's NTH threads write the
+// staged tile (StageGeo layout) to its destination as 16-byte chunks.
+template <int BM, int BN, int NTH, int EPI>
+__device__ __forceinline__ void staged_store(const GemmArgs& g, const char* lds, int m0, int n0) {
+  using St = StageGeo<BM, BN>;
+  constexpr int HD = 128, HALF = 64;
+  const int nq = g.Hq * HD, nkv = g.Hkv * HD;
+  const float inv_l = 1.0f / (float)g.Lq;  // rows per sequence
+  const int tid = threadIdx.x;
+  if (EPI == EPI_SWIGLU) {
+    const int F = g.N / 2, f0 = n0 / 2;
+    constexpr int CH = BN / 16;  // 16-byte chunks per row
+    for (int it = tid; it < BM * CH; it += NTH) {
+      const int r = it / CH, q = it - r * CH, m = m0 + r;
+      if (m < g.M)
+        *reinterpret_cast<uint4*>(g.out + (size_t)m * F + f0 + 8 * q) =
+            *reinterpret_cast<const uint4*>(lds + r * St::SW_ROW + 16 * q);
+    }
+    return;
+  }
+#pragma unroll 1
+  for (int jb = 0; jb < BN / 32; ++jb) {
+    const int vb = n0 + jb * 32;
+    const char* blk = lds + jb * St::BLK;
+    if (vb < nq + nkv) {
+      const bool isq = vb < nq;
+      const int rel = isq ? vb : vb - nq;
+      const int head = rel / HD, d0 = 16 * ((rel % HD) >> 5);
+      // q [B, Hq, Lq, hd] at row i; k [B, Hkv, L, hd] at position pos0 + i
+      const int H = isq ? g.Hq : g.Hkv, LL = isq ? g.Lq : g.L, p0 = isq ? 0 : g.pos0;
+      bf16_t* dst = isq ? g.q : g.k;
+      for (int it = tid; it < BM * 4; it += NTH) {
+        const int r = it >> 2, q = it & 3, m = m0 + r;
+        if (m >= g.M) continue;
+        const int2 bp = seq_pos(m, g.Lq, inv_l);
+        const int b = bp.x, pos = p0 + bp.y;
+        const int dim = (q < 2 ? d0 : HALF + d0) + 8 * (q & 1);
+        *reinterpret_cast<uint4*>(dst + (((size_t)b * H + head) * LL + pos) * HD + dim) =
+            *reinterpret_cast<const uint4*>(blk + r * 64 + 16 * q);
+      }
+    } else {
+      const int rel = vb - nq - nkv;
+      const int head = rel / HD, cj0 = rel % HD;
+      constexpr int RC = BM / 8;  // 8-row chunks per column
+      for (int it = tid; it < 32 * RC; it += NTH) {
+        const int c = it / RC, t = it - c * RC, m = m0 + 8 * t;
+        if (m >= g.M) continue;
+        const uint4 val = *reinterpret_cast<const uint4*>(blk + c * St::VROW + 16 * t);
+        if (((g.L | g.Lq | g.pos0) & 7) == 0 && m + 7 < g.M) {
+          // eight positions of one sequence, 16-byte aligned (L, Lq, pos0 and m
+          // multiples of 8)
+          const int2 bp = seq_pos(m, g.Lq, inv_l);
+          const int b = bp.x, pos = g.pos0 + bp.y;
+          *reinterpret_cast<uint4*>(g.vt + (((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos) = val;
+        } else {
+          const uint32_t wd[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int mm = m + e;
+            if (mm >= g.M) break;
+            const int2 bp = seq_pos(mm, g.Lq, inv_l);
+            const int b = bp.x, pos = g.pos0 + bp.y;
+            g.vt[(((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos] = (f16_t)(wd[e >> 1] >> (16 * (e & 1)));
+          }
+        }
+      }
+    }
+  }
 }
 
 template <class TL, int EPI>
@@ -510,66 +582,7 @@ __device__ __forceinline__ void epilogue_staged(const GemmArgs& g, char* lds, in
   __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
   barrier_nofence();
 
-  const int tid = threadIdx.x;
-  if (EPI == EPI_SWIGLU) {
-    const int F = g.N / 2, f0 = n0 / 2;
-    constexpr int CH = TL::BN / 16;  // 16-byte chunks per row
-    for (int it = tid; it < TL::BM * CH; it += TL::NTH) {
-      const int r = it / CH, q = it - r * CH, m = m0 + r;
-      if (m < g.M)
-        *reinterpret_cast<uint4*>(g.out + (size_t)m * F + f0 + 8 * q) =
-            *reinterpret_cast<const uint4*>(lds + r * St::SW_ROW + 16 * q);
-    }
-    return;
-  }
-#pragma unroll 1
-  for (int jb = 0; jb < TL::BN / 32; ++jb) {
-    const int vb = n0 + jb * 32;
-    const char* blk = lds + jb * St::BLK;
-    if (vb < nq + nkv) {
-      const bool isq = vb < nq;
-      const int rel = isq ? vb : vb - nq;
-      const int head = rel / HD, d0 = 16 * ((rel % HD) >> 5);
-      // q [B, Hq, Lq, hd] at row i; k [B, Hkv, L, hd] at position pos0 + i
-      const int H = isq ? g.Hq : g.Hkv, LL = isq ? g.Lq : g.L, p0 = isq ? 0 : g.pos0;
-      bf16_t* dst = isq ? g.q : g.k;
-      for (int it = tid; it < TL::BM * 4; it += TL::NTH) {
-        const int r = it >> 2, q = it & 3, m = m0 + r;
-        if (m >= g.M) continue;
-        const int2 bp = seq_pos(m, g.Lq, inv_l);
-        const int b = bp.x, pos = p0 + bp.y;
-        const int dim = (q < 2 ? d0 : HALF + d0) + 8 * (q & 1);
-        *reinterpret_cast<uint4*>(dst + (((size_t)b * H + head) * LL + pos) * HD + dim) =
-            *reinterpret_cast<const uint4*>(blk + r * 64 + 16 * q);
-      }
-    } else {
-      const int rel = vb - nq - nkv;
-      const int head = rel / HD, cj0 = rel % HD;
-      constexpr int RC = TL::BM / 8;  // 8-row chunks per column
-      for (int it = tid; it < 32 * RC; it += TL::NTH) {
-        const int c = it / RC, t = it - c * RC, m = m0 + 8 * t;
-        if (m >= g.M) continue;
-        const uint4 val = *reinterpret_cast<const uint4*>(blk + c * St::VROW + 16 * t);
-        if (((g.L | g.Lq | g.pos0) & 7) == 0 && m + 7 < g.M) {
-          // eight positions of one sequence, 16-byte aligned (L, Lq, pos0 and m
-          // multiples of 8)
-          const int2 bp = seq_pos(m, g.Lq, inv_l);
-          const int b = bp.x, pos = g.pos0 + bp.y;
-          *reinterpret_cast<uint4*>(g.vt + (((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos) = val;
-        } else {
-          const uint32_t wd[4] = {val.x, val.y, val.z, val.w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int mm = m + e;
-            if (mm >= g.M) break;
-            const int2 bp = seq_pos(mm, g.Lq, inv_l);
-            const int b = bp.x, pos = g.pos0 + bp.y;
-            g.vt[(((size_t)b * g.Hkv + head) * HD + cj0 + c) * g.L + pos] = (f16_t)(wd[e >> 1] >> (16 * (e & 1)));
-          }
-        }
-      }
-    }
-  }
+  staged_store<TL::BM, TL::BN, TL::NTH, EPI>(g, lds, m0, n0);
 }
 
 // Writes the finished tile at (m0, n0) from the accumulators.
@@ -1184,19 +1197,22 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
     }
     wait_vm_lds<0>();
     barrier_nofence();
-    if (kg == 1) return;
+    // the second group joins the staged epilogues' barriers and stores
+    if (kg == 1 && EPI == EPI_RESID) return;
+    if (kg == 0) {
 #pragma unroll
-    for (int j = 0; j < TJ; ++j)
+      for (int j = 0; j < TJ; ++j)
 #pragma unroll
-      for (int ii = 0; ii < TI; ++ii)
+        for (int ii = 0; ii < TI; ++ii)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 v = xa[((j * TI + ii) * 4 + q) * 64];
-          acc[j][ii][4 * q] += v.x;
-          acc[j][ii][4 * q + 1] += v.y;
-          acc[j][ii][4 * q + 2] += v.z;
-          acc[j][ii][4 * q + 3] += v.w;
-        }
+          for (int q = 0; q < 4; ++q) {
+            const float4 v = xa[((j * TI + ii) * 4 + q) * 64];
+            acc[j][ii][4 * q] += v.x;
+            acc[j][ii][4 * q + 1] += v.y;
+            acc[j][ii][4 * q + 2] += v.z;
+            acc[j][ii][4 * q + 3] += v.w;
+          }
+    }
   }
 
   // Epilogue.  Lane l holds, for token row m = m0 + 32 ii + l % 32 and group G,
@@ -1205,73 +1221,93 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
   const int nq = g.Hq * HD, nkv = g.Hkv * HD;
   const float inv_l = 1.0f / (float)g.Lq;
   bool v_over = false;
+  if (EPI == EPI_SWIGLU || EPI == EPI_QKV_ROPE) {
+    // 16-bit outputs go through LDS (the ring is idle) in the destination's
+    // order and leave as 16-byte stores of the whole workgroup (StageGeo, as
+    // in the LDS-staged kernel); written from the MFMA layout they were
+    // 8-byte pieces of 32 rows per instruction, and v^T 2-byte stores
+    using St = StageGeo<TL::BM, TL::BN>;
+    static_assert((EPI == EPI_SWIGLU ? St::SW_BYTES : St::QKV_BYTES) <= (int)TL::LDS_BYTES, "staging fits the ring");
+    wait_vm_lds<0>();
+    barrier_nofence();  // every wave is done reading the ring (and the k-group merge area)
+    if (kg == 0) {
+#pragma unroll
+      for (int ii = 0; ii < TI; ++ii) {
+        const int ml = 32 * ii + lrow, m = m0 + ml;  // rows past M are never staged nor stored
+        if (m >= g.M) continue;
+        int p = 0;
+        if (EPI == EPI_QKV_ROPE) p = seq_pos(m, g.Lq, inv_l).y;
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+          const int jb = wn * TJ + j, G = n0 / 32 + jb;
+          const f32x16_t& a = acc[j][ii];
+          char* blk = lds + jb * St::BLK;
+          if (EPI == EPI_SWIGLU) {
+            // registers 0..7: gate of tile column 16 jb + 8 (r / 4) + 4 (l / 32) + r % 4, r + 8: its up
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+              float o[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float gt = a[4 * q + e], up = a[4 * q + 8 + e];
+                o[e] = __fdividef(gt, 1.0f + __expf(-gt)) * up;
+              }
+              *reinterpret_cast<uint2*>(lds + ml * St::SW_ROW + (16 * jb + 8 * q + 4 * lhalf) * 2) =
+                  make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+            }
+          } else if (32 * G < nq + nkv) {
+            // q or k: registers 0..7 dimension d = 16 blk + 8 (r / 4) + 4 (l / 32) + r % 4 of the
+            // head, r + 8: d + 64; the block's row holds d0 .. d0 + 15, then d0 + 64 .. d0 + 79
+            const int rel = 32 * G < nq ? 32 * G : 32 * G - nq, bk = (rel % HD) >> 5, pos = g.pos0 + p;
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+              const int d = 16 * bk + 8 * q + 4 * lhalf;
+              const float4 c4 = *reinterpret_cast<const float4*>(g.cosb + (size_t)pos * HALF + d);
+              const float4 s4 = *reinterpret_cast<const float4*>(g.sinb + (size_t)pos * HALF + d);
+              const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, ss[4] = {s4.x, s4.y, s4.z, s4.w};
+              float lo[4], hi[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float x1 = a[4 * q + e], x2 = a[4 * q + 8 + e];
+                lo[e] = x1 * cc[e] - x2 * ss[e];
+                hi[e] = x2 * cc[e] + x1 * ss[e];
+              }
+              *reinterpret_cast<uint2*>(blk + ml * 64 + (8 * q + 4 * lhalf) * 2) =
+                  make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+              *reinterpret_cast<uint2*>(blk + ml * 64 + (16 + 8 * q + 4 * lhalf) * 2) =
+                  make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
+            }
+          } else {
+            // v: register r is channel 8 (r / 4) + 4 (l / 32) + r % 4 of the block, staged as v^T
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              *reinterpret_cast<f16_t*>(blk + (8 * (r >> 2) + 4 * lhalf + (r & 3)) * St::VROW + ml * 2) =
+                  v_half(a[r], v_over);
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+    barrier_nofence();
+    staged_store<TL::BM, TL::BN, TL::NTH, EPI>(g, lds, m0, n0);
+    if (EPI == EPI_QKV_ROPE && v_over && g.err) atomicOr(g.err, (int)ERR_V_RANGE);
+    return;
+  }
+  // residual projections: float32 results straight from the MFMA layout
 #pragma unroll
   for (int ii = 0; ii < TI; ++ii) {
     const int m = m0 + 32 * ii + lrow;
     if (m >= g.M) continue;
-    int b = 0, p = 0;
-    if (EPI == EPI_QKV_ROPE) {
-      const int2 bp = seq_pos(m, g.Lq, inv_l);
-      b = bp.x;
-      p = bp.y;
-    }
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
       const int G = n0 / 32 + wn * TJ + j;
       const f32x16_t& a = acc[j][ii];
-      if (EPI == EPI_SWIGLU) {
-        // registers 0..7: gate of f = 16 G + 8 (r / 4) + 4 (l / 32) + r % 4, r + 8: up of the same f
-        const int F = g.N / 2;
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          float o[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float gt = a[4 * q + e], up = a[4 * q + 8 + e];
-            o[e] = __fdividef(gt, 1.0f + __expf(-gt)) * up;
-          }
-          *reinterpret_cast<uint2*>(g.out + (size_t)m * F + 16 * G + 8 * q + 4 * lhalf) =
-              make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
-        }
-      } else if (EPI == EPI_QKV_ROPE) {
-        const int vb = 32 * G;
-        if (vb < nq + nkv) {
-          // registers 0..7: dimension d = 16 blk + 8 (r / 4) + 4 (l / 32) + r % 4
-          // of the head, r + 8: d + 64
-          const bool isq = vb < nq;
-          const int rel = isq ? vb : vb - nq, head = rel / HD, blk = (rel % HD) >> 5;
-          const int pos = g.pos0 + p;
-          bf16_t* dst = isq ? g.q + (((size_t)b * g.Hq + head) * g.Lq + p) * HD
-                            : g.k + (((size_t)b * g.Hkv + head) * g.L + pos) * HD;
-#pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            const int d = 16 * blk + 8 * q + 4 * lhalf;
-            const float4 c4 = *reinterpret_cast<const float4*>(g.cosb + (size_t)pos * HALF + d);
-            const float4 s4 = *reinterpret_cast<const float4*>(g.sinb + (size_t)pos * HALF + d);
-            const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, ss[4] = {s4.x, s4.y, s4.z, s4.w};
-            float lo[4], hi[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float x1 = a[4 * q + e], x2 = a[4 * q + 8 + e];
-              lo[e] = x1 * cc[e] - x2 * ss[e];
-              hi[e] = x2 * cc[e] + x1 * ss[e];
-            }
-            *reinterpret_cast<uint2*>(dst + d) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
-            *reinterpret_cast<uint2*>(dst + d + HALF) =
-                make_uint2(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
-          }
-        } else {
-          const int rel = vb - nq - nkv, head = rel / HD, cj0 = rel % HD;
-          f16_t* dst = g.vt + (((size_t)b * g.Hkv + head) * HD + cj0) * g.L + g.pos0 + p;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) dst[(size_t)(8 * (r >> 2) + 4 * lhalf + (r & 3)) * g.L] = v_half(a[r], v_over);
-        }
-      } else if (S > 1) {  // EPI_RESID split over K: partial z [M, N] float32, summed in z order later
+      if (S > 1) {  // split over K: partial z [M, N] float32, summed in z order later
         float* part = g.splitk_buf + (size_t)z * g.M * g.N + (size_t)m * g.N + 32 * G + 4 * lhalf;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           *reinterpret_cast<float4*>(part + 8 * q) = make_float4(a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]);
-      } else {  // EPI_RESID: h[m, n] += result, n = 32 G + 8 q + 4 (l / 32) + e
+      } else {  // h[m, n] += result, n = 32 G + 8 q + 4 (l / 32) + e
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           float4* hp = reinterpret_cast<float4*>(g.resid + (size_t)m * g.N + 32 * G + 8 * q + 4 * lhalf);
@@ -1285,7 +1321,6 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
       }
     }
   }
-  if (EPI == EPI_QKV_ROPE && v_over && g.err) atomicOr(g.err, (int)ERR_V_RANGE);
 #endif
 }
 

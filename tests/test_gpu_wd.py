@@ -10,6 +10,8 @@ N = 12288 (128 x 192 tiles in two k-groups: 64 column tiles), gate/up N =
     loaded clamped and never stored);
   * M = 400, two sequences of 200: row tiles straddle the sequence boundary
     (the epilogue's row -> (sequence, position) mapping for q/k/v^T);
+  * M = 394, two sequences of 197: as above with L not a multiple of 8, so
+    the staged v^T leaves by single positions instead of 16-byte chunks;
   * M = 512: the batch-1 decode shape.
 Every stage is checked against the oracle on the GPU's own stage inputs (the
 bars of gpu_stages), and the fused forward against per-layer calls (bitwise).
@@ -41,7 +43,7 @@ def wide_mha():
     model.close()
 
 
-@pytest.mark.parametrize("Bn,P,G", [(1, 336, 64), (2, 136, 64), (1, 448, 64)])
+@pytest.mark.parametrize("Bn,P,G", [(1, 336, 64), (2, 136, 64), (2, 133, 64), (1, 448, 64)])
 def test_wd_stages(wide_mha, Bn, P, G):
     model, wnp = wide_mha
     L = P + G
