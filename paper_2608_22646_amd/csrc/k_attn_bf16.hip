@@ -633,9 +633,78 @@ __global__ void __launch_bounds__(64 * QG * KGRP, 1) attn_kv4_kernel(const bf16_
   }
 
   // merge the four key groups of each query group in group order (the ring
-  // is idle once every wave has passed the barrier): groups 1..3 leave their
-  // 64 floats of o as 16 lane-contiguous float4 rows, then (m, l)
+  // is idle once every wave has passed the barrier)
   __syncthreads();
+  if (QG <= 2) {
+    // every wave leaves its 64 floats of o as 16 lane-contiguous float4 rows,
+    // then (m, l); wave (qg, kg) then finishes output dimensions 32 kg .. of
+    // query group qg (the same operations, in the same order, as a merge by
+    // one wave per query group), stages them as bf16 rows and the workgroup
+    // stores whole 256-byte rows
+    constexpr int SLOT = 17 * 64;                       // float4s per wave
+    constexpr int OPK = 272;                            // staged row pitch (bytes)
+    char* stg = lds + (size_t)NW * SLOT * 16;           // [QG * 32][OPK]
+    float4* xo = reinterpret_cast<float4*>(lds) + (size_t)wave * SLOT + lane;
+#pragma unroll
+    for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq)
+        xo[(ds * 4 + rq) * 64] = make_float4(o[ds][4 * rq], o[ds][4 * rq + 1], o[ds][4 * rq + 2], o[ds][4 * rq + 3]);
+    xo[16 * 64] = make_float4(m_run, l_run, 0.f, 0.f);
+    __syncthreads();
+    const float4* x4 = reinterpret_cast<const float4*>(lds) + lane;
+    float me[KGRP], le[KGRP], m = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < KGRP; ++e) {
+      const float4 ml = x4[(size_t)(qg + QG * e) * SLOT + 16 * 64];
+      me[e] = ml.x;
+      le[e] = ml.y;
+      m = fmaxf(m, ml.x);
+    }
+    float acc[16], l_lane = 0.f;
+#pragma unroll
+    for (int e = 0; e < KGRP; ++e) {
+      // a group that saw no key (m = -inf) contributes nothing
+      const float ae = me[e] == -INFINITY ? 0.f : exp2_hw(me[e] - m);
+      const float4* xe = x4 + (size_t)(qg + QG * e) * SLOT + kg * 4 * 64;
+      l_lane = e == 0 ? le[e] * ae : fmaf(le[e], ae, l_lane);
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const float4 v = xe[rq * 64];
+        if (e == 0) {
+          acc[4 * rq] = v.x * ae;
+          acc[4 * rq + 1] = v.y * ae;
+          acc[4 * rq + 2] = v.z * ae;
+          acc[4 * rq + 3] = v.w * ae;
+        } else {
+          acc[4 * rq] += v.x * ae;
+          acc[4 * rq + 1] += v.y * ae;
+          acc[4 * rq + 2] += v.z * ae;
+          acc[4 * rq + 3] += v.w * ae;
+        }
+      }
+    }
+    const float inv = 1.0f / sum_pair32(l_lane);
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      const int d = kg * 32 + 8 * rg + 4 * half;
+      uint2 w;
+      w.x = pack_bf16x2(acc[rg * 4 + 0] * inv, acc[rg * 4 + 1] * inv);
+      w.y = pack_bf16x2(acc[rg * 4 + 2] * inv, acc[rg * 4 + 3] * inv);
+      *reinterpret_cast<uint2*>(stg + (qg * QW + lq) * OPK + d * 2) = w;
+    }
+    __syncthreads();
+    const int qb0 = wb.x * (QW * QG);
+    for (int it = tid; it < QG * QW * 16; it += NW * 64) {
+      const int row = it >> 4, ch = it & 15, qi = qb0 + row;
+      if (qi < Lq)
+        *reinterpret_cast<uint4*>(out + ((size_t)b * Lq + qi) * ((size_t)Hq * HD) + (size_t)h * HD + ch * 8) =
+            *reinterpret_cast<const uint4*>(stg + row * OPK + ch * 16);
+    }
+    return;
+  }
+  // three query groups: groups 1..3 leave their 64 floats of o as 16
+  // lane-contiguous float4 rows, then (m, l), for group 0 to merge
   constexpr int XW = 17 * 64 * 4;  // floats per handed-over wave
   if (kg > 0) {
     float4* xo = reinterpret_cast<float4*>(lds) + (size_t)(wave - QG) * (XW / 4) + lane;
@@ -1019,7 +1088,11 @@ void launch_attn_bf16(const bf16_t* q, const bf16_t* k, const f16_t* vt, bf16_t*
       // still fits the CUs, else 96
       auto go = [&](auto qgc) {
         constexpr int QG = decltype(qgc)::value;
-        constexpr size_t ring = 2 * (size_t)STEP2, merge = (size_t)3 * QG * 17 * 64 * 16;
+        // merge: every wave's state and the staged rows (up to 64 queries), or
+        // the three handed-over groups' states (96)
+        constexpr size_t ring = 2 * (size_t)STEP2,
+                         merge = QG <= 2 ? (size_t)QG * KGRP * 17 * 64 * 16 + (size_t)QG * QW * 272
+                                         : (size_t)3 * QG * 17 * 64 * 16;
         constexpr size_t lds_kv = ring > merge ? ring : merge;
         static const hipError_t a = hipFuncSetAttribute((const void*)attn_kv4_kernel<QG>,
                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_kv);
