@@ -1012,6 +1012,10 @@ using WdKg2 = WdTile<4, 3, 2, 2, 4, 8>;
 // changed nothing, 85.8 / 60.4 us either way)
 using WdRes = WdTile<4, 2, 4, 2, 4, 8, 2>;
 using WdRes2 = WdTile<4, 2, 2, 2, 4, 8, 2>;
+// q/k/v or gate/up launches whose 128 x 192 tiles would leave most CUs idle
+// (Dream-7B shape at 768 rows: N = 4608, 216 tiles of 128 x 128 where 128 x
+// 192 makes 144): 128 x 128 in two k-groups
+using WdQ2 = WdTile<4, 2, 2, 2, 4, 8>;
 
 template <class TL, int EPI>
 __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
@@ -1325,7 +1329,7 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
 }
 
 // Register-direct-weight plan for a launch of 129 .. 1024 rows with the packed
-// copy (tile 0: none, 1: WdWide, 2: WdKg2, 3: WdRes, 4: WdRes2; split over K),
+// copy (tile 0: none, 1: WdWide, 2: WdKg2, 3: WdRes, 4: WdRes2, 5: WdQ2; split over K),
 // taken when the tile's workgroups fill at least 7/8 of the rounds they take
 // on the compute units.  At these sizes a workgroup is bounded by the bytes
 // its CU pulls through the vector-memory path, (BM + BN) x its k-range x 2
@@ -1346,10 +1350,10 @@ WdPlan wd_plan(int M, int N, int K, int epi) {
   const int nk = K / 64;
   const long cus = device_cu_count();
   double best_t = 1e30;
-  auto consider = [&](int id, int BM, int BN, int KSTEPS, int R, int split) {
+  auto consider = [&](int id, int BM, int BN, int KSTEPS, int R, int split, bool one_round = false) {
     if (N % BN != 0 || nk % (KSTEPS * split) != 0 || (nk / KSTEPS / split) % R != 0) return;
     const long T = (long)((M + BM - 1) / BM) * (N / BN) * split, rounds = (T + cus - 1) / cus;
-    if (8 * T < 7 * rounds * cus) return;
+    if (one_round ? (rounds > 1 || 4 * T < 3 * cus) : 8 * T < 7 * rounds * cus) return;
     double t = (double)rounds * (20.4e-6 * (BM + BN) * (double)(K / split) * 2 + 5.0);
     if (split > 1) t += 1.5 * split * (double)M * N / (1 << 21);
     if (t < best_t - 1e-9) {
@@ -1360,6 +1364,10 @@ WdPlan wd_plan(int M, int N, int K, int epi) {
   if (epi == EPI_SWIGLU || epi == EPI_QKV_ROPE) {
     consider(1, WdWide::BM, WdWide::BN, WdWide::KSTEPS, WdWide::R, 1);
     consider(2, WdKg2::BM, WdKg2::BN, WdKg2::KSTEPS, WdKg2::R, 1);
+    // 128 x 128 when its tiles take one round on at least three quarters of
+    // the CUs: the LDS-staged tiles fill no more of them at these widths (over
+    // several rounds the wider LDS-staged tiles pull fewer bytes per CU)
+    consider(5, WdQ2::BM, WdQ2::BN, WdQ2::KSTEPS, WdQ2::R, 1, true);
   } else if (epi == EPI_RESID) {
     // only splits of at least 2048 k: the output projection at 512 rows (K =
     // 4096, split 4) ran 27 us + 9.9 us for its partials in the norm against
@@ -1577,6 +1585,8 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
       a.epi == EPI_SWIGLU ? launch_wd_tile<WdWide, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdWide, EPI_QKV_ROPE>(a, 1, s);
     else if (wp.tile == 2)
       a.epi == EPI_SWIGLU ? launch_wd_tile<WdKg2, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdKg2, EPI_QKV_ROPE>(a, 1, s);
+    else if (wp.tile == 5)
+      a.epi == EPI_SWIGLU ? launch_wd_tile<WdQ2, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdQ2, EPI_QKV_ROPE>(a, 1, s);
     else if (wp.tile == 3)
       launch_wd_tile<WdRes, EPI_RESID>(a, wp.split, s);
     else

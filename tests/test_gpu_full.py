@@ -67,10 +67,11 @@ def check_invariants(st, forwards, P, G, bl, T, mask_id, ctl):
             assert cs[b, blk * bl:(blk + 1) * bl].max() + 1 <= forwards[blk]
 
 
-@pytest.mark.parametrize("name,packed", [(n, False) for n in WORKLOADS] + [("llada_b1", True)])
+@pytest.mark.parametrize("name,packed", [(n, False) for n in WORKLOADS] + [("llada_b1", True), ("dream_b1", True)])
 def test_full_size_stages_and_head(models, name, packed):
     """packed: a second handle on the same weights with the packed copies, so
-    the batch-1 q/k/v and gate/up GEMMs stream their weights register-direct."""
+    the batch-1 q/k/v and gate/up GEMMs (LLaDA-8B shape) and the q/k/v GEMM
+    (Dream-7B shape, 128 x 128 tiles) stream their weights register-direct."""
     wl = synth.WORKLOADS[name]
     cfg = wl.model
     w, model = models(cfg)
