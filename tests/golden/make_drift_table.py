@@ -1,5 +1,6 @@
-"""Writes tests/golden/bf16_drift_llada.json: how far the oracle's own bf16 forward
-moves between float32 and float64 accumulation, by depth, at the LLaDA-8B shape.
+"""Writes tests/golden/bf16_drift_llada.json (bf16_drift_dream.json with
+--workload dream_b1): how far the oracle's own bf16 forward moves between
+float32 and float64 accumulation, by depth, at the LLaDA-8B (Dream-7B) shape.
 
 A bf16 model rounds every matrix-product operand to bf16 (the oracle's "bf16"
 mode).  Two correct implementations whose float32 sums differ in the last bit
@@ -10,13 +11,15 @@ the same model and input through mode "bf16" (float32 products) and mode
 confidences (Box 1) compared after 1, 2, 4, 8, 16 and 32 layers.  The GPU's
 end-to-end bar is derived from this table.
 
-Input: the LLaDA-8B-shaped model with weights drawn by torch's CPU generator
+Input: the workload's model with weights drawn by torch's CPU generator
 (seed 1234 + tensor index; the GPU tests draw theirs with the GPU generator, a
-different stream of the same distribution), prompt set 0 (256 tokens) followed
-by 256 mask tokens, the head on the first generated block (32 rows).  Calls
-only oracle/ and the seeded input generators.
+different stream of the same distribution), its prompt set 0 followed by its
+generation length of mask tokens (LLaDA-8B: 256 + 256; Dream-7B: 512 + 256),
+the head on the first generated block (32 rows).  Calls only oracle/ and the
+seeded input generators.
 
-  python tests/golden/make_drift_table.py [--depths 1,2,4,8,16,32]
+  python tests/golden/make_drift_table.py [--workload llada_b1] [--depths 1,2,4,8,16,32]
+  python tests/golden/make_drift_table.py --workload dream_b1 --depths 1,2,4,8,16,28
 """
 import argparse
 import json
@@ -34,12 +37,14 @@ from oracle import forward as of  # noqa: E402
 from oracle import vocab as ov  # noqa: E402
 from paper_2608_22646_amd import synth  # noqa: E402
 
-OUT = os.path.join(HERE, "bf16_drift_llada.json")
+OUTS = {"llada_b1": os.path.join(HERE, "bf16_drift_llada.json"),
+        "dream_b1": os.path.join(HERE, "bf16_drift_dream.json")}
+OUT = OUTS["llada_b1"]
 MODES = ("bf16", "bf16_f64acc")
 
 
-def drift(depths, log=print):
-    wl = synth.WORKLOADS["llada_b1"]
+def drift(depths, log=print, workload="llada_b1"):
+    wl = synth.WORKLOADS[workload]
     cfg = wl.model
     P, G, bl = wl.prompt_len, wl.gen_len, wl.block_len
     L = P + G
@@ -83,20 +88,24 @@ def drift(depths, log=print):
 
 def main():
     ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", default="llada_b1", choices=sorted(OUTS))
     ap.add_argument("--depths", default="1,2,4,8,16,32")
     a = ap.parse_args()
     depths = sorted({int(v) for v in a.depths.split(",")})
-    table = drift(depths, log=lambda s: print(s, flush=True))
+    table = drift(depths, log=lambda s: print(s, flush=True), workload=a.workload)
+    wl = synth.WORKLOADS[a.workload]
+    shape = {"llada_b1": "LLaDA-8B", "dream_b1": "Dream-7B"}[a.workload]
     doc = {
         "what": ("max |difference| between the oracle's bf16-model forward with float32 and with float64 "
-                 "accumulation (same bf16 rounding points), LLaDA-8B shape, prompt set 0 + 256 masks, "
+                 f"accumulation (same bf16 rounding points), {shape} shape, prompt set 0 + {wl.gen_len} masks, "
                  "first block's 32 rows; logits exclude the mask column"),
-        "generator": "tests/golden/make_drift_table.py",
+        "generator": "tests/golden/make_drift_table.py" + ("" if a.workload == "llada_b1" else
+                                                            f" --workload {a.workload}"),
         "rows": table,
     }
-    with open(OUT, "w") as f:
+    with open(OUTS[a.workload], "w") as f:
         json.dump(doc, f, indent=1)
-    print(OUT)
+    print(OUTS[a.workload])
 
 
 if __name__ == "__main__":

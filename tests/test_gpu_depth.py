@@ -1,12 +1,14 @@
-"""End-to-end bf16 parity by depth: the LLaDA-8B-shaped forward on the GPU
-against the oracle's bf16 forward (float32 products), logits and confidences of
-the first block (Box 1), teacher-forced on the workload's first input (prompt
-set 0 + 256 masks), after 1, 2, 4, 8, 16 and 32 layers.
+"""End-to-end bf16 parity by depth: the LLaDA-8B- and Dream-7B-shaped forwards
+on the GPU against the oracle's bf16 forward (float32 products), logits and
+confidences of the first block (Box 1), teacher-forced on the workload's first
+input (prompt set 0 + the generation length of masks), after 1, 2, 4, 8, 16
+layers and the last (32 / 28).
 
 Two correct float32 accumulation orders of a bf16 model drift apart by bf16
 rounding flips that later layers carry forward; the oracle's own float32 and
-float64 runs of this model and input differ by the amounts in
-tests/golden/bf16_drift_llada.json.  The bars are derived from that table: the
+float64 runs of each model and input differ by the amounts in
+tests/golden/bf16_drift_llada.json and bf16_drift_dream.json (written by
+make_drift_table.py from the oracle alone).  The bars are derived from that table: the
 GPU may differ from the float32 oracle by at most twice the oracle's own
 spread at that depth (logits), and by at most 2e-2 or twice the table's
 spread, whichever is larger (confidences).  An argmax may differ only where
@@ -28,21 +30,28 @@ from paper_2608_22646_amd import synth
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-DRIFT = {r["depth"]: r for r in json.load(open(os.path.join(HERE, "golden", "bf16_drift_llada.json")))["rows"]}
-DEPTHS = (1, 2, 4, 8, 16, 32)
+CASES = {"llada_b1": ("bf16_drift_llada.json", (1, 2, 4, 8, 16, 32)),
+         "dream_b1": ("bf16_drift_dream.json", (1, 2, 4, 8, 16, 28))}
 
 
-def bars(depth):
-    r = DRIFT[depth]
+def drift_table(name):
+    path = os.path.join(HERE, "golden", CASES[name][0])
+    return {r["depth"]: r for r in json.load(open(path))["rows"]}
+
+
+def bars(drift, depth):
+    r = drift[depth]
     return 2.0 * r["logit_max_abs_diff"], max(2e-2, 2.0 * r["conf_max_abs_diff"])
 
 
-def test_llada_forward_against_oracle_by_depth():
-    wl = synth.WORKLOADS["llada_b1"]
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_forward_against_oracle_by_depth(name):
+    drift, DEPTHS = drift_table(name), CASES[name][1]
+    wl = synth.WORKLOADS[name]
     cfg = wl.model
     P, G, bl = wl.prompt_len, wl.gen_len, wl.block_len
     L = P + G
-    say("llada_b1 depth parity: weights")
+    say(f"{name} depth parity: weights")
     w = synth.make_weights(cfg, "cuda")
     model = B.Model(cfg, w)
     x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((1, G), cfg.mask_id)], axis=1)
@@ -65,7 +74,7 @@ def test_llada_forward_against_oracle_by_depth():
         depth = l + 1
         if depth not in DEPTHS:
             continue
-        say(f"llada_b1 depth {depth}: head")
+        say(f"{name} depth {depth}: head")
         conf_g, arg_g, lg_g = model.head(1, L, P, bl, ws, logits=True)
         torch.cuda.synchronize()
         lg_ref, _ = of.lm_head(cfg, h[0, rows, :], final_norm, lm, "bf16")
@@ -74,7 +83,7 @@ def test_llada_forward_against_oracle_by_depth():
         err = np.abs(lg - lg_ref)
         err[:, cfg.mask_id] = 0
         cerr = np.abs(to_np(conf_g[0], np.float64) - conf_ref).max()
-        bar_l, bar_c = bars(depth)
+        bar_l, bar_c = bars(drift, depth)
         diff = arg_g[0].cpu().numpy() != arg_ref
         gap = ov.top2_gap(lg_ref, cfg.mask_id)
         rec = dict(depth=depth, logit_err=float(err.max()), logit_bar=bar_l, conf_err=float(cerr), conf_bar=bar_c,
