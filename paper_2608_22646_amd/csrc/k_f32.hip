@@ -3,62 +3,74 @@
 // storage but accumulate products and softmax sums in float64 (cheap at these
 // sizes), so each stored value is the float32 rounding of a nearly exact
 // result; fixed reduction order everywhere, so results are run-to-run identical.
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace dllm {
 
-// C[M, N] (+)= A[M, K] W[N, K]^T (C row stride ldc).  64x64 tile, BK = 16, 256 threads, 4x4 per thread.
+// C[M, N] (+)= A[M, K] W[N, K]^T (C row stride ldc).  One 16 x 16 output tile
+// per workgroup of 256 threads, one output per thread: the tile's 16 rows of A
+// and of W are staged in LDS for a chunk of up to GF_KC k at once (each thread
+// issues all its loads of the chunk before it writes any to LDS, so the chunk
+// costs one memory latency), then each thread continues its float64 dot
+// product over the chunk in k order.  At the fp32 models' sizes (a few hundred
+// rows) this puts 6-12x more workgroups on the CUs than 64 x 64 tiles.
+constexpr int GF_T = 16, GF_KC = 512, GF_PER = GF_KC / 256;
 __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ A, const float* __restrict__ W,
                                                        float* __restrict__ C, int M, int N, int K, int ldc,
                                                        int accumulate) {
-  __shared__ float As[16][64 + 4];
-  __shared__ float Ws[16][64 + 4];
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
-  double acc[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += 16) {
-    // 64 rows x 16 k of A and W: each thread loads 4 of each
-    for (int e = threadIdx.x; e < 64 * 16; e += 256) {
-      const int r = e / 16, kk = e % 16;
-      const int gm = m0 + r, gn = n0 + r, gk = k0 + kk;
-      As[kk][r] = (gm < M && gk < K) ? A[(size_t)gm * K + gk] : 0.f;
-      Ws[kk][r] = (gn < N && gk < K) ? W[(size_t)gn * K + gk] : 0.f;
-    }
-    __syncthreads();
+  extern __shared__ float gf_lds[];
+  const int m0 = blockIdx.y * GF_T, n0 = blockIdx.x * GF_T;
+  const int tr = threadIdx.x / GF_T, tc = threadIdx.x % GF_T;
+  double acc = 0.0;
+  for (int k0 = 0; k0 < K; k0 += GF_KC) {
+    const int kc = min(GF_KC, K - k0), kp = kc + 1;  // odd row pitch: the 16 W rows a k step reads hit 16 banks
+    float* As = gf_lds;
+    float* Ws = gf_lds + GF_T * kp;
+    float ra[GF_T][GF_PER], rw[GF_T][GF_PER];
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-      float a[4], w[4];
+    for (int r = 0; r < GF_T; ++r)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a[i] = As[kk][ty * 4 + i];
-        w[i] = Ws[kk][tx * 4 + i];
+      for (int j = 0; j < GF_PER; ++j) {
+        const int k = threadIdx.x + 256 * j;
+        ra[r][j] = (k < kc && m0 + r < M) ? A[(size_t)(m0 + r) * K + k0 + k] : 0.f;
+        rw[r][j] = (k < kc && n0 + r < N) ? W[(size_t)(n0 + r) * K + k0 + k] : 0.f;
       }
+    if (k0 > 0) __syncthreads();  // the previous chunk's reads are done
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int r = 0; r < GF_T; ++r)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fma((double)a[i], (double)w[j], acc[i][j]);
-    }
+      for (int j = 0; j < GF_PER; ++j) {
+        const int k = threadIdx.x + 256 * j;
+        if (k < kc) {
+          As[r * kp + k] = ra[r][j];
+          Ws[r * kp + k] = rw[r][j];
+        }
+      }
     __syncthreads();
+    const float* ar = As + tr * kp;
+    const float* wr = Ws + tc * kp;
+#pragma unroll 16
+    for (int k = 0; k < kc; ++k) acc = fma((double)ar[k], (double)wr[k], acc);
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int gm = m0 + ty * 4 + i;
-    if (gm >= M) continue;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gn = n0 + tx * 4 + j;
-      if (gn >= N) continue;
-      float* c = C + (size_t)gm * ldc + gn;
-      *c = accumulate ? (float)((double)*c + acc[i][j]) : (float)acc[i][j];
-    }
+  const int gm = m0 + tr, gn = n0 + tc;
+  if (gm < M && gn < N) {
+    float* c = C + (size_t)gm * ldc + gn;
+    *c = accumulate ? (float)((double)*c + acc) : (float)acc;
   }
 }
 
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc, bool accumulate,
                      hipStream_t s) {
   if (M == 0 || N == 0) return;
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3(ceil_div(N, 64), ceil_div(M, 64)), dim3(256), 0, s, A, W, C, M, N, K,
-                     ldc, (int)accumulate);
+  const size_t lds = (size_t)2 * GF_T * (std::min(K, GF_KC) + 1) * sizeof(float);
+  static const hipError_t attr = hipFuncSetAttribute((const void*)gemm_f32_kernel,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     (int)(2 * GF_T * (GF_KC + 1) * sizeof(float)));
+  hip_check(attr, "hipFuncSetAttribute(gemm_f32)");
+  hipLaunchKernelGGL(gemm_f32_kernel, dim3(ceil_div(N, GF_T), ceil_div(M, GF_T)), dim3(256), lds, s, A, W, C, M, N,
+                     K, ldc, (int)accumulate);
   DLLM_LAUNCH_CHECK("gemm_f32");
 }
 
