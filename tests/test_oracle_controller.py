@@ -54,6 +54,16 @@ def test_cosine_schedule_closed_form_properties(T, b):
     assert all(te <= x <= 0.90 for x in th)
 
 
+@pytest.mark.parametrize("b,t,expect", [(1, 8, 0.89325), (1, 16, 0.82737), (1, 24, 0.73974), (1, 31, 0.70067),
+                                         (4, 16, 0.71842), (4, 31, 0.40167)])
+def test_cosine_schedule_hand_values(b, t, expect):
+    # Box 3 at T = 32, w = 0.15 (wT = 4.8): theta = theta_e + (theta_s - theta_e)(1 + cos(pi u)) / 2 with
+    # u = (t - 4.8) / 27.2, worked by hand: t = 8 -> u = 0.11765, cos(pi u) = 0.93247; t = 16 -> 0.41176,
+    # 0.27366; t = 24 -> 0.70588, -0.60263; t = 31 -> 0.96324, -0.99334.  theta_e = 0.70 (b = 1), 0.40
+    # (b = 4, Box 4): 0.70 + 0.10 (1.93247) = 0.89325, ..., 0.40 + 0.25 (1.27366) = 0.71842.
+    assert oc.block_threshold(t, b, P0) == pytest.approx(expect, abs=6e-6)
+
+
 def test_position_factors_and_clip():
     # Box 6: r = 0.80 (p<16), 0.90 (16<=p<32), 1.05 (32<=p<48), 1.10 (p>=48)
     want = {0: 0.80, 15: 0.80, 16: 0.90, 31: 0.90, 32: 1.05, 47: 1.05, 48: 1.10, 63: 1.10}
