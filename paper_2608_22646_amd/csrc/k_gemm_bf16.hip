@@ -1016,6 +1016,11 @@ using WdRes2 = WdTile<4, 2, 2, 2, 4, 8, 2>;
 // (Dream-7B shape at 768 rows: N = 4608, 216 tiles of 128 x 128 where 128 x
 // 192 makes 144): 128 x 128 in two k-groups
 using WdQ2 = WdTile<4, 2, 2, 2, 4, 8>;
+// gate/up widths that no 192- or 384-wide tile divides (Dream-7B: N = 37888 =
+// 148 x 256): 256 x 256 on 4 waves of 256 x 64, one 64-k step per stage (the
+// four-stage ring takes 128 KiB of LDS); per flop a quarter fewer bytes per CU
+// than 128 x 384, and 256 registers of accumulators per lane
+using WdBig = WdTile<8, 2, 4, 1, 4, 8>;
 
 template <class TL, int EPI>
 __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
@@ -1350,10 +1355,12 @@ WdPlan wd_plan(int M, int N, int K, int epi) {
   const int nk = K / 64;
   const long cus = device_cu_count();
   double best_t = 1e30;
-  auto consider = [&](int id, int BM, int BN, int KSTEPS, int R, int split, bool one_round = false) {
+  // fill16: the least sixteenths of the rounds' workgroup slots the tiles must fill
+  auto consider = [&](int id, int BM, int BN, int KSTEPS, int R, int split, bool one_round = false,
+                      int fill16 = 14) {
     if (N % BN != 0 || nk % (KSTEPS * split) != 0 || (nk / KSTEPS / split) % R != 0) return;
     const long T = (long)((M + BM - 1) / BM) * (N / BN) * split, rounds = (T + cus - 1) / cus;
-    if (one_round ? (rounds > 1 || 4 * T < 3 * cus) : 8 * T < 7 * rounds * cus) return;
+    if (one_round ? (rounds > 1 || 4 * T < 3 * cus) : 16 * T < fill16 * rounds * cus) return;
     double t = (double)rounds * (20.4e-6 * (BM + BN) * (double)(K / split) * 2 + 5.0);
     if (split > 1) t += 1.5 * split * (double)M * N / (1 << 21);
     if (t < best_t - 1e-9) {
@@ -1363,6 +1370,9 @@ WdPlan wd_plan(int M, int N, int K, int epi) {
   };
   if (epi == EPI_SWIGLU || epi == EPI_QKV_ROPE) {
     consider(1, WdWide::BM, WdWide::BN, WdWide::KSTEPS, WdWide::R, 1);
+    // 256 x 256 also at 13/16 of its rounds' slots (Dream-7B gate/up at 768
+    // rows: 444 tiles), where no other register-direct tile divides N
+    if (epi == EPI_SWIGLU) consider(6, WdBig::BM, WdBig::BN, WdBig::KSTEPS, WdBig::R, 1, false, 13);
     consider(2, WdKg2::BM, WdKg2::BN, WdKg2::KSTEPS, WdKg2::R, 1);
     // 128 x 128 when its tiles take one round on at least three quarters of
     // the CUs: the LDS-staged tiles fill no more of them at these widths (over
@@ -1587,6 +1597,8 @@ void launch_gemm_bf16(const GemmArgs& a, hipStream_t s, PendingResid* defer) {
       a.epi == EPI_SWIGLU ? launch_wd_tile<WdKg2, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdKg2, EPI_QKV_ROPE>(a, 1, s);
     else if (wp.tile == 5)
       a.epi == EPI_SWIGLU ? launch_wd_tile<WdQ2, EPI_SWIGLU>(a, 1, s) : launch_wd_tile<WdQ2, EPI_QKV_ROPE>(a, 1, s);
+    else if (wp.tile == 6)
+      launch_wd_tile<WdBig, EPI_SWIGLU>(a, 1, s);
     else if (wp.tile == 3)
       launch_wd_tile<WdRes, EPI_RESID>(a, wp.split, s);
     else
