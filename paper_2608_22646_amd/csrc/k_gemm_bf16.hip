@@ -1230,7 +1230,7 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
   const int nq = g.Hq * HD, nkv = g.Hkv * HD;
   const float inv_l = 1.0f / (float)g.Lq;
   bool v_over = false;
-  if (EPI == EPI_SWIGLU || EPI == EPI_QKV_ROPE) {
+  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV_ROPE) {
     // 16-bit outputs go through LDS (the ring is idle) in the destination's
     // order and leave as 16-byte stores of the whole workgroup (StageGeo, as
     // in the LDS-staged kernel); written from the MFMA layout they were
