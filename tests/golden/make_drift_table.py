@@ -1,6 +1,7 @@
 """Writes tests/golden/bf16_drift_llada.json (bf16_drift_dream.json with
---workload dream_b1): how far the oracle's own bf16 forward moves between
-float32 and float64 accumulation, by depth, at the LLaDA-8B (Dream-7B) shape.
+--workload dream_b1, bf16_drift_llada_b8.json with --workload llada_b8): how
+far the oracle's own bf16 forward moves between float32 and float64
+accumulation, by depth, at the LLaDA-8B (Dream-7B) shape.
 
 A bf16 model rounds every matrix-product operand to bf16 (the oracle's "bf16"
 mode).  Two correct implementations whose float32 sums differ in the last bit
@@ -13,13 +14,16 @@ end-to-end bar is derived from this table.
 
 Input: the workload's model with weights drawn by torch's CPU generator
 (seed 1234 + tensor index; the GPU tests draw theirs with the GPU generator, a
-different stream of the same distribution), its prompt set 0 followed by its
-generation length of mask tokens (LLaDA-8B: 256 + 256; Dream-7B: 512 + 256),
-the head on the first generated block (32 rows).  Calls only oracle/ and the
-seeded input generators.
+different stream of the same distribution), one sequence of its prompt set 0
+(the first; sequence 5 of the eight for llada_b8) followed by its generation
+length of mask tokens (LLaDA-8B: 256 + 256, batch 8: 512 + 512; Dream-7B: 512 +
+256), the head on the first generated block (32 rows).  Sequences of a batch
+do not interact, so one sequence stands for the batch.  Calls only oracle/ and
+the seeded input generators.
 
   python tests/golden/make_drift_table.py [--workload llada_b1] [--depths 1,2,4,8,16,32]
   python tests/golden/make_drift_table.py --workload dream_b1 --depths 1,2,4,8,16,28
+  python tests/golden/make_drift_table.py --workload llada_b8
 """
 import argparse
 import json
@@ -38,7 +42,9 @@ from oracle import vocab as ov  # noqa: E402
 from paper_2608_22646_amd import synth  # noqa: E402
 
 OUTS = {"llada_b1": os.path.join(HERE, "bf16_drift_llada.json"),
-        "dream_b1": os.path.join(HERE, "bf16_drift_dream.json")}
+        "dream_b1": os.path.join(HERE, "bf16_drift_dream.json"),
+        "llada_b8": os.path.join(HERE, "bf16_drift_llada_b8.json")}
+SEQ = {"llada_b1": 0, "dream_b1": 0, "llada_b8": 5}  # the sequence of the batch the table follows
 OUT = OUTS["llada_b1"]
 MODES = ("bf16", "bf16_f64acc")
 
@@ -48,7 +54,9 @@ def drift(depths, log=print, workload="llada_b1"):
     cfg = wl.model
     P, G, bl = wl.prompt_len, wl.gen_len, wl.block_len
     L = P + G
-    x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((1, G), cfg.mask_id)], axis=1)
+    seq = SEQ[workload]
+    x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64)[seq:seq + 1], np.full((1, G), cfg.mask_id)],
+                       axis=1)
     host = lambda i: synth.make_weight(cfg, i).float().numpy()  # noqa: E731
     h0 = host(0)[x].astype(np.float64)
     h = {m: h0.copy() for m in MODES}
@@ -94,10 +102,11 @@ def main():
     depths = sorted({int(v) for v in a.depths.split(",")})
     table = drift(depths, log=lambda s: print(s, flush=True), workload=a.workload)
     wl = synth.WORKLOADS[a.workload]
-    shape = {"llada_b1": "LLaDA-8B", "dream_b1": "Dream-7B"}[a.workload]
+    shape = {"llada_b1": "LLaDA-8B", "dream_b1": "Dream-7B", "llada_b8": "LLaDA-8B"}[a.workload]
     doc = {
         "what": ("max |difference| between the oracle's bf16-model forward with float32 and with float64 "
-                 f"accumulation (same bf16 rounding points), {shape} shape, prompt set 0 + {wl.gen_len} masks, "
+                 f"accumulation (same bf16 rounding points), {shape} shape, sequence {SEQ[a.workload]} of prompt set 0 + "
+                 f"{wl.gen_len} masks, "
                  "first block's 32 rows; logits exclude the mask column"),
         "generator": "tests/golden/make_drift_table.py" + ("" if a.workload == "llada_b1" else
                                                             f" --workload {a.workload}"),

@@ -2,7 +2,10 @@
 on the GPU against the oracle's bf16 forward (float32 products), logits and
 confidences of the first block (Box 1), teacher-forced on the workload's first
 input (prompt set 0 + the generation length of masks), after 1, 2, 4, 8, 16
-layers and the last (32 / 28).
+layers and the last (32 / 28).  The batch-8 LLaDA-8B workload (8 x 1024
+tokens: the large-row GEMM tiles, batched attention and the many-row LM head)
+runs its whole batch on the GPU; the oracle follows its sequence 5 (sequences
+of a batch do not interact).
 
 Two correct float32 accumulation orders of a bf16 model drift apart by bf16
 rounding flips that later layers carry forward; the oracle's own float32 and
@@ -10,9 +13,13 @@ float64 runs of each model and input differ by the amounts in
 tests/golden/bf16_drift_llada.json and bf16_drift_dream.json (written by
 make_drift_table.py from the oracle alone).  The bars are derived from that table: the
 GPU may differ from the float32 oracle by at most twice the oracle's own
-spread at that depth (logits), and by at most 2e-2 or twice the table's
-spread, whichever is larger (confidences).  An argmax may differ only where
-the oracle's top-two logit gap is within twice the measured logit error.
+spread (logits), and by at most 2e-2 or twice the table's spread, whichever is
+larger (confidences), where the spread at a depth is the largest the table
+shows at that depth or any shallower one: rounding drift accumulates with
+depth, and the maximum over 32 rows at a single depth is one noisy extreme
+(the batch-8 table's confidence spread is 0.014 at depth 4 and 0.011 at 8).
+An argmax may differ only where the oracle's top-two logit gap is within twice
+the measured logit error.
 """
 import json
 import os
@@ -30,8 +37,9 @@ from paper_2608_22646_amd import synth
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-CASES = {"llada_b1": ("bf16_drift_llada.json", (1, 2, 4, 8, 16, 32)),
-         "dream_b1": ("bf16_drift_dream.json", (1, 2, 4, 8, 16, 28))}
+CASES = {"llada_b1": ("bf16_drift_llada.json", (1, 2, 4, 8, 16, 32), 0),
+         "dream_b1": ("bf16_drift_dream.json", (1, 2, 4, 8, 16, 28), 0),
+         "llada_b8": ("bf16_drift_llada_b8.json", (1, 2, 4, 8, 16, 32), 5)}
 
 
 def drift_table(name):
@@ -40,34 +48,36 @@ def drift_table(name):
 
 
 def bars(drift, depth):
-    r = drift[depth]
-    return 2.0 * r["logit_max_abs_diff"], max(2e-2, 2.0 * r["conf_max_abs_diff"])
+    rows = [r for d, r in drift.items() if d <= depth]
+    logit = max(r["logit_max_abs_diff"] for r in rows)
+    conf = max(r["conf_max_abs_diff"] for r in rows)
+    return 2.0 * logit, max(2e-2, 2.0 * conf)
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
 def test_forward_against_oracle_by_depth(name):
-    drift, DEPTHS = drift_table(name), CASES[name][1]
+    drift, DEPTHS, seq = drift_table(name), CASES[name][1], CASES[name][2]
     wl = synth.WORKLOADS[name]
     cfg = wl.model
-    P, G, bl = wl.prompt_len, wl.gen_len, wl.block_len
+    Bn, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
     L = P + G
     say(f"{name} depth parity: weights")
     w = synth.make_weights(cfg, "cuda")
     model = B.Model(cfg, w)
-    x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((1, G), cfg.mask_id)], axis=1)
-    ws = model.workspace(1, L, bl)
+    x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((Bn, G), cfg.mask_id)], axis=1)
+    ws = model.workspace(Bn, L, bl)
     # layer calls (rows 0) and head calls (rows bl) share h and the RoPE tables
-    l0, lb = model.layout(1, L, 0), model.layout(1, L, bl)
+    l0, lb = model.layout(Bn, L, 0), model.layout(Bn, L, bl)
     assert [getattr(l0, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")] == \
         [getattr(lb, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")]
     model.embed(torch.from_numpy(x.astype(np.int32)).cuda(), ws)
-    h = to_np(w[0], np.float32)[x].astype(np.float64)
+    h = to_np(w[0], np.float32)[x[seq:seq + 1]].astype(np.float64)
     cos, sin = of.rope_tables(L, cfg.head_dim, cfg.rope_base)
     final_norm, lm = to_np(w[-2]), to_np(w[-1])
     rows = np.arange(P, P + bl)
     report = []
     for l in range(cfg.n_layers):
-        model.layer(l, 2, 1, L, ws)
+        model.layer(l, 2, Bn, L, ws)
         lw = [to_np(t) for t in w[1 + 9 * l: 10 + 9 * l]]
         h = of.layer(cfg, lw, h, cos, sin, "bf16")
         del lw
@@ -75,16 +85,16 @@ def test_forward_against_oracle_by_depth(name):
         if depth not in DEPTHS:
             continue
         say(f"{name} depth {depth}: head")
-        conf_g, arg_g, lg_g = model.head(1, L, P, bl, ws, logits=True)
+        conf_g, arg_g, lg_g = model.head(Bn, L, P, bl, ws, logits=True)
         torch.cuda.synchronize()
         lg_ref, _ = of.lm_head(cfg, h[0, rows, :], final_norm, lm, "bf16")
         conf_ref, arg_ref = ov.confidence_argmax(lg_ref, cfg.mask_id)
-        lg = to_np(lg_g[0], np.float64)
+        lg = to_np(lg_g[seq], np.float64)
         err = np.abs(lg - lg_ref)
         err[:, cfg.mask_id] = 0
-        cerr = np.abs(to_np(conf_g[0], np.float64) - conf_ref).max()
+        cerr = np.abs(to_np(conf_g[seq], np.float64) - conf_ref).max()
         bar_l, bar_c = bars(drift, depth)
-        diff = arg_g[0].cpu().numpy() != arg_ref
+        diff = arg_g[seq].cpu().numpy() != arg_ref
         gap = ov.top2_gap(lg_ref, cfg.mask_id)
         rec = dict(depth=depth, logit_err=float(err.max()), logit_bar=bar_l, conf_err=float(cerr), conf_bar=bar_c,
                    argmax_diff=int(diff.sum()))
