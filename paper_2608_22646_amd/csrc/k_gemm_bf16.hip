@@ -1191,37 +1191,43 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
   wait_vm_lds<0>();
   barrier_nofence();  // the ring is idle
 
+  // With two k-groups the sum of the groups' accumulators is finished by
+  // group 0 for the residual epilogue; for the staged ones group 0 finishes
+  // row blocks ii < TI / 2 and group 1 the others (each hands the other its
+  // share through LDS), so all four waves stage.  Two addends: the same sum
+  // in either order.
+  constexpr bool SPLIT_ROWS = TL::KG == 2 && EPI != EPI_RESID && TI % 2 == 0;
+  auto own_rows = [&](int ii) { return !SPLIT_ROWS ? kg == 0 : (ii < TI / 2) == (kg == 0); };
   if (TL::KG == 2) {
-    // acc(group 0) += acc(group 1) through LDS, lane-contiguous float4s
     float4* xa = reinterpret_cast<float4*>(lds) + (size_t)wn * (TI * TJ * 4 * 64) + lane;
-    if (kg == 1) {
 #pragma unroll
-      for (int j = 0; j < TJ; ++j)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
-        for (int ii = 0; ii < TI; ++ii)
+      for (int ii = 0; ii < TI; ++ii) {
+        if (own_rows(ii) || (!SPLIT_ROWS && kg == 0)) continue;
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            xa[((j * TI + ii) * 4 + q) * 64] =
-                make_float4(acc[j][ii][4 * q], acc[j][ii][4 * q + 1], acc[j][ii][4 * q + 2], acc[j][ii][4 * q + 3]);
-    }
+        for (int q = 0; q < 4; ++q)
+          xa[((j * TI + ii) * 4 + q) * 64] =
+              make_float4(acc[j][ii][4 * q], acc[j][ii][4 * q + 1], acc[j][ii][4 * q + 2], acc[j][ii][4 * q + 3]);
+      }
     wait_vm_lds<0>();
     barrier_nofence();
     // the second group joins the staged epilogues' barriers and stores
     if (kg == 1 && EPI == EPI_RESID) return;
-    if (kg == 0) {
 #pragma unroll
-      for (int j = 0; j < TJ; ++j)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
-        for (int ii = 0; ii < TI; ++ii)
+      for (int ii = 0; ii < TI; ++ii) {
+        if (!own_rows(ii)) continue;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float4 v = xa[((j * TI + ii) * 4 + q) * 64];
-            acc[j][ii][4 * q] += v.x;
-            acc[j][ii][4 * q + 1] += v.y;
-            acc[j][ii][4 * q + 2] += v.z;
-            acc[j][ii][4 * q + 3] += v.w;
-          }
-    }
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = xa[((j * TI + ii) * 4 + q) * 64];
+          acc[j][ii][4 * q] += v.x;
+          acc[j][ii][4 * q + 1] += v.y;
+          acc[j][ii][4 * q + 2] += v.z;
+          acc[j][ii][4 * q + 3] += v.w;
+        }
+      }
   }
 
   // Epilogue.  Lane l holds, for token row m = m0 + 32 ii + l % 32 and group G,
@@ -1239,9 +1245,10 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
     static_assert((EPI == EPI_SWIGLU ? St::SW_BYTES : St::QKV_BYTES) <= (int)TL::LDS_BYTES, "staging fits the ring");
     wait_vm_lds<0>();
     barrier_nofence();  // every wave is done reading the ring (and the k-group merge area)
-    if (kg == 0) {
+    {
 #pragma unroll
       for (int ii = 0; ii < TI; ++ii) {
+        if (!own_rows(ii)) continue;
         const int ml = 32 * ii + lrow, m = m0 + ml;  // rows past M are never staged nor stored
         if (m >= g.M) continue;
         int p = 0;
