@@ -4,8 +4,16 @@
   python -m paper_2608_22646_amd.profsum traffic <fetch.csv> <write.csv> <copy_fetch.csv> <copy_write.csv>
         <kernel-name-substring> <copy-bytes> <command...> > profiles/<name>_traffic.txt
 
+  python -m paper_2608_22646_amd.profsum util <counters.csv> <compute-units> <xcds> <command...> > profiles/<name>_util.txt
+
 The traffic summary scales each counter (KiB per dispatch) by the ratio of the
 known traffic of a plain copy kernel to what the same counter reads for it.
+The utilisation summary reads one pass of GRBM_GUI_ACTIVE,
+SQ_VALU_MFMA_BUSY_CYCLES, TA_TA_BUSY_sum, SQ_WAIT_INST_ANY and SQ_WAVE_CYCLES
+and gives, per kernel, the clock (busy cycles over the dispatch's duration;
+GRBM_GUI_ACTIVE is summed over the XCDs), the MFMA busy fraction (per SIMD,
+four per compute unit), the texture-address busy fraction (per compute unit)
+and the waves' share of cycles spent waiting.
 """
 import csv
 import hashlib
@@ -68,10 +76,45 @@ def traffic(fetch, write, cfetch, cwrite, substr, copy_bytes, command):
     print(f"{name}_source_sha256={sha}")
 
 
+def util(path, cus, xcds, command):
+    import collections
+    import statistics
+    keys = ("gemm_wd_kernel", "gemm_bf16_kernel", "gemm_rows_kernel", "attn_", "head_")
+    per = collections.defaultdict(lambda: collections.defaultdict(list))
+    dur = collections.defaultdict(dict)
+    for r in csv.DictReader(open(path)):
+        name = r["Kernel_Name"]
+        if not any(k in name for k in keys):
+            continue
+        k = short(name, 400).split("(")[0]
+        per[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        dur[k][r.get("Dispatch_Id", len(dur[k]))] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    print(f"# MFMA and texture-address utilisation per kernel from one rocprofv3 --pmc pass\n# command: {command}")
+    print(f"# per dispatch, with cycles = GRBM_GUI_ACTIVE / {xcds} XCDs: clock = cycles / duration; mfma_busy = "
+          f"SQ_VALU_MFMA_BUSY_CYCLES / (cycles x {cus} CUs x 4 SIMDs); ta_busy = TA_TA_BUSY_sum / (cycles x {cus}); "
+          f"wait = SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES\n")
+    print(f"{'dispatches':>10} {'us':>8} {'GHz':>6} {'mfma_busy':>10} {'ta_busy':>8} {'wait':>6}  kernel")
+    rows = []
+    for k, c in per.items():
+        if not all(n in c for n in ("GRBM_GUI_ACTIVE", "SQ_VALU_MFMA_BUSY_CYCLES", "TA_TA_BUSY_sum",
+                                    "SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES")):
+            continue
+        mean = {n: sum(v) / len(v) for n, v in c.items()}
+        us = statistics.median(dur[k].values())
+        cyc = mean["GRBM_GUI_ACTIVE"] / xcds
+        rows.append((len(dur[k]) * us, len(dur[k]), us, cyc / (us * 1e3),
+                     mean["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * cus * 4), mean["TA_TA_BUSY_sum"] / (cyc * cus),
+                     mean["SQ_WAIT_INST_ANY"] / mean["SQ_WAVE_CYCLES"], k))
+    for _, n, us, ghz, mf, ta, wt, k in sorted(rows, reverse=True):
+        print(f"{n:10d} {us:8.1f} {ghz:6.2f} {mf:10.3f} {ta:8.3f} {wt:6.3f}  {short(k)}")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
         stats(sys.argv[2], " ".join(sys.argv[3:]))
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:6], sys.argv[6], int(sys.argv[7]), " ".join(sys.argv[8:]))
+    elif sys.argv[1] == "util":
+        util(sys.argv[2], int(sys.argv[3]), int(sys.argv[4]), " ".join(sys.argv[5:]))
     else:
         raise SystemExit(__doc__)
