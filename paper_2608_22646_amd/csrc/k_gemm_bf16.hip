@@ -1204,7 +1204,7 @@ __global__ void __launch_bounds__(256, 1) gemm_wd_kernel(GemmArgs g) {
     for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int ii = 0; ii < TI; ++ii) {
-        if (own_rows(ii) || (!SPLIT_ROWS && kg == 0)) continue;
+        if (own_rows(ii)) continue;  // the share this wave hands over
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           xa[((j * TI + ii) * 4 + q) * 64] =
