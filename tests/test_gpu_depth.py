@@ -5,7 +5,9 @@ input (prompt set 0 + the generation length of masks), after 1, 2, 4, 8, 16
 layers and the last (32 / 28).  The batch-8 LLaDA-8B workload (8 x 1024
 tokens: the large-row GEMM tiles, batched attention and the many-row LM head)
 runs its whole batch on the GPU; the oracle follows its sequence 5 (sequences
-of a batch do not interact).
+of a batch do not interact).  The batch-1 workloads run twice: on the plain
+weights (the LDS-staged GEMM tiles) and with the packed weight copies the bench
+decodes with (the register-direct tiles at these row counts).
 
 Two correct float32 accumulation orders of a bf16 model drift apart by bf16
 rounding flips that later layers carry forward; the oracle's own float32 and
@@ -54,8 +56,9 @@ def bars(drift, depth):
     return 2.0 * logit, max(2e-2, 2.0 * conf)
 
 
-@pytest.mark.parametrize("name", sorted(CASES))
-def test_forward_against_oracle_by_depth(name):
+@pytest.mark.parametrize("name,packed", [("dream_b1", False), ("dream_b1", True), ("llada_b1", False),
+                                         ("llada_b1", True), ("llada_b8", False)])
+def test_forward_against_oracle_by_depth(name, packed):
     drift, DEPTHS, seq = drift_table(name), CASES[name][1], CASES[name][2]
     wl = synth.WORKLOADS[name]
     cfg = wl.model
@@ -64,6 +67,8 @@ def test_forward_against_oracle_by_depth(name):
     say(f"{name} depth parity: weights")
     w = synth.make_weights(cfg, "cuda")
     model = B.Model(cfg, w)
+    if packed:
+        model.pack_weights()
     x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((Bn, G), cfg.mask_id)], axis=1)
     ws = model.workspace(Bn, L, bl)
     # layer calls (rows 0) and head calls (rows bl) share h and the RoPE tables
@@ -84,7 +89,7 @@ def test_forward_against_oracle_by_depth(name):
         depth = l + 1
         if depth not in DEPTHS:
             continue
-        say(f"{name} depth {depth}: head")
+        say(f"{name}{' packed' if packed else ''} depth {depth}: head")
         conf_g, arg_g, lg_g = model.head(Bn, L, P, bl, ws, logits=True)
         torch.cuda.synchronize()
         lg_ref, _ = of.lm_head(cfg, h[0, rows, :], final_norm, lm, "bf16")
