@@ -46,3 +46,27 @@ def test_work_per_forward_matches_the_scope_table(name):
 def test_traffic_is_reported_only_for_the_workload_its_counters_cover():
     for kernel in bench.TRAFFIC:
         assert bench.measured_traffic("dream_b1", kernel) is None
+
+
+def test_profile_utilisation_summary(tmp_path, capsys):
+    """profsum util on a hand-made counter CSV: one kernel, two dispatches of
+    10 us; 8 XCDs x 20000 busy cycles (2.0 GHz), the MFMA busy on half of the
+    1024 SIMDs' cycles, the texture-address units 3/4 busy, waves waiting a
+    third of their cycles."""
+    from paper_2608_22646_amd import profsum
+    cyc = 20000
+    vals = {"GRBM_GUI_ACTIVE": 8 * cyc, "SQ_VALU_MFMA_BUSY_CYCLES": 0.5 * cyc * 256 * 4,
+            "TA_TA_BUSY_sum": 0.75 * cyc * 256, "SQ_WAIT_INST_ANY": 100.0, "SQ_WAVE_CYCLES": 300.0}
+    lines = ["Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value,Start_Timestamp,End_Timestamp"]
+    for d in (1, 2):
+        for k, v in vals.items():
+            lines.append(f'{d},"void dllm::(anonymous namespace)::gemm_wd_kernel<X, 2>(dllm::GemmArgs)",{k},{v},'
+                         f'{1000000 * d},{1000000 * d + 10000}')
+    path = tmp_path / "c.csv"
+    path.write_text("\n".join(lines) + "\n")
+    profsum.util(str(path), 256, 8, "cmd")
+    row = [ln for ln in capsys.readouterr().out.splitlines() if "gemm_wd_kernel<X, 2>" in ln]
+    assert len(row) == 1
+    n, us, ghz, mf, ta, wt = row[0].split()[:6]
+    assert (int(n), float(us), float(ghz)) == (2, 10.0, 2.0)
+    assert (float(mf), float(ta), float(wt)) == (0.5, 0.75, 0.333)
