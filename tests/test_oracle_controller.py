@@ -220,7 +220,10 @@ def test_nan_confidence_never_passes_a_threshold():
 
 # ---------------------------------------------------------------- invariants
 def _check_invariants(stt, trace, p, G, P):
-    """Invariants any controller run must satisfy (spec list + recurrences)."""
+    """Invariants any controller run must satisfy: committed tokens are never
+    re-masked, every block ends with no mask left, no token exceeds its step
+    budget, the block-end threshold never rises over blocks; plus the
+    recurrences the decode's records obey."""
     bl, T = p.block_len, p.T
     B = stt.x.shape[0]
     # no mask left at the end; prompt untouched; every token committed once
