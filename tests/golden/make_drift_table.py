@@ -1,5 +1,6 @@
 """Writes tests/golden/bf16_drift_llada.json (bf16_drift_dream.json with
---workload dream_b1, bf16_drift_llada_b8.json with --workload llada_b8): how
+--workload dream_b1, bf16_drift_llada_b8.json with --workload llada_b8,
+bf16_drift_dream_long.json with --workload dream_long): how
 far the oracle's own bf16 forward moves between float32 and float64
 accumulation, by depth, at the LLaDA-8B (Dream-7B) shape.
 
@@ -24,6 +25,7 @@ the seeded input generators.
   python tests/golden/make_drift_table.py [--workload llada_b1] [--depths 1,2,4,8,16,32]
   python tests/golden/make_drift_table.py --workload dream_b1 --depths 1,2,4,8,16,28
   python tests/golden/make_drift_table.py --workload llada_b8
+  python tests/golden/make_drift_table.py --workload dream_long --depths 1,2
 """
 import argparse
 import json
@@ -43,13 +45,15 @@ from paper_2608_22646_amd import synth  # noqa: E402
 
 OUTS = {"llada_b1": os.path.join(HERE, "bf16_drift_llada.json"),
         "dream_b1": os.path.join(HERE, "bf16_drift_dream.json"),
-        "llada_b8": os.path.join(HERE, "bf16_drift_llada_b8.json")}
-SEQ = {"llada_b1": 0, "dream_b1": 0, "llada_b8": 5}  # the sequence of the batch the table follows
+        "llada_b8": os.path.join(HERE, "bf16_drift_llada_b8.json"),
+        "dream_long": os.path.join(HERE, "bf16_drift_dream_long.json")}
+SEQ = {"llada_b1": 0, "dream_b1": 0, "llada_b8": 5, "dream_long": 0}  # the sequence of the batch the table follows
 OUT = OUTS["llada_b1"]
 MODES = ("bf16", "bf16_f64acc")
+DEFAULT_DEPTHS = "1,2,4,8,16,32"
 
 
-def drift(depths, log=print, workload="llada_b1"):
+def drift(depths, log=print, workload="llada_b1", checkpoint=None):
     wl = synth.WORKLOADS[workload]
     cfg = wl.model
     P, G, bl = wl.prompt_len, wl.gen_len, wl.block_len
@@ -91,29 +95,35 @@ def drift(depths, log=print, workload="llada_b1"):
         }
         out.append(rec)
         log(f"[drift] {time.time() - t0:.0f}s " + json.dumps(rec))
+        if checkpoint:
+            checkpoint(out)
     return out
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="llada_b1", choices=sorted(OUTS))
-    ap.add_argument("--depths", default="1,2,4,8,16,32")
+    ap.add_argument("--depths", default=DEFAULT_DEPTHS)
     a = ap.parse_args()
     depths = sorted({int(v) for v in a.depths.split(",")})
-    table = drift(depths, log=lambda s: print(s, flush=True), workload=a.workload)
     wl = synth.WORKLOADS[a.workload]
-    shape = {"llada_b1": "LLaDA-8B", "dream_b1": "Dream-7B", "llada_b8": "LLaDA-8B"}[a.workload]
-    doc = {
-        "what": ("max |difference| between the oracle's bf16-model forward with float32 and with float64 "
-                 f"accumulation (same bf16 rounding points), {shape} shape, sequence {SEQ[a.workload]} of prompt set 0 + "
-                 f"{wl.gen_len} masks, "
-                 "first block's 32 rows; logits exclude the mask column"),
-        "generator": "tests/golden/make_drift_table.py" + ("" if a.workload == "llada_b1" else
-                                                            f" --workload {a.workload}"),
-        "rows": table,
-    }
-    with open(OUTS[a.workload], "w") as f:
-        json.dump(doc, f, indent=1)
+
+    def write(table):  # after every depth, so that a long run keeps what it has measured
+        doc = {
+            "what": ("max |difference| between the oracle's bf16-model forward with float32 and with float64 "
+                     f"accumulation (same bf16 rounding points), {shape} shape, sequence {SEQ[a.workload]} of prompt "
+                     f"set 0 + {wl.gen_len} masks, first block's 32 rows; logits exclude the mask column"),
+            "generator": "tests/golden/make_drift_table.py" + ("" if a.workload == "llada_b1" else
+                                                                f" --workload {a.workload}")
+                         + ("" if a.depths == DEFAULT_DEPTHS else f" --depths {a.depths}"),
+            "rows": table,
+        }
+        with open(OUTS[a.workload], "w") as f:
+            json.dump(doc, f, indent=1)
+
+    shape = {"llada_b1": "LLaDA-8B", "dream_b1": "Dream-7B", "llada_b8": "LLaDA-8B", "dream_long": "Dream-7B"}[
+        a.workload]
+    drift(depths, log=lambda s: print(s, flush=True), workload=a.workload, checkpoint=write)
     print(OUTS[a.workload])
 
 

@@ -5,7 +5,9 @@ input (prompt set 0 + the generation length of masks), after 1, 2, 4, 8, 16
 layers and the last (32 / 28).  The batch-8 LLaDA-8B workload (8 x 1024
 tokens: the large-row GEMM tiles, batched attention and the many-row LM head)
 runs its whole batch on the GPU; the oracle follows its sequence 5 (sequences
-of a batch do not interact).  The batch-1 workloads run twice: on the plain
+of a batch do not interact).  The Dream-7B long-context workload (8448 tokens,
+where the oracle's forward takes minutes per layer) is compared after its
+first and second layers.  The batch-1 workloads run twice: on the plain
 weights (the LDS-staged GEMM tiles) and with the packed weight copies the bench
 decodes with (the register-direct tiles at these row counts).
 
@@ -41,7 +43,8 @@ pytestmark = pytest.mark.gpu
 HERE = os.path.dirname(os.path.abspath(__file__))
 CASES = {"llada_b1": ("bf16_drift_llada.json", (1, 2, 4, 8, 16, 32), 0),
          "dream_b1": ("bf16_drift_dream.json", (1, 2, 4, 8, 16, 28), 0),
-         "llada_b8": ("bf16_drift_llada_b8.json", (1, 2, 4, 8, 16, 32), 5)}
+         "llada_b8": ("bf16_drift_llada_b8.json", (1, 2, 4, 8, 16, 32), 5),
+         "dream_long": ("bf16_drift_dream_long.json", (1, 2), 0)}
 
 
 def drift_table(name):
@@ -57,7 +60,7 @@ def bars(drift, depth):
 
 
 @pytest.mark.parametrize("name,packed", [("dream_b1", False), ("dream_b1", True), ("llada_b1", False),
-                                         ("llada_b1", True), ("llada_b8", False)])
+                                         ("llada_b1", True), ("llada_b8", False), ("dream_long", False)])
 def test_forward_against_oracle_by_depth(name, packed):
     drift, DEPTHS, seq = drift_table(name), CASES[name][1], CASES[name][2]
     wl = synth.WORKLOADS[name]
@@ -81,7 +84,7 @@ def test_forward_against_oracle_by_depth(name, packed):
     final_norm, lm = to_np(w[-2]), to_np(w[-1])
     rows = np.arange(P, P + bl)
     report = []
-    for l in range(cfg.n_layers):
+    for l in range(max(DEPTHS)):
         model.layer(l, 2, Bn, L, ws)
         lw = [to_np(t) for t in w[1 + 9 * l: 10 + 9 * l]]
         h = of.layer(cfg, lw, h, cos, sin, "bf16")
