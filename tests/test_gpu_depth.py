@@ -44,7 +44,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CASES = {"llada_b1": ("bf16_drift_llada.json", (1, 2, 4, 8, 16, 32), 0),
          "dream_b1": ("bf16_drift_dream.json", (1, 2, 4, 8, 16, 28), 0),
          "llada_b8": ("bf16_drift_llada_b8.json", (1, 2, 4, 8, 16, 32), 5),
-         "dream_long": ("bf16_drift_dream_long.json", (1, 2), 0)}
+         "dream_long": ("bf16_drift_dream_long.json", (1, 2, 4, 8), 0)}
 
 
 def drift_table(name):
