@@ -5,9 +5,8 @@ input (prompt set 0 + the generation length of masks), after 1, 2, 4, 8, 16
 layers and the last (32 / 28).  The batch-8 LLaDA-8B workload (8 x 1024
 tokens: the large-row GEMM tiles, batched attention and the many-row LM head)
 runs its whole batch on the GPU; the oracle follows its sequence 5 (sequences
-of a batch do not interact).  The Dream-7B long-context workload (8448 tokens,
-where the oracle's forward takes minutes per layer) is compared after its
-first and second layers.  The batch-1 workloads run twice: on the plain
+of a batch do not interact).  The Dream-7B long-context workload (8448 tokens)
+runs all 28 layers as well (about five minutes with the oracle beside it).  The batch-1 workloads run twice: on the plain
 weights (the LDS-staged GEMM tiles) and with the packed weight copies the bench
 decodes with (the register-direct tiles at these row counts).
 
@@ -44,7 +43,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CASES = {"llada_b1": ("bf16_drift_llada.json", (1, 2, 4, 8, 16, 32), 0),
          "dream_b1": ("bf16_drift_dream.json", (1, 2, 4, 8, 16, 28), 0),
          "llada_b8": ("bf16_drift_llada_b8.json", (1, 2, 4, 8, 16, 32), 5),
-         "dream_long": ("bf16_drift_dream_long.json", (1, 2, 4, 8), 0)}
+         "dream_long": ("bf16_drift_dream_long.json", (1, 2, 4, 8, 16, 28), 0)}
 
 
 def drift_table(name):
