@@ -6,14 +6,15 @@ layers and the last (32 / 28).  The batch-8 LLaDA-8B workload (8 x 1024
 tokens: the large-row GEMM tiles, batched attention and the many-row LM head)
 runs its whole batch on the GPU; the oracle follows its sequence 5 (sequences
 of a batch do not interact).  The Dream-7B long-context workload (8448 tokens)
-runs all 28 layers as well (about five minutes with the oracle beside it).  The batch-1 workloads run twice: on the plain
-weights (the LDS-staged GEMM tiles) and with the packed weight copies the bench
-decodes with (the register-direct tiles at these row counts).
+runs all 28 layers as well (about five minutes with the oracle beside it).
+The batch-1 workloads run twice: on the plain weights (the LDS-staged GEMM
+tiles) and with the packed weight copies the bench decodes with (the
+register-direct tiles at these row counts).
 
 Two correct float32 accumulation orders of a bf16 model drift apart by bf16
 rounding flips that later layers carry forward; the oracle's own float32 and
 float64 runs of each model and input differ by the amounts in
-tests/golden/bf16_drift_llada.json and bf16_drift_dream.json (written by
+tests/golden/bf16_drift_*.json (one table per workload, written by
 make_drift_table.py from the oracle alone).  The bars are derived from that table: the
 GPU may differ from the float32 oracle by at most twice the oracle's own
 spread (logits), and by at most 2e-2 or twice the table's spread, whichever is
