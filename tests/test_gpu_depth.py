@@ -6,7 +6,7 @@ layers and the last (32 / 28).  The batch-8 LLaDA-8B workload (8 x 1024
 tokens: the large-row GEMM tiles, batched attention and the many-row LM head)
 runs its whole batch on the GPU; the oracle follows its sequence 5 (sequences
 of a batch do not interact).  The Dream-7B long-context workload (8448 tokens)
-runs all 28 layers as well (about five minutes with the oracle beside it).
+runs all 28 layers as well, in four tests of at most eight layers.
 The batch-1 workloads run twice: on the plain weights (the LDS-staged GEMM
 tiles) and with the packed weight copies the bench decodes with (the
 register-direct tiles at these row counts).
@@ -59,56 +59,100 @@ def bars(drift, depth):
     return 2.0 * logit, max(2e-2, 2.0 * conf)
 
 
+class DepthRun:
+    """One workload's forward on the GPU (layer calls into one workspace) and
+    the oracle's float32 forward of the followed sequence, advanced together;
+    the head is compared at every depth of the workload's table."""
+
+    def __init__(self, name, packed):
+        self.name, self.packed = name, packed
+        self.drift, self.depths, self.seq = drift_table(name), CASES[name][1], CASES[name][2]
+        wl = synth.WORKLOADS[name]
+        self.cfg = cfg = wl.model
+        self.Bn, self.P, G, self.bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
+        self.L = L = self.P + G
+        say(f"{name} depth parity: weights")
+        self.w = w = synth.make_weights(cfg, "cuda")
+        self.model = B.Model(cfg, w)
+        if packed:
+            self.model.pack_weights()
+        x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((self.Bn, G), cfg.mask_id)],
+                           axis=1)
+        self.ws = self.model.workspace(self.Bn, L, self.bl)
+        # layer calls (rows 0) and head calls (rows bl) share h and the RoPE tables
+        l0, lb = self.model.layout(self.Bn, L, 0), self.model.layout(self.Bn, L, self.bl)
+        assert [getattr(l0, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")] == \
+            [getattr(lb, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")]
+        self.model.embed(torch.from_numpy(x.astype(np.int32)).cuda(), self.ws)
+        self.h = to_np(w[0], np.float32)[x[self.seq:self.seq + 1]].astype(np.float64)
+        self.cos, self.sin = of.rope_tables(L, cfg.head_dim, cfg.rope_base)
+        self.final_norm, self.lm = to_np(w[-2]), to_np(w[-1])
+        self.rows = np.arange(self.P, self.P + self.bl)
+        self.layers_done = 0
+        self.report = []
+
+    def advance(self, to_depth):
+        cfg, seq = self.cfg, self.seq
+        for l in range(self.layers_done, to_depth):
+            self.model.layer(l, 2, self.Bn, self.L, self.ws)
+            lw = [to_np(t) for t in self.w[1 + 9 * l: 10 + 9 * l]]
+            self.h = of.layer(cfg, lw, self.h, self.cos, self.sin, "bf16")
+            del lw
+            self.layers_done = depth = l + 1
+            if depth not in self.depths:
+                continue
+            say(f"{self.name}{' packed' if self.packed else ''} depth {depth}: head")
+            conf_g, arg_g, lg_g = self.model.head(self.Bn, self.L, self.P, self.bl, self.ws, logits=True)
+            torch.cuda.synchronize()
+            lg_ref, _ = of.lm_head(cfg, self.h[0, self.rows, :], self.final_norm, self.lm, "bf16")
+            conf_ref, arg_ref = ov.confidence_argmax(lg_ref, cfg.mask_id)
+            lg = to_np(lg_g[seq], np.float64)
+            err = np.abs(lg - lg_ref)
+            err[:, cfg.mask_id] = 0
+            cerr = np.abs(to_np(conf_g[seq], np.float64) - conf_ref).max()
+            bar_l, bar_c = bars(self.drift, depth)
+            diff = arg_g[seq].cpu().numpy() != arg_ref
+            gap = ov.top2_gap(lg_ref, cfg.mask_id)
+            rec = dict(depth=depth, logit_err=float(err.max()), logit_bar=bar_l, conf_err=float(cerr), conf_bar=bar_c,
+                       argmax_diff=int(diff.sum()))
+            self.report.append(rec)
+            say("  " + json.dumps(rec))
+            assert err.max() <= bar_l, rec
+            assert cerr <= bar_c, rec
+            assert np.all(gap[diff] <= 2 * err.max()), rec
+
+
 @pytest.mark.parametrize("name,packed", [("dream_b1", False), ("dream_b1", True), ("llada_b1", False),
-                                         ("llada_b1", True), ("llada_b8", False), ("dream_long", False)])
+                                         ("llada_b1", True), ("llada_b8", False)])
 def test_forward_against_oracle_by_depth(name, packed):
-    drift, DEPTHS, seq = drift_table(name), CASES[name][1], CASES[name][2]
-    wl = synth.WORKLOADS[name]
-    cfg = wl.model
-    Bn, P, G, bl = wl.batch, wl.prompt_len, wl.gen_len, wl.block_len
-    L = P + G
-    say(f"{name} depth parity: weights")
-    w = synth.make_weights(cfg, "cuda")
-    model = B.Model(cfg, w)
-    if packed:
-        model.pack_weights()
-    x = np.concatenate([synth.make_prompts(wl).numpy().astype(np.int64), np.full((Bn, G), cfg.mask_id)], axis=1)
-    ws = model.workspace(Bn, L, bl)
-    # layer calls (rows 0) and head calls (rows bl) share h and the RoPE tables
-    l0, lb = model.layout(Bn, L, 0), model.layout(Bn, L, bl)
-    assert [getattr(l0, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")] == \
-        [getattr(lb, f) for f in ("h", "a_attn", "q", "k", "vt", "attn", "a_mlp", "u")]
-    model.embed(torch.from_numpy(x.astype(np.int32)).cuda(), ws)
-    h = to_np(w[0], np.float32)[x[seq:seq + 1]].astype(np.float64)
-    cos, sin = of.rope_tables(L, cfg.head_dim, cfg.rope_base)
-    final_norm, lm = to_np(w[-2]), to_np(w[-1])
-    rows = np.arange(P, P + bl)
-    report = []
-    for l in range(max(DEPTHS)):
-        model.layer(l, 2, Bn, L, ws)
-        lw = [to_np(t) for t in w[1 + 9 * l: 10 + 9 * l]]
-        h = of.layer(cfg, lw, h, cos, sin, "bf16")
-        del lw
-        depth = l + 1
-        if depth not in DEPTHS:
-            continue
-        say(f"{name}{' packed' if packed else ''} depth {depth}: head")
-        conf_g, arg_g, lg_g = model.head(Bn, L, P, bl, ws, logits=True)
-        torch.cuda.synchronize()
-        lg_ref, _ = of.lm_head(cfg, h[0, rows, :], final_norm, lm, "bf16")
-        conf_ref, arg_ref = ov.confidence_argmax(lg_ref, cfg.mask_id)
-        lg = to_np(lg_g[seq], np.float64)
-        err = np.abs(lg - lg_ref)
-        err[:, cfg.mask_id] = 0
-        cerr = np.abs(to_np(conf_g[seq], np.float64) - conf_ref).max()
-        bar_l, bar_c = bars(drift, depth)
-        diff = arg_g[seq].cpu().numpy() != arg_ref
-        gap = ov.top2_gap(lg_ref, cfg.mask_id)
-        rec = dict(depth=depth, logit_err=float(err.max()), logit_bar=bar_l, conf_err=float(cerr), conf_bar=bar_c,
-                   argmax_diff=int(diff.sum()))
-        report.append(rec)
-        say("  " + json.dumps(rec))
-        assert err.max() <= bar_l, rec
-        assert cerr <= bar_c, rec
-        assert np.all(gap[diff] <= 2 * err.max()), rec
-    assert [r["depth"] for r in report] == list(DEPTHS)
+    run = DepthRun(name, packed)
+    run.advance(max(run.depths))
+    assert [r["depth"] for r in run.report] == list(run.depths)
+
+
+# The long-context forward in segments of at most eight layers (the oracle
+# takes ~11 s per layer there), each its own test, so that every test ends
+# within two minutes; a segment whose predecessor did not finish is skipped.
+LONG_SEGMENTS = [8, 16, 22, 28]
+
+
+@pytest.fixture(scope="module")
+def long_run():
+    state = {}
+    yield state
+    state.clear()
+
+
+@pytest.mark.parametrize("to_depth", LONG_SEGMENTS)
+def test_long_context_forward_against_oracle_by_depth(long_run, to_depth):
+    k = LONG_SEGMENTS.index(to_depth)
+    if k == 0:
+        long_run["run"] = DepthRun("dream_long", False)
+    elif long_run.get("done") != LONG_SEGMENTS[k - 1]:
+        pytest.skip("the previous segment of the long-context forward did not finish")
+    run = long_run["run"]
+    run.advance(to_depth)
+    long_run["done"] = to_depth
+    if to_depth == LONG_SEGMENTS[-1]:
+        assert [r["depth"] for r in run.report] == list(run.depths)
+        long_run.clear()
